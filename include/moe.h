@@ -1,0 +1,229 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) MoE-layer library.
+ *
+ * One GPU's share of an expert-parallel MoE layer (paper section 2.1, Fig 3):
+ * top-k routing, dispatch of token rows into expert-contiguous buffers, a
+ * per-expert SwiGLU grouped GEMM (GEMM0 = gate and up projection, SiLU times
+ * up, GEMM1 = down projection) and the weighted combine.  The forward pass is
+ * one persistent megakernel whose workers are split at run time into
+ * data-movement workers (dispatch and combine) and MFMA compute workers
+ * (section 3, section 4); an in-kernel cost model (Eq 1-16) picks the split c,
+ * the chunk count K and the steal count from the routing histogram.
+ *
+ * On one GPU the cross-GPU dispatch and combine become HBM-to-HBM copies:
+ * rows of source rank r live in the staging region x[r*Tr .. (r+1)*Tr) and
+ * their outputs go to y[r*Tr .. (r+1)*Tr).  This GPU is EP rank 0 and holds
+ * the local experts [first_local_expert, first_local_expert + n_local_experts).
+ *
+ * Conventions for every entry point
+ *  - bf16 tensors are passed as uint16_t bit patterns, row-major, densely
+ *    packed (no strides), in device memory.
+ *  - Every pointer argument is a device pointer unless marked "host".
+ *  - The caller owns all memory: inputs, outputs, packed weights and the
+ *    workspace.  The library never allocates or frees device memory; the
+ *    handle holds host state only.
+ *  - Streams are hipStream_t passed as void* (NULL = the null stream).  Calls
+ *    are asynchronous on that stream unless documented to synchronise.
+ *  - A handle is used from one host thread and one stream at a time.
+ *  - Argument errors are detected on the host before anything is launched
+ *    and return MOE_ERR_INVALID_ARG (nothing is enqueued).  Errors detected on
+ *    the device (out-of-range routing ids, a wait that timed out) are latched
+ *    in a device error word and returned by moe_sync_status and by the next
+ *    synchronising call.
+ *  - moe_last_error() returns a thread-local message for the last failure.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct moe_handle moe_handle;
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1, /* bad argument, detected on the host */
+  MOE_ERR_UNSUPPORTED = -2, /* valid but outside what the kernels support */
+  MOE_ERR_HIP = -3,         /* a HIP runtime call failed */
+  MOE_ERR_TIMEOUT = -4,     /* a device-side wait exceeded its time limit */
+  MOE_ERR_ROUTING = -5,     /* routing ids out of range or repeated in a row */
+  MOE_ERR_STATE = -6        /* call order violated (e.g. forward before tables) */
+} moe_status;
+
+typedef enum {
+  MOE_MODE_DYNAMIC = 0, /* megakernel, plan from the in-kernel cost model */
+  MOE_MODE_STATIC = 1,  /* megakernel, fixed split c = static_c, K = 1, no steal,
+                           combine by movement workers only */
+  MOE_MODE_SERIAL = 2   /* four kernels in sequence, each on every CU:
+                           dispatch, GEMM0 + SiLU*up, GEMM1, combine */
+} moe_mode;
+
+/* Problem shape (section 3.1 notation: H hidden, I = ffn, E experts, top-k). */
+typedef struct {
+  int32_t n_src_ranks;        /* R >= 1 source ranks (staging regions) */
+  int32_t tokens_per_rank;    /* Tr >= 1; T = R*Tr tokens in total */
+  int32_t hidden;             /* H, multiple of 64, <= 16384 */
+  int32_t ffn;                /* I (F), multiple of 64, <= 32768 */
+  int32_t n_experts;          /* E, 1..512 */
+  int32_t top_k;              /* k, 1..min(E, 8) */
+  int32_t n_local_experts;    /* E_l, 1..128 */
+  int32_t first_local_expert; /* e0, 0 <= e0 <= E - E_l */
+  int32_t n_shared_experts;   /* S, 0..8, always-on experts applied to rank-0 tokens */
+  int32_t n_workers;          /* persistent workgroups N; 0 = one per CU */
+} moe_config;
+
+#define MOE_CALIB_MAX_C 32
+#define MOE_CALIB_MAX_K 4
+
+/* Hardware input of the cost model (section 3, Fig 4a/b, Fig 7a).
+ * For grid point i: c[i] movement workers move bw_bytes_per_s[i] payload
+ * bytes/s (BW(c)) while N - c[i] compute workers reach comp_flop_per_s[i]
+ * (TFLOPS(N - c)).  eff_chunk[j] is the chunked/unchunked GEMM throughput
+ * ratio at k_chunks[j] chunks; alpha is the tile-level overlap ratio (Eq 6).
+ * literal_volumes = 1 uses the printed remote-only volumes of Eq 2-3;
+ * 0 (default) counts every moved row, since on one GPU rank 0's rows also go
+ * through the movement workers. */
+typedef struct {
+  int32_t n_c;
+  int32_t c[MOE_CALIB_MAX_C];            /* ascending, 1 <= c < N */
+  double bw_bytes_per_s[MOE_CALIB_MAX_C];
+  double comp_flop_per_s[MOE_CALIB_MAX_C];
+  int32_t n_k;
+  int32_t k_chunks[MOE_CALIB_MAX_K];     /* ascending, each in {1,2,4,8} */
+  double eff_chunk[MOE_CALIB_MAX_K];     /* in (0, 1] */
+  double alpha;                          /* in [0, 1] */
+  int32_t literal_volumes;
+  int32_t static_c;                      /* split used by MOE_MODE_STATIC */
+} moe_calib;
+
+/* Execution plan (section 3.3): the split, the chunk count and the steal count. */
+typedef struct {
+  int32_t c;          /* movement workers (section 3.1) */
+  int32_t K;          /* chunk count of the chunk pipeline (section 3.2.1) */
+  int32_t n_steal;    /* GEMM tiles each movement worker steals (Eq 14) */
+  int32_t final_all;  /* 1: every worker joins the combine once the compute
+                         queue is empty (section 4); 0: movement workers only */
+  double t_pred_s;    /* T_total(c, K) predicted by Eq 15; 0 for forced plans */
+} moe_plan;
+
+/* Byte offsets of the workspace regions (for inspection by tests). */
+typedef struct {
+  size_t total;
+  size_t slot;        /* int32 [T*k]: slot of pair (g,j) or -1 */
+  size_t inv;         /* int32 [T*min(k,E_l)]: g*k+j of each slot */
+  size_t first_slot;  /* int32 [T] */
+  size_t off;         /* int32 [E_l+1] */
+  size_t sub_off;     /* int32 [4][E_l][9]: chunk offsets for K = 1,2,4,8 */
+  size_t cnt_rank;    /* int32 [E_l][R] */
+  size_t uniq;        /* int32 [R] */
+  size_t stats;       /* int32 [16]: X, X_local, X_in, U_local, U_in, ... */
+  size_t plan;        /* moe_plan of the last megakernel launch */
+  size_t err;         /* int32 device error word */
+  size_t A;           /* bf16 [X_max + pad][H]: dispatched rows */
+  size_t Hbuf;        /* bf16 [X_max + S*Tr + pad][F]: SiLU(gate)*up */
+  size_t O;           /* bf16 [X_max + S*Tr + pad][H]: expert outputs */
+} moe_ws_layout;
+
+/* Creates a handle.  cfg (host) is copied; calib (host) may be NULL for the
+ * built-in MI355X calibration.  Validates the shape; does not touch the GPU
+ * beyond querying the current device's CU count.  *out receives the handle. */
+moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** out);
+
+/* Releases the handle (host memory only).  NULL is accepted. */
+moe_status moe_destroy(moe_handle* h);
+
+/* Thread-local text of the last error returned on this thread ("" if none). */
+const char* moe_last_error(void);
+
+/* Replaces the calibration table (host struct, copied; validated against N).
+ * The table lives in the workspace: if one is bound it is updated with a
+ * synchronous copy, so call this between launches, not while one runs. */
+moe_status moe_set_calib(moe_handle* h, const moe_calib* calib);
+moe_status moe_get_calib(const moe_handle* h, moe_calib* out);
+
+/* Time limit of every device-side wait of the megakernel (a wait for
+ * dispatched rows, finished GEMM tiles or a finished chunk).  When a wait
+ * exceeds it the workgroup latches MOE_ERR_TIMEOUT, raises an abort word that
+ * makes every other wait give up, and the launch drains and exits.
+ * inject_stall != 0 is a test hook that makes every wait target unreachable,
+ * so the next megakernel launch exercises this path and exits after ~ms.
+ * Default: 2000 ms, no injection. */
+moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
+
+/* Workspace size in bytes and its region offsets (host out-parameters). */
+moe_status moe_workspace_size(const moe_handle* h, size_t* bytes);
+moe_status moe_workspace_layout(const moe_handle* h, moe_ws_layout* out);
+
+/* Binds a caller-owned device workspace of at least moe_workspace_size bytes,
+ * 256-byte aligned, and initialises its control words on `stream`.  The
+ * workspace must stay alive and unused by others while the handle uses it. */
+moe_status moe_set_workspace(moe_handle* h, void* ws, size_t bytes, void* stream);
+
+/* Size of the packed expert weights: (E_l + S) * 3 * H * F * 2 bytes. */
+moe_status moe_packed_weights_size(const moe_handle* h, size_t* bytes);
+
+/* Packs the expert weights into the GEMM operand layout (not part of the
+ * layer; done once).  w1, w3: bf16 [E_l][H][F] (gate, up), w2: bf16
+ * [E_l][F][H] (down); ws1, ws3, ws2 the same for the S shared experts (NULL
+ * when S = 0).  packed: device buffer of moe_packed_weights_size bytes. */
+moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w3,
+                            const uint16_t* w2, const uint16_t* ws1, const uint16_t* ws3,
+                            const uint16_t* ws2, void* packed, void* stream);
+
+/* Top-k routing (the routing that precedes the layer, section 4) followed by
+ * moe_build_tables.  x: bf16 [T][H] (rank r's rows at r*Tr); wg: bf16 [H][E];
+ * logit_bias: fp32 [E] added to the logits, or NULL.  Logits are accumulated
+ * in fp32 over ascending h (one accumulator per (token, expert)); the top_k
+ * largest logits are selected (ties -> smaller expert id), written in
+ * descending order to topk_idx int32 [T][k]; topk_w fp32 [T][k] receives the
+ * selected softmax probabilities divided by their sum.  top_k must equal the
+ * configured k. */
+moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg,
+                     const float* logit_bias, int32_t top_k, int32_t* topk_idx,
+                     float* topk_w, void* stream);
+
+/* Builds the routing tables of this GPU's share from topk_idx int32 [T][k]
+ * (section 3.1 descriptors and the dispatch permutation): per-(expert, rank)
+ * counts, unique-token counts, expert offsets, the slot of each local pair
+ * (slots ordered by local expert, then token), its inverse, each token's
+ * first slot and the chunk offsets for K = 1, 2, 4, 8.  Ids outside [0, E) or
+ * repeated within a row latch MOE_ERR_ROUTING and are treated as non-local. */
+moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream);
+
+/* The MoE layer (section 2.1 stages 1-5) on the tables built from topk_idx.
+ * x: bf16 [T][H] staging regions; topk_idx/topk_w: the routing result
+ * (topk_idx must be the array the current tables were built from: checked by
+ * address); packed: from moe_pack_weights; y: bf16 [T][H] output staging
+ * regions, y[g] = sum over local j of topk_w[g,j] * FFN(x[g]) (+ the shared
+ * experts for rank-0 tokens), 0 for tokens with no local expert.
+ * mode: a moe_mode.  forced: host plan overriding the cost model (c, K,
+ * n_steal, final_all) in the megakernel modes, or NULL. */
+moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx,
+                       const float* topk_w, const void* packed, uint16_t* y,
+                       int32_t mode, const moe_plan* forced, void* stream);
+
+/* Copies the plan of the last megakernel launch to *out (host).  Synchronises
+ * the stream. */
+moe_status moe_get_plan(moe_handle* h, moe_plan* out, void* stream);
+
+/* Reads and clears the device error word; synchronises the stream. */
+moe_status moe_sync_status(moe_handle* h, void* stream);
+
+/* The cost model alone, on the host, for given routing volumes (fp64, same
+ * operation order as the in-kernel prologue).  n_tiles[j]: GEMM tiles at
+ * k_chunks[j]. */
+moe_status moe_plan_host(const moe_handle* h, double w_comp, double w_dispatch,
+                         double w_combine, const int64_t* n_tiles, moe_plan* out);
+
+/* Tile geometry of the grouped GEMM: rows per tile (BM) and column tiles of
+ * GEMM0 / GEMM1 for this shape. */
+moe_status moe_tile_geometry(const moe_handle* h, int32_t* bm, int32_t* nt0, int32_t* nt1);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

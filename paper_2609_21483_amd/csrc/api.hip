@@ -1,0 +1,499 @@
+// Host side of the C ABI declared in include/moe.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "common.h"
+#include "kernels.h"
+
+using namespace moe;
+
+namespace {
+
+thread_local std::string g_err;
+
+moe_status fail(moe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(MOE_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+struct moe_handle {
+  moe_config cfg;
+  int N = 0;
+  int T = 0, xmax = 0, mt_max = 0, ctl_words = 0, nblk = 0, nseg = 0, nt0 = 0, nt1 = 0;
+  moe_calib calib{};
+  DevCalib dcal{};
+  moe_ws_layout lay{};
+  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_ctl[2] = {0, 0};
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  const int32_t* tables_from = nullptr;
+  unsigned long long launch_seq = 0;
+  long long timeout_ticks = 200000000LL;  // 2 s at 100 MHz
+  int inject_stall = 0;
+};
+
+namespace {
+
+moe_status validate_cfg(const moe_config* c) {
+  if (!c) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  if (c->n_src_ranks < 1 || c->n_src_ranks > 64) return fail(MOE_ERR_INVALID_ARG, "n_src_ranks must be in [1, 64]");
+  if (c->tokens_per_rank < 1) return fail(MOE_ERR_INVALID_ARG, "tokens_per_rank must be >= 1");
+  long long T = (long long)c->n_src_ranks * c->tokens_per_rank;
+  if (T > (1 << 22)) return fail(MOE_ERR_UNSUPPORTED, "T = %lld tokens exceeds 2^22", T);
+  if (c->hidden < 64 || c->hidden % 64 || c->hidden > 16384)
+    return fail(MOE_ERR_INVALID_ARG, "hidden must be a multiple of 64 in [64, 16384]");
+  if (c->ffn < 64 || c->ffn % 64 || c->ffn > 32768)
+    return fail(MOE_ERR_INVALID_ARG, "ffn must be a multiple of 64 in [64, 32768]");
+  if (c->n_experts < 1 || c->n_experts > MAX_E) return fail(MOE_ERR_INVALID_ARG, "n_experts must be in [1, %d]", MAX_E);
+  if (c->top_k < 1 || c->top_k > MAX_TOPK || c->top_k > c->n_experts)
+    return fail(MOE_ERR_INVALID_ARG, "top_k must be in [1, min(E, %d)]", MAX_TOPK);
+  if (c->n_local_experts < 1 || c->n_local_experts > 128)
+    return fail(MOE_ERR_INVALID_ARG, "n_local_experts must be in [1, 128]");
+  if (c->first_local_expert < 0 || c->first_local_expert + c->n_local_experts > c->n_experts)
+    return fail(MOE_ERR_INVALID_ARG, "local experts [e0, e0+E_l) must lie in [0, E)");
+  if (c->n_shared_experts < 0 || c->n_shared_experts > 8)
+    return fail(MOE_ERR_INVALID_ARG, "n_shared_experts must be in [0, 8]");
+  if (c->n_workers < 0) return fail(MOE_ERR_INVALID_ARG, "n_workers must be >= 0");
+  long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
+  if (xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM > (1LL << 31) / 2)
+    return fail(MOE_ERR_UNSUPPORTED, "too many routed rows");
+  return MOE_OK;
+}
+
+moe_status validate_calib(const moe_calib* k, int N) {
+  if (k->n_c < 1 || k->n_c > MOE_CALIB_MAX_C) return fail(MOE_ERR_INVALID_ARG, "calib n_c must be in [1, %d]", MOE_CALIB_MAX_C);
+  if (k->n_k < 1 || k->n_k > MOE_CALIB_MAX_K) return fail(MOE_ERR_INVALID_ARG, "calib n_k must be in [1, %d]", MOE_CALIB_MAX_K);
+  for (int i = 0; i < k->n_c; ++i) {
+    if (k->c[i] < 1 || k->c[i] >= N) return fail(MOE_ERR_INVALID_ARG, "calib c[%d] = %d outside [1, N-1], N = %d", i, k->c[i], N);
+    if (i && k->c[i] <= k->c[i - 1]) return fail(MOE_ERR_INVALID_ARG, "calib c must ascend");
+    if (!(k->bw_bytes_per_s[i] > 0) || !(k->comp_flop_per_s[i] > 0) || !std::isfinite(k->bw_bytes_per_s[i]) ||
+        !std::isfinite(k->comp_flop_per_s[i]))
+      return fail(MOE_ERR_INVALID_ARG, "calib throughputs must be positive and finite");
+  }
+  for (int j = 0; j < k->n_k; ++j) {
+    int K = k->k_chunks[j];
+    if (K != 1 && K != 2 && K != 4 && K != 8) return fail(MOE_ERR_INVALID_ARG, "calib K must be 1, 2, 4 or 8");
+    if (j && K <= k->k_chunks[j - 1]) return fail(MOE_ERR_INVALID_ARG, "calib K must ascend");
+    if (!(k->eff_chunk[j] > 0) || k->eff_chunk[j] > 1) return fail(MOE_ERR_INVALID_ARG, "eff_chunk must be in (0, 1]");
+  }
+  if (!(k->alpha >= 0 && k->alpha <= 1)) return fail(MOE_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+  if (k->static_c < 1 || k->static_c >= N) return fail(MOE_ERR_INVALID_ARG, "static_c must be in [1, N-1]");
+  return MOE_OK;
+}
+
+// Nominal MI355X curves used until a measured table is supplied.
+void default_calib(int N, moe_calib* k) {
+  memset(k, 0, sizeof *k);
+  int n = 0;
+  for (int c = 8; c <= 128 && c < N && n < MOE_CALIB_MAX_C; c += 8) {
+    k->c[n] = c;
+    k->bw_bytes_per_s[n] = std::min(40e9 * c, 5.0e12);
+    k->comp_flop_per_s[n] = 4.0e12 * (N - c);
+    ++n;
+  }
+  if (n == 0) {
+    k->c[0] = std::max(1, N / 4);
+    k->bw_bytes_per_s[0] = 40e9 * k->c[0];
+    k->comp_flop_per_s[0] = 4.0e12 * (N - k->c[0]);
+    n = 1;
+  }
+  k->n_c = n;
+  k->n_k = 4;
+  const int kk[4] = {1, 2, 4, 8};
+  const double eff[4] = {1.0, 0.93, 0.85, 0.73};
+  for (int j = 0; j < 4; ++j) { k->k_chunks[j] = kk[j]; k->eff_chunk[j] = eff[j]; }
+  k->alpha = 0.5;
+  k->literal_volumes = 0;
+  int sc = (int)std::lround(N * 20.0 / 132.0 / 8.0) * 8;  // 20 of 132 SMs, rounded to XCD multiples
+  k->static_c = std::min(std::max(sc, 1), N - 1);
+}
+
+void to_dev(const moe_calib& k, DevCalib* d) {
+  memset(d, 0, sizeof *d);
+  d->n_c = k.n_c;
+  for (int i = 0; i < k.n_c; ++i) { d->c[i] = k.c[i]; d->bw[i] = k.bw_bytes_per_s[i]; d->fl[i] = k.comp_flop_per_s[i]; }
+  d->n_k = k.n_k;
+  for (int j = 0; j < k.n_k; ++j) { d->kk[j] = k.k_chunks[j]; d->eff[j] = k.eff_chunk[j]; }
+  d->alpha = k.alpha;
+  d->literal = k.literal_volumes;
+  d->static_c = k.static_c;
+}
+
+void compute_layout(moe_handle* h) {
+  const moe_config& c = h->cfg;
+  const int T = h->T, k = c.top_k, El = c.n_local_experts, R = c.n_src_ranks, S = c.n_shared_experts;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 256); return at; };
+  moe_ws_layout& L = h->lay;
+  L.slot = take(sizeof(int32_t) * (size_t)T * k);
+  L.inv = take(sizeof(int32_t) * (size_t)std::max(h->xmax, 1));
+  L.first_slot = take(sizeof(int32_t) * (size_t)T);
+  L.off = take(sizeof(int32_t) * (size_t)(El + 1));
+  L.sub_off = take(sizeof(int32_t) * (size_t)KOPT * El * SUBW);
+  L.cnt_rank = take(sizeof(int32_t) * (size_t)El * R);
+  L.uniq = take(sizeof(int32_t) * (size_t)R);
+  L.stats = take(sizeof(int32_t) * 16);
+  L.plan = take(sizeof(moe_plan));
+  L.err = take(sizeof(int32_t) * 4);
+  h->off_calib = take(sizeof(DevCalib));
+  h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
+  h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
+  h->off_ctl[0] = take(sizeof(int32_t) * (size_t)h->ctl_words);
+  h->off_ctl[1] = take(sizeof(int32_t) * (size_t)h->ctl_words);
+  const size_t orows = (size_t)h->xmax + (size_t)S * c.tokens_per_rank + BM;
+  L.A = take(sizeof(uint16_t) * ((size_t)h->xmax + BM) * c.hidden);
+  L.Hbuf = take(sizeof(uint16_t) * orows * c.ffn);
+  L.O = take(sizeof(uint16_t) * orows * c.hidden);
+  L.total = o;
+}
+
+template <typename T>
+T* at(moe_handle* h, size_t off) { return reinterpret_cast<T*>(h->ws + off); }
+
+moe_status need_ws(moe_handle* h) {
+  if (!h) return fail(MOE_ERR_INVALID_ARG, "handle is NULL");
+  if (!h->ws) return fail(MOE_ERR_STATE, "no workspace bound (moe_set_workspace)");
+  return MOE_OK;
+}
+
+TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
+  TableArgs a{};
+  a.topk_idx = topk_idx;
+  a.slot = at<int32_t>(h, h->lay.slot);
+  a.inv = at<int32_t>(h, h->lay.inv);
+  a.first_slot = at<int32_t>(h, h->lay.first_slot);
+  a.off = at<int32_t>(h, h->lay.off);
+  a.sub_off = at<int32_t>(h, h->lay.sub_off);
+  a.cnt_rank = at<int32_t>(h, h->lay.cnt_rank);
+  a.uniq = at<int32_t>(h, h->lay.uniq);
+  a.stats = at<int32_t>(h, h->lay.stats);
+  a.blk_cnt = at<int32_t>(h, h->off_blk_cnt);
+  a.blk_off = at<int32_t>(h, h->off_blk_off);
+  a.err = at<int32_t>(h, h->lay.err);
+  a.T = h->T;
+  a.Tr = h->cfg.tokens_per_rank;
+  a.R = h->cfg.n_src_ranks;
+  a.k = h->cfg.top_k;
+  a.E = h->cfg.n_experts;
+  a.e0 = h->cfg.first_local_expert;
+  a.El = h->cfg.n_local_experts;
+  a.nblk = h->nblk;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_last_error(void) { return g_err.c_str(); }
+
+moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** out) {
+  if (!out) return fail(MOE_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  moe_status st = validate_cfg(cfg);
+  if (st != MOE_OK) return st;
+  int N = cfg->n_workers;
+  if (N == 0) {
+    int dev = 0, cus = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    N = cus;
+  }
+  if (N < 2) return fail(MOE_ERR_INVALID_ARG, "need at least 2 workers");
+  moe_handle* h = new moe_handle();
+  h->cfg = *cfg;
+  h->N = N;
+  h->T = cfg->n_src_ranks * cfg->tokens_per_rank;
+  h->xmax = h->T * std::min(cfg->top_k, cfg->n_local_experts);
+  h->nseg = cfg->n_local_experts + cfg->n_shared_experts;
+  h->mt_max = (h->xmax + cfg->n_shared_experts * cfg->tokens_per_rank) / BM + MAX_K * h->nseg + 1;
+  h->ctl_words = CTL_READY + 2 * h->mt_max;
+  h->nblk = (h->T + NTH - 1) / NTH;
+  h->nt0 = (2 * cfg->ffn + BN - 1) / BN;
+  h->nt1 = (cfg->hidden + BN - 1) / BN;
+  if (calib) {
+    st = validate_calib(calib, N);
+    if (st != MOE_OK) { delete h; return st; }
+    h->calib = *calib;
+  } else {
+    default_calib(N, &h->calib);
+  }
+  to_dev(h->calib, &h->dcal);
+  compute_layout(h);
+  *out = h;
+  return MOE_OK;
+}
+
+moe_status moe_destroy(moe_handle* h) {
+  delete h;
+  return MOE_OK;
+}
+
+moe_status moe_set_calib(moe_handle* h, const moe_calib* calib) {
+  if (!h || !calib) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  moe_status st = validate_calib(calib, h->N);
+  if (st != MOE_OK) return st;
+  h->calib = *calib;
+  to_dev(h->calib, &h->dcal);
+  if (h->ws) HIP_TRY(hipMemcpy(h->ws + h->off_calib, &h->dcal, sizeof(DevCalib), hipMemcpyHostToDevice));
+  return MOE_OK;
+}
+
+moe_status moe_get_calib(const moe_handle* h, moe_calib* out) {
+  if (!h || !out) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  *out = h->calib;
+  return MOE_OK;
+}
+
+moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall) {
+  if (!h) return fail(MOE_ERR_INVALID_ARG, "handle is NULL");
+  if (!(ms >= 0) || ms > 600000.0) return fail(MOE_ERR_INVALID_ARG, "timeout must be in [0, 600000] ms");
+  h->timeout_ticks = (long long)(ms * 1e5);
+  h->inject_stall = inject_stall ? 1 : 0;
+  return MOE_OK;
+}
+
+moe_status moe_workspace_size(const moe_handle* h, size_t* bytes) {
+  if (!h || !bytes) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  *bytes = h->lay.total;
+  return MOE_OK;
+}
+
+moe_status moe_workspace_layout(const moe_handle* h, moe_ws_layout* out) {
+  if (!h || !out) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  *out = h->lay;
+  return MOE_OK;
+}
+
+moe_status moe_set_workspace(moe_handle* h, void* ws, size_t bytes, void* stream) {
+  if (!h || !ws) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(MOE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (bytes < h->lay.total) return fail(MOE_ERR_INVALID_ARG, "workspace too small: %zu < %zu", bytes, h->lay.total);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  h->ws = static_cast<char*>(ws);
+  h->ws_bytes = bytes;
+  h->tables_from = nullptr;
+  h->launch_seq = 0;
+  // control words: both counter sets, error word, stats, plan
+  const size_t ctl_bytes = h->off_ctl[1] + sizeof(int32_t) * (size_t)h->ctl_words - h->lay.stats;
+  zero_i32_kernel<<<256, NTH, 0, s>>>(at<int32_t>(h, h->lay.stats), (int)(ctl_bytes / 4));
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(h->ws + h->off_calib, &h->dcal, sizeof(DevCalib), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return MOE_OK;
+}
+
+moe_status moe_packed_weights_size(const moe_handle* h, size_t* bytes) {
+  if (!h || !bytes) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  *bytes = (size_t)h->nseg * 3 * (size_t)h->cfg.hidden * h->cfg.ffn * sizeof(uint16_t);
+  return MOE_OK;
+}
+
+moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+                            const uint16_t* ws1, const uint16_t* ws3, const uint16_t* ws2, void* packed,
+                            void* stream) {
+  if (!h || !w1 || !w3 || !w2 || !packed) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  const int El = h->cfg.n_local_experts, S = h->cfg.n_shared_experts, H = h->cfg.hidden, F = h->cfg.ffn;
+  if (S > 0 && (!ws1 || !ws3 || !ws2)) return fail(MOE_ERR_INVALID_ARG, "shared-expert weights are NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint16_t* w13 = static_cast<uint16_t*>(packed);
+  uint16_t* w2t = w13 + (size_t)h->nseg * 2 * F * H;
+  auto launch = [&](const uint16_t* src, uint16_t* dst, int nseg, int rows, int cols, long long stride,
+                    int inter, int which) -> moe_status {
+    if (nseg == 0) return MOE_OK;
+    PackArgs a{src, dst, rows, cols, stride, inter, which};
+    dim3 grid((cols + 31) / 32, (rows + 31) / 32, nseg);
+    pack_transpose_kernel<<<grid, NTH, 0, s>>>(a);
+    HIP_TRY(hipGetLastError());
+    return MOE_OK;
+  };
+  const long long s13 = 2LL * F * H, s2 = (long long)H * F;
+  moe_status st;
+  if ((st = launch(w1, w13, El, H, F, s13, 1, 0)) != MOE_OK) return st;
+  if ((st = launch(w3, w13, El, H, F, s13, 1, 1)) != MOE_OK) return st;
+  if ((st = launch(w2, w2t, El, F, H, s2, 0, 0)) != MOE_OK) return st;
+  if (S > 0) {
+    if ((st = launch(ws1, w13 + El * s13, S, H, F, s13, 1, 0)) != MOE_OK) return st;
+    if ((st = launch(ws3, w13 + El * s13, S, H, F, s13, 1, 1)) != MOE_OK) return st;
+    if ((st = launch(ws2, w2t + El * s2, S, F, H, s2, 0, 0)) != MOE_OK) return st;
+  }
+  return MOE_OK;
+}
+
+moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!topk_idx) return fail(MOE_ERR_INVALID_ARG, "topk_idx is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  TableArgs a = table_args(h, topk_idx);
+  zero_i32_kernel<<<1, 64, 0, s>>>(a.stats, 16);
+  tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
+  tab_scan_kernel<<<1, NTH, 0, s>>>(a);
+  tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);
+  tab_finalize_kernel<<<1, NTH, 0, s>>>(a);
+  HIP_TRY(hipGetLastError());
+  h->tables_from = topk_idx;
+  return MOE_OK;
+}
+
+moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const float* logit_bias, int32_t top_k,
+                     int32_t* topk_idx, float* topk_w, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!x || !wg || !topk_idx || !topk_w) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (top_k != h->cfg.top_k) return fail(MOE_ERR_INVALID_ARG, "top_k %d differs from the configured %d", top_k, h->cfg.top_k);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  GateArgs g{};
+  g.x = x;
+  g.wg = wg;
+  g.bias = logit_bias;
+  g.topk_idx = topk_idx;
+  g.topk_w = topk_w;
+  g.T = h->T;
+  g.H = h->cfg.hidden;
+  g.E = h->cfg.n_experts;
+  g.k = top_k;
+  const int EQ = (g.E + 3) / 4;
+  g.tq = std::max(1, std::min(64, NTH / EQ));
+  const int TT = 4 * g.tq;
+  gate_topk_kernel<<<(h->T + TT - 1) / TT, NTH, 0, s>>>(g);
+  HIP_TRY(hipGetLastError());
+  return moe_build_tables(h, topk_idx, stream);
+}
+
+moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, const float* topk_w,
+                       const void* packed, uint16_t* y, int32_t mode, const moe_plan* forced, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!x || !topk_idx || !topk_w || !packed || !y) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (mode != MOE_MODE_DYNAMIC && mode != MOE_MODE_STATIC && mode != MOE_MODE_SERIAL)
+    return fail(MOE_ERR_INVALID_ARG, "unknown mode %d", mode);
+  if (h->tables_from != topk_idx)
+    return fail(MOE_ERR_STATE, "routing tables were not built from this topk_idx (call moe_route or moe_build_tables)");
+  if (forced) {
+    if (forced->c < 1 || forced->c >= h->N) return fail(MOE_ERR_INVALID_ARG, "forced c must be in [1, N-1]");
+    if (forced->K != 1 && forced->K != 2 && forced->K != 4 && forced->K != 8)
+      return fail(MOE_ERR_INVALID_ARG, "forced K must be 1, 2, 4 or 8");
+    if (forced->n_steal < 0) return fail(MOE_ERR_INVALID_ARG, "forced n_steal must be >= 0");
+    if (forced->final_all != 0 && forced->final_all != 1) return fail(MOE_ERR_INVALID_ARG, "forced final_all must be 0 or 1");
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const moe_config& c = h->cfg;
+  const int cur = (int)(h->launch_seq & 1ULL);
+  FwdArgs a{};
+  a.T = h->T;
+  a.Tr = c.tokens_per_rank;
+  a.R = c.n_src_ranks;
+  a.H = c.hidden;
+  a.F = c.ffn;
+  a.k = c.top_k;
+  a.El = c.n_local_experts;
+  a.S = c.n_shared_experts;
+  a.e0 = c.first_local_expert;
+  a.N = h->N;
+  a.nt0 = h->nt0;
+  a.nt1 = h->nt1;
+  a.xmax = h->xmax;
+  a.mt_max = h->mt_max;
+  a.ctl_words = h->ctl_words;
+  a.x = x;
+  a.topk_idx = topk_idx;
+  a.topk_w = topk_w;
+  a.w13 = static_cast<const uint16_t*>(packed);
+  a.w2t = a.w13 + (size_t)h->nseg * 2 * c.ffn * c.hidden;
+  a.y = y;
+  a.slot = at<int32_t>(h, h->lay.slot);
+  a.sub_off = at<int32_t>(h, h->lay.sub_off);
+  a.stats = at<int32_t>(h, h->lay.stats);
+  a.A = at<uint16_t>(h, h->lay.A);
+  a.Hb = at<uint16_t>(h, h->lay.Hbuf);
+  a.O = at<uint16_t>(h, h->lay.O);
+  a.ctl = at<int32_t>(h, h->off_ctl[cur]);
+  a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
+  a.err = at<int32_t>(h, h->lay.err);
+  a.plan_out = at<moe_plan>(h, h->lay.plan);
+  a.calib = at<DevCalib>(h, h->off_calib);
+  a.mode = mode;
+  a.forced = forced ? 1 : 0;
+  if (forced) a.fplan = *forced;
+  a.timeout_ticks = h->timeout_ticks;
+  a.inject_stall = h->inject_stall;
+  if (mode == MOE_MODE_SERIAL) {
+    serial_dispatch_kernel<<<h->N, NTH, 0, s>>>(a);
+    serial_gemm0_kernel<<<h->N, NTH, 0, s>>>(a);
+    serial_gemm1_kernel<<<h->N, NTH, 0, s>>>(a);
+    serial_combine_kernel<<<h->N, NTH, 0, s>>>(a);
+    HIP_TRY(hipGetLastError());
+  } else {
+    void* args[] = {&a};
+    HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(NTH), args, 0, s));
+  }
+  h->launch_seq++;
+  return MOE_OK;
+}
+
+moe_status moe_get_plan(moe_handle* h, moe_plan* out, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!out) return fail(MOE_ERR_INVALID_ARG, "out is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemcpyAsync(out, h->ws + h->lay.plan, sizeof(moe_plan), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return MOE_OK;
+}
+
+moe_status moe_sync_status(moe_handle* h, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  int32_t e = 0;
+  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(hipMemcpy(&e, h->ws + h->lay.err, sizeof e, hipMemcpyDeviceToHost));
+  if (e) {
+    zero_i32_kernel<<<1, 64, 0, s>>>(at<int32_t>(h, h->lay.err), 1);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  if (e & ERR_TIMEOUT) return fail(MOE_ERR_TIMEOUT, "a device-side wait timed out");
+  if (e & ERR_ROUTING) return fail(MOE_ERR_ROUTING, "routing ids out of range or repeated within a row");
+  return MOE_OK;
+}
+
+moe_status moe_plan_host(const moe_handle* h, double w_comp, double w_dispatch, double w_combine,
+                         const int64_t* n_tiles, moe_plan* out) {
+  if (!h || !n_tiles || !out) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  long long nt[MOE_CALIB_MAX_K];
+  for (int j = 0; j < h->dcal.n_k; ++j) nt[j] = n_tiles[j];
+  cost_model(h->dcal, h->N, w_comp, w_dispatch, w_combine, nt, out);
+  return MOE_OK;
+}
+
+moe_status moe_tile_geometry(const moe_handle* h, int32_t* bm, int32_t* nt0, int32_t* nt1) {
+  if (!h || !bm || !nt0 || !nt1) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  *bm = BM;
+  *nt0 = h->nt0;
+  *nt1 = h->nt1;
+  return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// Device-side building blocks shared by the routing, forward and packing
+// kernels of the MI355X (gfx950, CDNA4) MoE-layer library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/moe.h"
+
+namespace moe {
+
+// ---- fixed launch geometry ------------------------------------------------
+constexpr int NTH = 256;        // threads per workgroup (4 wave64s) everywhere
+constexpr int WAVE = 64;
+
+// grouped-GEMM tile: BM rows x BN columns, BK-deep K steps (bf16 MFMA 32x32x16)
+constexpr int BM = 128;
+constexpr int BN = 256;
+constexpr int BK = 64;
+
+constexpr int DT = 16;          // tokens per dispatch unit
+constexpr int CT = 16;          // tokens per combine unit
+
+constexpr int MAX_SEG = 136;    // local + shared experts
+constexpr int MAX_K = 8;        // chunk count limit
+constexpr int MAX_TOPK = 8;
+constexpr int MAX_E = 512;
+constexpr int KOPT = 4;         // chunk options with stored offsets: K = 1, 2, 4, 8
+constexpr int SUBW = 9;         // stored offsets per (K option, expert): K+1 <= 9
+
+__host__ __device__ inline int kopt_index(int K) { return K == 1 ? 0 : K == 2 ? 1 : K == 4 ? 2 : 3; }
+__host__ __device__ inline int kopt_value(int i) { return 1 << i; }
+
+// ---- control block: queue heads, readiness counters (int32 words) ------------
+// Two sets are kept; launch n uses set n%2 and clears set (n+1)%2 for the next
+// launch, so the layer is a single kernel launch with no host-side reset.
+constexpr int CTL_Q_COMP = 0;     // compute-tile queue head
+constexpr int CTL_Q_DISP = 64;    // dispatch-unit queue head
+constexpr int CTL_Q_COMB = 128;   // combine-unit queue head
+constexpr int CTL_TICKET = 192;   // arrival ticket -> role
+constexpr int CTL_ABORT = 256;    // set once any wait times out
+constexpr int CTL_G1DONE = 320;   // [MAX_K] GEMM1 tiles finished per chunk
+constexpr int CTL_SQ = 384;       // [4] queue heads of the four serial kernels (stride 64)
+constexpr int CTL_READY = 640;    // [mt_max] dispatched rows per row tile
+// CTL_G0DONE = CTL_READY + mt_max: GEMM0 column tiles finished per row tile
+
+// stats words written by the table builder
+constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;
+
+// device error word values
+constexpr int ERR_TIMEOUT = 1;
+constexpr int ERR_ROUTING = 2;
+
+// ---- bf16 -----------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (NaN stays NaN)
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// ---- memory-model helpers (agent scope: every CU of every XCD) ---------------
+__device__ __forceinline__ int ld_acquire(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_relaxed(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int fetch_add_relaxed(int* p, int v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_relaxed(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void fence_release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+__device__ __forceinline__ uint64_t now_ticks() { return __builtin_amdgcn_s_memrealtime(); }  // 100 MHz
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace moe

@@ -1,0 +1,172 @@
+// Kernel argument blocks and launch prototypes shared by the host API and
+// the kernels of the MoE-layer library.
+#pragma once
+
+#include "common.h"
+
+namespace moe {
+
+struct GateArgs {
+  const uint16_t* x;
+  const uint16_t* wg;
+  const float* bias;
+  int32_t* topk_idx;
+  float* topk_w;
+  int T, H, E, k;
+  int tq;  // token quads per workgroup
+};
+
+struct TableArgs {
+  const int32_t* topk_idx;
+  int32_t* slot;
+  int32_t* inv;
+  int32_t* first_slot;
+  int32_t* off;
+  int32_t* sub_off;
+  int32_t* cnt_rank;
+  int32_t* uniq;
+  int32_t* stats;
+  int32_t* blk_cnt;
+  int32_t* blk_off;
+  int32_t* err;
+  int T, Tr, R, k, E, e0, El, nblk;
+};
+
+struct PackArgs {
+  const uint16_t* src;
+  uint16_t* dst;
+  int rows, cols;
+  long long seg_stride;
+  int interleave, which;
+};
+
+// Calibration table as the kernels read it (copied into the workspace).
+struct DevCalib {
+  int32_t n_c;
+  int32_t c[MOE_CALIB_MAX_C];
+  double bw[MOE_CALIB_MAX_C];
+  double fl[MOE_CALIB_MAX_C];
+  int32_t n_k;
+  int32_t kk[MOE_CALIB_MAX_K];
+  double eff[MOE_CALIB_MAX_K];
+  double alpha;
+  int32_t literal;
+  int32_t static_c;
+};
+
+struct FwdArgs {
+  // shape
+  int T, Tr, R, H, F, k, El, S, e0, N;
+  int nt0, nt1;   // column tiles of GEMM0 (over 2F) and GEMM1 (over H)
+  int xmax;       // rows reserved for routed pairs in A / Hbuf / O
+  int mt_max;     // capacity of the per-row-tile counters
+  int ctl_words;  // int32 words per control set
+  // inputs / output
+  const uint16_t* x;
+  const int32_t* topk_idx;
+  const float* topk_w;
+  const uint16_t* w13;  // packed [E_l+S][2F][H]
+  const uint16_t* w2t;  // packed [E_l+S][H][F]
+  uint16_t* y;
+  // routing tables
+  const int32_t* slot;
+  const int32_t* sub_off;
+  const int32_t* stats;
+  // intermediate buffers
+  uint16_t* A;
+  uint16_t* Hb;
+  uint16_t* O;
+  // control
+  int32_t* ctl;       // this launch's control set
+  int32_t* ctl_next;  // cleared for the next launch
+  int32_t* err;
+  moe_plan* plan_out;
+  const DevCalib* calib;
+  int mode;           // MOE_MODE_DYNAMIC or MOE_MODE_STATIC
+  int forced;
+  moe_plan fplan;
+  long long timeout_ticks;  // per wait, 100 MHz ticks
+  int inject_stall;         // test hook: every wait targets an unreachable value
+};
+
+// ---- cost model (sections 3.1-3.3) ------------------------------------------
+// Evaluates T_total(c, K) of Eq 15 over the calibrated (c, K) grid, takes the
+// first strict minimum (c ascending, then K ascending; Eq 16), then the steal
+// count of Eq 11-14 at (c*, K*).  fp64, no contraction; the host entry point
+// and the megakernel prologue run this same function.
+__host__ __device__ inline double cm_t_total(const DevCalib& cb, int ci, int ki, double w_comp,
+                                             double w_disp, double w_comb) {
+#pragma clang fp contract(off)
+  double bw = cb.bw[ci];
+  double fl = cb.fl[ci];
+  double K = (double)cb.kk[ki];
+  double t_comp = w_comp / (fl * cb.eff[ki]);                // Eq 9 (Eq 4 at K = 1)
+  double t_comm = (w_disp + w_comb) / bw;                    // Eq 5
+  double t_tail = ((1.0 - cb.alpha) * w_comb) / (bw * K);    // Eq 10 (Eq 6 at K = 1)
+  double s = t_comp + t_tail;
+  return s > t_comm ? s : t_comm;                            // Eq 15 (Eq 7 at K = 1)
+}
+
+__host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_comp, double w_disp,
+                                           double w_comb, const long long* n_tiles_by_k,
+                                           moe_plan* out) {
+#pragma clang fp contract(off)
+  int bc = 0, bk = 0;
+  double best = cm_t_total(cb, 0, 0, w_comp, w_disp, w_comb);
+  for (int ci = 0; ci < cb.n_c; ++ci)
+    for (int ki = 0; ki < cb.n_k; ++ki) {
+      double t = cm_t_total(cb, ci, ki, w_comp, w_disp, w_comb);
+      if (t < best) { best = t; bc = ci; bk = ki; }
+    }
+  double t_comm = (w_disp + w_comb) / cb.bw[bc];             // Eq 11
+  double w_partial = t_comm * cb.fl[bc];                     // Eq 12
+  double w_steal = w_comp - w_partial;                       // Eq 13
+  if (w_steal < 0.0) w_steal = 0.0;
+  long long nt = n_tiles_by_k[bk];
+  int n_steal = 0;
+  if (nt > 0 && w_comp > 0.0) {
+    double w_tile = w_comp / (double)nt;
+    n_steal = (int)floor(w_steal / ((double)N * w_tile));   // Eq 14
+  }
+  out->c = cb.c[bc];
+  out->K = cb.kk[bk];
+  out->n_steal = n_steal;
+  out->final_all = 1;
+  out->t_pred_s = best;
+}
+
+// Volumes of section 3.1 from the routing stats.  With `literal` the moved
+// bytes are Eq 2-3 as printed (remote rows only); otherwise every moved row
+// counts, since on one GPU rank 0's rows also pass through the movement
+// workers.  Shared-expert rows are compute-only work.
+__host__ __device__ inline void cm_volumes(const int32_t* stats, int H, int F, int shared_rows,
+                                           int literal, double* w_comp, double* w_disp,
+                                           double* w_comb) {
+#pragma clang fp contract(off)
+  double B = 2.0 * (double)H;
+  double X = (double)stats[ST_X];
+  *w_comp = (((X + (double)shared_rows) * 6.0) * (double)H) * (double)F;   // Eq 1
+  if (literal) {
+    *w_disp = (double)stats[ST_UIN] * B;                                   // Eq 2
+    *w_comb = (double)stats[ST_XIN] * B;                                   // Eq 3
+  } else {
+    *w_disp = ((double)stats[ST_ULOCAL] + (double)stats[ST_UIN]) * B;
+    *w_comb = X * B;
+  }
+}
+
+// ---- launch prototypes ---------------------------------------------------------
+__global__ void gate_topk_kernel(GateArgs a);
+__global__ void tab_count_kernel(TableArgs a);
+__global__ void tab_scan_kernel(TableArgs a);
+__global__ void tab_perm_kernel(TableArgs a);
+__global__ void tab_finalize_kernel(TableArgs a);
+__global__ void zero_i32_kernel(int* p, int n);
+__global__ void pack_transpose_kernel(PackArgs a);
+__global__ void moe_megakernel(FwdArgs a);
+__global__ void serial_dispatch_kernel(FwdArgs a);
+__global__ void serial_gemm0_kernel(FwdArgs a);
+__global__ void serial_gemm1_kernel(FwdArgs a);
+__global__ void serial_combine_kernel(FwdArgs a);
+
+}  // namespace moe

@@ -1,0 +1,204 @@
+"""GPU parity of the MoE layer (dispatch, GEMM0 + SiLU*up, GEMM1, combine)
+against the CPU oracle, in the three execution modes and under forced plans.
+
+Bar: max|y_gpu - y_ref| <= 2e-2 * max|y_ref| over the checked rows (bf16
+inputs, fp32 accumulation, bf16 intermediates).  The dispatched rows are
+checked bit for bit.  Every plan computes each output element with the same
+operations in the same order, so y must also be bit-identical across modes
+and plans."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_21483_amd import workloads as W
+from tests.cases import bf16_to_f64, make_case, oracle_rows, pick_rows, rel_err
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_21483_amd import binding
+    return binding
+
+
+def run_modes(B, layer, c, idx, w, modes=("dynamic", "static", "serial"), forced=()):
+    shape = c.shape
+    x = c.x.cuda()
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx, np.int32)).cuda()
+    w_d = torch.from_numpy(np.ascontiguousarray(w, np.float32)).cuda()
+    B.moe_build_tables(layer.h, idx_d)
+    outs = {}
+    for m in modes:
+        y = torch.full((shape.T, shape.hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+        layer.forward(x, idx_d, w_d, y, m)
+        st = B.moe_sync_status(layer.h)
+        assert st == B.MOE_OK, (m, B.moe_last_error())
+        outs[m] = y
+    for p in forced:
+        y = torch.full((shape.T, shape.hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+        layer.forward(x, idx_d, w_d, y, "dynamic", forced=B.moe_plan(*p, 0.0))
+        st = B.moe_sync_status(layer.h)
+        assert st == B.MOE_OK, (p, B.moe_last_error())
+        outs[p] = y
+    return outs
+
+
+def check_case(B, c, rows=None, forced=(), check_A=False):
+    shape = c.shape
+    idx, w = c.oracle_route()
+    layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+    try:
+        outs = run_modes(B, layer, c, idx, w, forced=forced)
+        rows = np.arange(shape.T) if rows is None else rows
+        y_ref = oracle_rows(c, idx, w, rows)
+        first = None
+        for key, y in outs.items():
+            yg = bf16_to_f64(y[torch.from_numpy(rows).cuda()])
+            assert np.all(np.isfinite(yg)), key
+            err = rel_err(yg, y_ref)
+            assert err <= TOL, (key, err)
+            if first is None:
+                first = y
+            else:
+                assert torch.equal(y.view(torch.int16), first.view(torch.int16)), f"{key} differs from dynamic"
+        if check_A:
+            tab = O.route_tables(idx, shape.n_src_ranks, shape.tokens_per_rank, 0, shape.n_local_experts)
+            A = layer.ws_view("A", torch.int16, tab.X * shape.hidden).cpu().numpy().view(np.uint16)
+            assert np.array_equal(A.reshape(tab.X, shape.hidden), O.dispatch(c.xu, tab, shape.top_k))
+        return err
+    finally:
+        layer.close()
+
+
+FORCED_SMALL = [(1, 1, 0, 1), (8, 2, 3, 1), (64, 4, 0, 0), (255, 8, 1000, 1), (40, 1, 0, 0), (128, 8, 2, 0)]
+
+
+def test_tiny_all_rows_all_plans(B):
+    c = make_case(W.TINY)
+    check_case(B, c, forced=FORCED_SMALL, check_A=True)
+
+
+@pytest.mark.parametrize("shape", [
+    W.MoeShape("ragged", 98, 3, 45, 192, 320, 10, 3, 4, n_shared_experts=1),
+    W.MoeShape("one_token", 97, 1, 1, 128, 128, 8, 2, 8),
+    W.MoeShape("all_local", 96, 2, 150, 256, 192, 4, 4, 4),
+    W.MoeShape("skew_empty", 95, 4, 77, 128, 256, 32, 8, 5, zipf_s=3.0),
+    W.MoeShape("wide_tail", 94, 2, 200, 320, 576, 12, 2, 3, n_shared_experts=2),
+], ids=lambda s: s.name)
+def test_edge_shapes(B, shape):
+    c = make_case(shape.with_(w_std=0.05))
+    check_case(B, c, forced=FORCED_SMALL, check_A=True)
+
+
+def test_no_local_pairs(B):
+    """Every token routed off this GPU: y must be all zeros (no shared experts),
+    or only the shared output on rank 0."""
+    for S in (0, 1):
+        shape = W.MoeShape("nolocal", 93, 2, 64, 128, 128, 16, 2, 4, n_shared_experts=S)
+        c = make_case(shape.with_(w_std=0.05))
+        idx, w = W.random_routing(shape.T, 12, 2, seed=5)
+        idx = (idx + 4).astype(np.int32)  # experts 4..15, all remote
+        layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+        try:
+            outs = run_modes(B, layer, c, idx, w.astype(np.float64))
+            y_ref = oracle_rows(c, idx, w.astype(np.float64), np.arange(shape.T))
+            for y in outs.values():
+                yg = bf16_to_f64(y)
+                if S == 0:
+                    assert np.all(yg == 0.0)
+                else:
+                    assert np.all(yg[shape.tokens_per_rank:] == 0.0)
+                    assert rel_err(yg, y_ref) <= TOL
+        finally:
+            layer.close()
+
+
+FULL = [("mixtral_ep4", 0), ("fine_zipf", 0), ("shared_routed", 0), ("large_stack", 0), ("large_stack", 5)]
+
+
+@pytest.mark.parametrize("name,layer", FULL, ids=[f"{n}-L{l}" for n, l in FULL])
+def test_full_size_sampled_rows(B, name, layer):
+    shape = W.WORKLOADS[name]
+    c = make_case(shape, layer)
+    idx, _ = c.oracle_route()
+    rows = pick_rows(shape, idx, per_rank=16, seed=100 + layer)
+    forced = [(8, 8, 4, 1), (120, 2, 0, 1)] if name == "fine_zipf" else []
+    check_case(B, c, rows=rows, forced=forced)
+
+
+def test_route_then_forward_end_to_end(B):
+    """moe_route output fed straight into moe_forward."""
+    shape = W.FINE_ZIPF.with_(tokens_per_rank=256)
+    c = make_case(shape)
+    idx_ref, w_ref = c.oracle_route()
+    layer = B.MoeLayer(shape, c.w1, c.w3, c.w2)
+    try:
+        x = c.x.cuda()
+        idx = torch.empty((shape.T, shape.top_k), dtype=torch.int32, device="cuda")
+        w = torch.empty((shape.T, shape.top_k), dtype=torch.float32, device="cuda")
+        layer.route(x, c.wg.cuda(), c.bias.cuda(), idx, w)
+        y = torch.empty((shape.T, shape.hidden), dtype=torch.bfloat16, device="cuda")
+        layer.forward(x, idx, w, y, "dynamic")
+        assert B.moe_sync_status(layer.h) == B.MOE_OK
+        assert np.array_equal(idx.cpu().numpy(), idx_ref)
+        y_ref = oracle_rows(c, idx_ref, w_ref, np.arange(shape.T))
+        assert rel_err(bf16_to_f64(y), y_ref) <= TOL
+        # forward refuses routing the tables were not built from
+        other = idx.clone()
+        with pytest.raises(B.MoeError) as ei:
+            layer.forward(x, other, w, y, "dynamic")
+        assert ei.value.status == B.MOE_ERR_STATE
+    finally:
+        layer.close()
+
+
+def test_repeat_launches_deterministic(B):
+    c = make_case(W.FINE_ZIPF.with_(tokens_per_rank=512))
+    idx, w = c.oracle_route()
+    layer = B.MoeLayer(c.shape, c.w1, c.w3, c.w2)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(idx).cuda()
+        w_d = torch.from_numpy(w.astype(np.float32)).cuda()
+        B.moe_build_tables(layer.h, idx_d)
+        ys = []
+        for i in range(6):
+            y = torch.empty((c.shape.T, c.shape.hidden), dtype=torch.bfloat16, device="cuda")
+            layer.forward(x, idx_d, w_d, y, ("dynamic", "static", "serial")[i % 3])
+            ys.append(y)
+        assert B.moe_sync_status(layer.h) == B.MOE_OK
+        for y in ys[1:]:
+            assert torch.equal(y.view(torch.int16), ys[0].view(torch.int16))
+    finally:
+        layer.close()
+
+
+def test_timeout_path_recovers(B):
+    """Host-forced stall: every wait targets an unreachable value, so the
+    launch times out on its own bounded waits, reports MOE_ERR_TIMEOUT, and the
+    next launch (other control set) is correct again."""
+    c = make_case(W.TINY)
+    idx, w = c.oracle_route()
+    layer = B.MoeLayer(c.shape, c.w1, c.w3, c.w2)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(idx).cuda()
+        w_d = torch.from_numpy(w.astype(np.float32)).cuda()
+        B.moe_build_tables(layer.h, idx_d)
+        y = torch.empty((c.shape.T, c.shape.hidden), dtype=torch.bfloat16, device="cuda")
+        B.moe_set_timeout_ms(layer.h, 20.0, 1)
+        layer.forward(x, idx_d, w_d, y, "dynamic")
+        assert B.moe_sync_status(layer.h) == B.MOE_ERR_TIMEOUT
+        B.moe_set_timeout_ms(layer.h, 2000.0, 0)
+        for _ in range(2):
+            layer.forward(x, idx_d, w_d, y, "dynamic")
+            assert B.moe_sync_status(layer.h) == B.MOE_OK
+            y_ref = oracle_rows(c, idx, w, np.arange(c.shape.T))
+            assert rel_err(bf16_to_f64(y), y_ref) <= TOL
+    finally:
+        layer.close()

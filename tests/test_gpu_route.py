@@ -1,0 +1,136 @@
+"""GPU parity of routing (gate logits, softmax, top-k, renormalise) and of the
+routing tables, against the CPU oracle.  Expert ids, counts, offsets, slots,
+inverse permutation, first slots, chunk offsets and stats must match bit for
+bit; the renormalised weights within 1e-6 absolute."""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_21483_amd import workloads as W
+from tests.cases import make_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_21483_amd import binding
+    return binding
+
+
+@functools.lru_cache(maxsize=2)
+def _tokens(name):
+    return W.tokens(W.WORKLOADS[name])
+
+
+class Handle:
+    def __init__(self, B, shape):
+        self.B = B
+        self.h = B.moe_init(B.make_config(shape))
+        self.ws = torch.empty(B.moe_workspace_size(self.h), dtype=torch.uint8, device="cuda")
+        B.moe_set_workspace(self.h, self.ws)
+        self.L = B.moe_workspace_layout(self.h)
+
+    def view(self, name, n):
+        off = getattr(self.L, name)
+        return self.ws[off:off + 4 * n].view(torch.int32).cpu().numpy()
+
+    def close(self):
+        self.B.moe_destroy(self.h)
+
+
+def check_tables(hd: Handle, shape, idx_ref):
+    T, k, R, Tr, El = shape.T, shape.top_k, shape.n_src_ranks, shape.tokens_per_rank, shape.n_local_experts
+    tab = O.route_tables(idx_ref, R, Tr, 0, El)
+    assert np.array_equal(hd.view("slot", T * k).reshape(T, k), tab.slot)
+    assert np.array_equal(hd.view("inv", tab.X), tab.inv)
+    assert np.array_equal(hd.view("first_slot", T), tab.first_slot)
+    assert np.array_equal(hd.view("off", El + 1), tab.off)
+    assert np.array_equal(hd.view("cnt_rank", El * R).reshape(El, R), tab.cnt_rank)
+    assert np.array_equal(hd.view("uniq", R), tab.uniq)
+    st = hd.view("stats", 16)
+    X_local = int(tab.cnt_rank[:, 0].sum())
+    assert list(st[:6]) == [tab.X, X_local, tab.X - X_local, int(tab.uniq[0]), int(tab.uniq[1:].sum()), 0]
+    sub = hd.view("sub_off", 4 * El * 9).reshape(4, El, 9)
+    for ki, K in enumerate((1, 2, 4, 8)):
+        assert np.array_equal(sub[ki, :, :K + 1], O.chunk_offsets(tab, T, k, K)), K
+    return tab
+
+
+ROUTE_CASES = [("tiny", 0), ("mixtral_ep4", 0), ("fine_zipf", 0), ("shared_routed", 0)] + \
+    [("large_stack", l) for l in range(8)]
+
+
+@pytest.mark.parametrize("name,layer", ROUTE_CASES, ids=[f"{n}-L{l}" for n, l in ROUTE_CASES])
+def test_route_parity(B, name, layer):
+    shape = W.WORKLOADS[name]
+    c = make_case(shape, layer, weights=False) if name != "large_stack" else None
+    if c is None:
+        from tests.cases import Case
+        c = Case(shape, layer, _tokens(name), W.gate(shape, layer), W.zipf_log_prior(shape, layer))
+    idx_ref, w_ref = c.oracle_route()
+    hd = Handle(B, shape)
+    try:
+        x = c.x.cuda()
+        wg = c.wg.cuda()
+        bias = None if c.bias is None else c.bias.cuda()
+        idx = torch.full((shape.T, shape.top_k), -7, dtype=torch.int32, device="cuda")
+        w = torch.zeros((shape.T, shape.top_k), dtype=torch.float32, device="cuda")
+        B.moe_route(hd.h, x, wg, bias, shape.top_k, idx, w)
+        assert B.moe_sync_status(hd.h) == B.MOE_OK, B.moe_last_error()
+        idx_g = idx.cpu().numpy()
+        mism = np.nonzero((idx_g != idx_ref).any(axis=1))[0]
+        assert mism.size == 0, f"{mism.size} tokens differ, first {mism[:5]}"
+        assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= 1e-6
+        check_tables(hd, shape, idx_ref)
+    finally:
+        hd.close()
+
+
+@pytest.mark.parametrize("R,Tr,E,k,El,skew", [
+    (3, 45, 10, 3, 4, 0.0),      # ragged token count
+    (1, 1, 8, 2, 8, 0.0),        # a single token
+    (2, 300, 16, 4, 16, 0.0),    # every expert local
+    (4, 77, 32, 8, 5, 2.5),      # heavy skew: empty local experts
+    (2, 513, 64, 6, 16, 1.0),    # more than one table block
+])
+def test_build_tables_supplied_routing(B, R, Tr, E, k, El, skew):
+    shape = W.MoeShape("t", 99, R, Tr, 64, 64, E, k, El)
+    idx_ref, _ = W.random_routing(shape.T, E, k, seed=R * 1000 + Tr, skew=skew)
+    hd = Handle(B, shape)
+    try:
+        idx = torch.from_numpy(idx_ref).cuda()
+        B.moe_build_tables(hd.h, idx)
+        assert B.moe_sync_status(hd.h) == B.MOE_OK
+        check_tables(hd, shape, idx_ref)
+    finally:
+        hd.close()
+
+
+def test_bad_routing_ids_are_flagged(B):
+    shape = W.MoeShape("t", 99, 2, 40, 64, 64, 8, 2, 4)
+    idx_ref, _ = W.random_routing(shape.T, 8, 2, seed=3)
+    bad = idx_ref.copy()
+    bad[5, 1] = 8          # out of range
+    bad[9, 1] = bad[9, 0]  # repeated in a row
+    bad[11, 0] = -1
+    hd = Handle(B, shape)
+    try:
+        B.moe_build_tables(hd.h, torch.from_numpy(bad).cuda())
+        assert B.moe_sync_status(hd.h) == B.MOE_ERR_ROUTING
+        # the flagged pairs are treated as not local; everything else is intact
+        clean = bad.copy()
+        clean[5, 1] = 100
+        clean[9, 1] = 100
+        clean[11, 0] = 100
+        tab = O.route_tables(clean, 2, 40, 0, 4)
+        assert np.array_equal(hd.view("slot", shape.T * 2).reshape(-1, 2), tab.slot)
+        assert hd.view("stats", 16)[5] == 3
+        assert B.moe_sync_status(hd.h) == B.MOE_OK  # the error word was cleared
+    finally:
+        hd.close()
