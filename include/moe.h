@@ -70,7 +70,7 @@ typedef struct {
   int32_t ffn;                /* I (F), multiple of 64, <= 32768 */
   int32_t n_experts;          /* E, 1..512 */
   int32_t top_k;              /* k, 1..min(E, 8) */
-  int32_t n_local_experts;    /* E_l, 1..128 */
+  int32_t n_local_experts;    /* E_l, 1..64 */
   int32_t first_local_expert; /* e0, 0 <= e0 <= E - E_l */
   int32_t n_shared_experts;   /* S, 0..8, always-on experts applied to rank-0 tokens */
   int32_t n_workers;          /* persistent workgroups N; 0 = one per CU */
@@ -219,8 +219,9 @@ moe_status moe_sync_status(moe_handle* h, void* stream);
 moe_status moe_plan_host(const moe_handle* h, double w_comp, double w_dispatch,
                          double w_combine, const int64_t* n_tiles, moe_plan* out);
 
-/* Tile geometry of the grouped GEMM: rows per tile (BM) and column tiles of
- * GEMM0 / GEMM1 for this shape. */
+/* Tile geometry of the grouped GEMM for this shape: rows per tile (bm), GEMM0
+ * tiles per row tile (nt0: column tiles over 2F) and GEMM1 tiles per row tile
+ * (nt1: column tiles over H times the split-K factor of GEMM1). */
 moe_status moe_tile_geometry(const moe_handle* h, int32_t* bm, int32_t* nt0, int32_t* nt1);
 
 #ifdef __cplusplus

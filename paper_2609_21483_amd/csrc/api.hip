@@ -39,11 +39,11 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 struct moe_handle {
   moe_config cfg;
   int N = 0;
-  int T = 0, xmax = 0, mt_max = 0, ctl_words = 0, nblk = 0, nseg = 0, nt0 = 0, nt1 = 0;
+  int T = 0, xmax = 0, mt_max = 0, ctl_words = 0, nblk = 0, nseg = 0, nt0 = 0, nt1 = 0, nsplit = 1;
   moe_calib calib{};
   DevCalib dcal{};
   moe_ws_layout lay{};
-  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_ctl[2] = {0, 0};
+  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_ctl[2] = {0, 0}, off_part = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
   const int32_t* tables_from = nullptr;
@@ -67,12 +67,12 @@ moe_status validate_cfg(const moe_config* c) {
   if (c->n_experts < 1 || c->n_experts > MAX_E) return fail(MOE_ERR_INVALID_ARG, "n_experts must be in [1, %d]", MAX_E);
   if (c->top_k < 1 || c->top_k > MAX_TOPK || c->top_k > c->n_experts)
     return fail(MOE_ERR_INVALID_ARG, "top_k must be in [1, min(E, %d)]", MAX_TOPK);
-  if (c->n_local_experts < 1 || c->n_local_experts > 128)
-    return fail(MOE_ERR_INVALID_ARG, "n_local_experts must be in [1, 128]");
+  if (c->n_local_experts < 1 || c->n_local_experts > MAX_EL)
+    return fail(MOE_ERR_INVALID_ARG, "n_local_experts must be in [1, %d]", MAX_EL);
   if (c->first_local_expert < 0 || c->first_local_expert + c->n_local_experts > c->n_experts)
     return fail(MOE_ERR_INVALID_ARG, "local experts [e0, e0+E_l) must lie in [0, E)");
-  if (c->n_shared_experts < 0 || c->n_shared_experts > 8)
-    return fail(MOE_ERR_INVALID_ARG, "n_shared_experts must be in [0, 8]");
+  if (c->n_shared_experts < 0 || c->n_shared_experts > MAX_S)
+    return fail(MOE_ERR_INVALID_ARG, "n_shared_experts must be in [0, %d]", MAX_S);
   if (c->n_workers < 0) return fail(MOE_ERR_INVALID_ARG, "n_workers must be >= 0");
   long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
   if (xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM > (1LL << 31) / 2)
@@ -164,6 +164,7 @@ void compute_layout(moe_handle* h) {
   L.A = take(sizeof(uint16_t) * ((size_t)h->xmax + BM) * c.hidden);
   L.Hbuf = take(sizeof(uint16_t) * orows * c.ffn);
   L.O = take(sizeof(uint16_t) * orows * c.hidden);
+  h->off_part = h->nsplit > 1 ? take(sizeof(float) * (size_t)h->mt_max * h->nt1 * h->nsplit * BM * BN) : 0;
   L.total = o;
 }
 
@@ -227,10 +228,14 @@ moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** 
   h->xmax = h->T * std::min(cfg->top_k, cfg->n_local_experts);
   h->nseg = cfg->n_local_experts + cfg->n_shared_experts;
   h->mt_max = (h->xmax + cfg->n_shared_experts * cfg->tokens_per_rank) / BM + MAX_K * h->nseg + 1;
-  h->ctl_words = CTL_READY + 2 * h->mt_max;
   h->nblk = (h->T + NTH - 1) / NTH;
   h->nt0 = (2 * cfg->ffn + BN - 1) / BN;
   h->nt1 = (cfg->hidden + BN - 1) / BN;
+  // split GEMM1 (K = F) when F is large against H, so its tiles are about as
+  // long as GEMM0's (K = H) and there are enough of them to fill the CUs
+  h->nsplit = cfg->ffn >= 3 * cfg->hidden ? 4 : (2 * cfg->ffn >= 3 * cfg->hidden ? 2 : 1);
+  while (h->nsplit > 1 && cfg->ffn % (32 * h->nsplit)) h->nsplit /= 2;
+  h->ctl_words = CTL_READY + 2 * h->mt_max + h->mt_max * h->nt1;
   if (calib) {
     st = validate_calib(calib, N);
     if (st != MOE_OK) { delete h; return st; }
@@ -413,6 +418,7 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
   a.N = h->N;
   a.nt0 = h->nt0;
   a.nt1 = h->nt1;
+  a.nsplit = h->nsplit;
   a.xmax = h->xmax;
   a.mt_max = h->mt_max;
   a.ctl_words = h->ctl_words;
@@ -428,6 +434,7 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
   a.A = at<uint16_t>(h, h->lay.A);
   a.Hb = at<uint16_t>(h, h->lay.Hbuf);
   a.O = at<uint16_t>(h, h->lay.O);
+  a.part = h->nsplit > 1 ? at<float>(h, h->off_part) : nullptr;
   a.ctl = at<int32_t>(h, h->off_ctl[cur]);
   a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
   a.err = at<int32_t>(h, h->lay.err);
@@ -439,14 +446,14 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
   a.timeout_ticks = h->timeout_ticks;
   a.inject_stall = h->inject_stall;
   if (mode == MOE_MODE_SERIAL) {
-    serial_dispatch_kernel<<<h->N, NTH, 0, s>>>(a);
-    serial_gemm0_kernel<<<h->N, NTH, 0, s>>>(a);
-    serial_gemm1_kernel<<<h->N, NTH, 0, s>>>(a);
-    serial_combine_kernel<<<h->N, NTH, 0, s>>>(a);
+    serial_dispatch_kernel<<<h->N, FNTH, 0, s>>>(a);
+    serial_gemm0_kernel<<<h->N, FNTH, 0, s>>>(a);
+    serial_gemm1_kernel<<<h->N, FNTH, 0, s>>>(a);
+    serial_combine_kernel<<<h->N, FNTH, 0, s>>>(a);
     HIP_TRY(hipGetLastError());
   } else {
     void* args[] = {&a};
-    HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(NTH), args, 0, s));
+    HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(FNTH), args, 0, s));
   }
   h->launch_seq++;
   return MOE_OK;
@@ -492,7 +499,7 @@ moe_status moe_tile_geometry(const moe_handle* h, int32_t* bm, int32_t* nt0, int
   if (!h || !bm || !nt0 || !nt1) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
   *bm = BM;
   *nt0 = h->nt0;
-  *nt1 = h->nt1;
+  *nt1 = h->nt1 * h->nsplit;
   return MOE_OK;
 }
 

@@ -10,18 +10,21 @@
 namespace moe {
 
 // ---- fixed launch geometry ------------------------------------------------
-constexpr int NTH = 256;        // threads per workgroup (4 wave64s) everywhere
+constexpr int NTH = 256;        // threads per workgroup of the routing kernels
+constexpr int FNTH = 512;       // threads per workgroup of the forward kernels (8 wave64s)
 constexpr int WAVE = 64;
 
-// grouped-GEMM tile: BM rows x BN columns, BK-deep K steps (bf16 MFMA 32x32x16)
-constexpr int BM = 128;
+// grouped-GEMM tile: BM rows x BN columns (bf16 MFMA 32x32x16, see gemm.h)
+constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int BK = 64;
+constexpr int MAX_SPLIT = 4;    // split-K factor limit of GEMM1
 
 constexpr int DT = 16;          // tokens per dispatch unit
 constexpr int CT = 16;          // tokens per combine unit
 
-constexpr int MAX_SEG = 136;    // local + shared experts
+constexpr int MAX_EL = 64;      // local experts
+constexpr int MAX_S = 8;        // shared experts
+constexpr int MAX_SEG = MAX_EL + MAX_S;
 constexpr int MAX_K = 8;        // chunk count limit
 constexpr int MAX_TOPK = 8;
 constexpr int MAX_E = 512;
@@ -42,7 +45,8 @@ constexpr int CTL_ABORT = 256;    // set once any wait times out
 constexpr int CTL_G1DONE = 320;   // [MAX_K] GEMM1 tiles finished per chunk
 constexpr int CTL_SQ = 384;       // [4] queue heads of the four serial kernels (stride 64)
 constexpr int CTL_READY = 640;    // [mt_max] dispatched rows per row tile
-// CTL_G0DONE = CTL_READY + mt_max: GEMM0 column tiles finished per row tile
+// then [mt_max] GEMM0 column tiles finished per row tile,
+// then [mt_max * nt1] split-K arrivals per GEMM1 (row tile, column tile)
 
 // stats words written by the table builder
 constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;

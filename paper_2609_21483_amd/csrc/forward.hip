@@ -1,156 +1,30 @@
 // The MoE layer on one GPU's share (paper section 2.1, Fig 3), run either as
 // one persistent megakernel with movement and compute workers (sections 3-4)
-// or as four separate kernels (the serial baseline of section 5.6, "w/o S+T").
+// or as four separate kernels (the serial baseline, "w/o S+T" of section 5.6).
 //
 // Data layout in HBM
 //   x    bf16 [T][H]        staging regions: rank r's rows at r*Tr
 //   A    bf16 [X+pad][H]    dispatched rows, expert-contiguous (slot order)
 //   Hbuf bf16 [X+S*Tr+pad][F]  SiLU(gate)*up per row (shared experts after X)
 //   O    bf16 [X+S*Tr+pad][H]  expert outputs per row
+//   part fp32 [row tile][col tile][split][256*256]  split-K partials of GEMM1
 //   y    bf16 [T][H]        output staging regions
 //   w13  bf16 [E_l+S][2F][H] gate/up weights, k-contiguous, 32-col interleave
 //   w2t  bf16 [E_l+S][H][F]  down weights, k-contiguous
 #include "common.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace moe {
 
-// ===========================================================================
-// Grouped-GEMM tile: C[BM x BN] = A[BM x Kd] * B[BN x Kd]^T on bf16 MFMA
-// (v_mfma_f32_32x32x16_bf16), fp32 accumulation.  4 waves in a 2 x 2 grid,
-// each wave owns 64 x 128 outputs (2 x 4 MFMA blocks).  A and B stream
-// through double-buffered LDS tiles of BK = 64; 16-byte chunks are XOR-swizzled
-// by row so the fragment reads are free of bank conflicts.
-// EPI 0 (GEMM0): columns come in gate/up 32-column pairs; the epilogue writes
-//   bf16(silu(gate) * up), BN/2 columns.
-// EPI 1 (GEMM1): the epilogue writes bf16(C), BN columns.
-// ===========================================================================
-constexpr int GEMM_SMEM = 2 * (BM * BK + BN * BK) * 2;  // bytes (96 KiB)
-
-__device__ __forceinline__ int swz(int row, int chunk) { return row * BK + ((chunk ^ (row & 7)) << 3); }
-
-template <int EPI>
-__device__ void gemm_tile(const uint16_t* __restrict__ A, int lda, int a_rows,
-                          const uint16_t* __restrict__ B, int ldb, int b_rows, int Kd,
-                          uint16_t* __restrict__ out, int ldo, int out_rows, int out_cols,
-                          char* smem) {
-  uint16_t* As = reinterpret_cast<uint16_t*>(smem);
-  uint16_t* Bs = As + 2 * BM * BK;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
-
-  constexpr int AV = BM * BK / 8 / NTH;  // 16-byte vectors per thread (A)
-  constexpr int BV = BN * BK / 8 / NTH;  // (B)
-  u32x4_t ra[AV], rb[BV];
-
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      int v = tid + i * NTH, row = v >> 3, c = v & 7;
-      u32x4_t z = {0u, 0u, 0u, 0u};
-      ra[i] = row < a_rows ? *reinterpret_cast<const u32x4_t*>(A + (size_t)row * lda + k0 + c * 8) : z;
-    }
-#pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      int v = tid + i * NTH, row = v >> 3, c = v & 7;
-      u32x4_t z = {0u, 0u, 0u, 0u};
-      rb[i] = row < b_rows ? *reinterpret_cast<const u32x4_t*>(B + (size_t)row * ldb + k0 + c * 8) : z;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      int v = tid + i * NTH, row = v >> 3, c = v & 7;
-      *reinterpret_cast<u32x4_t*>(As + buf * BM * BK + swz(row, c)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      int v = tid + i * NTH, row = v >> 3, c = v & 7;
-      *reinterpret_cast<u32x4_t*>(Bs + buf * BN * BK + swz(row, c)) = rb[i];
-    }
-  };
-
-  f32x16_t acc[2][4];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
-
-  const int nk = Kd / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int ks = 0; ks < nk; ++ks) {
-    const int buf = ks & 1;
-    if (ks + 1 < nk) gload((ks + 1) * BK);
-    const uint16_t* as = As + buf * BM * BK;
-    const uint16_t* bs = Bs + buf * BN * BK;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = kk * 2 + (lane >> 5);
-      bf16x8_t af[2], bfr[4];
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        int row = wm * 64 + mb * 32 + (lane & 31);
-        af[mb] = *reinterpret_cast<const bf16x8_t*>(as + swz(row, c));
-      }
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        int row = wn * 128 + nb * 32 + (lane & 31);
-        bfr[nb] = *reinterpret_cast<const bf16x8_t*>(bs + swz(row, c));
-      }
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
-    }
-    if (ks + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  // epilogue: stage the bf16 tile in LDS, then write 16-byte rows
-  constexpr int OC = EPI == 0 ? BN / 2 : BN;
-  constexpr int CST = OC + 8;
-  uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
-  const int j = lane & 31;
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (EPI == 0) {
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          float g = acc[mb][2 * p][r];
-          float u = acc[mb][2 * p + 1][r];
-          float hv = (g / (1.0f + __expf(-g))) * u;
-          Cs[row * CST + wn * 64 + p * 32 + j] = (uint16_t)f32_to_bf16(hv);
-        }
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          Cs[row * CST + wn * 128 + nb * 32 + j] = (uint16_t)f32_to_bf16(acc[mb][nb][r]);
-      }
-    }
-  __syncthreads();
-  constexpr int VPR = OC / 8;
-  for (int v = tid; v < BM * VPR; v += NTH) {
-    int row = v / VPR, col = (v % VPR) * 8;
-    if (row < out_rows && col < out_cols)
-      *reinterpret_cast<u32x4_t*>(out + (size_t)row * ldo + col) =
-          *reinterpret_cast<const u32x4_t*>(Cs + row * CST + col);
-  }
-  __syncthreads();
-}
+constexpr int NWF = FNTH / WAVE;  // waves per forward workgroup
 
 // ===========================================================================
 // Schedule of one launch for chunk count K (built by every workgroup in LDS).
 // Segment seg < E_l is local expert seg; seg >= E_l is shared expert seg-E_l.
+// Queue order (section 4, chunk-pipeline DAG order): chunk, then phase (GEMM0
+// tiles, then GEMM1 tiles), then segment; inside a group the row tile runs
+// fastest (GEMM1: the split runs fastest, then the row tile).
 // ===========================================================================
 struct Sched {
   int K, nseg, G;        // chunks, segments, groups = K*2*nseg
@@ -158,7 +32,7 @@ struct Sched {
   int c, n_steal, final_all;
   int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
   int cstart[MAX_K + 1]; // combine units before chunk q
-  int g1need[MAX_K];     // GEMM1 tiles of chunk q
+  int g1need[MAX_K];     // GEMM1 (row, column) tiles of chunk q
   // per (chunk q, segment) at index q*nseg + seg
   int rows[MAX_K * MAX_SEG];
   int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts)
@@ -170,7 +44,7 @@ struct Sched {
 struct Scratch {
   int bc[8];
   long long ntk[KOPT];
-  int part[NTH];
+  int part[NWF];
   int sl[DT * MAX_TOPK];
   float wt[CT * MAX_TOPK];
 };
@@ -178,10 +52,10 @@ struct Scratch {
 // block-wide exclusive scan of n ints in LDS (all threads call): each thread
 // sums a contiguous run, wavefront shuffles scan the run sums, then the runs
 // are rewritten with their offsets
-__device__ void block_exscan(int* v, int n, int* part) {
+__device__ __forceinline__ void block_exscan(int* v, int n, int* part) {
   const int tid = threadIdx.x;
   const int lane = tid & (WAVE - 1), wave = tid / WAVE;
-  const int per = (n + NTH - 1) / NTH;
+  const int per = (n + FNTH - 1) / FNTH;
   const int b = tid * per, e = min(n, b + per);
   int mine = 0;
   for (int i = b; i < e; ++i) mine += v[i];
@@ -199,10 +73,11 @@ __device__ void block_exscan(int* v, int n, int* part) {
   __syncthreads();
 }
 
-__device__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
+__device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
   const int tid = threadIdx.x;
   const int ki = kopt_index(K);
   const int nseg = a.El + a.S;
+  const int g1tiles = a.nt1 * a.nsplit;  // GEMM1 tiles per row tile
   if (tid == 0) {
     S.K = K;
     S.nseg = nseg;
@@ -215,7 +90,7 @@ __device__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
     S.n_disp = ceil_div(a.T, DT);
   }
   __syncthreads();
-  for (int v = tid; v < K * nseg; v += NTH) {
+  for (int v = tid; v < K * nseg; v += FNTH) {
     int q = v / nseg, seg = v % nseg;
     int rows, row0, arow0;
     if (seg < a.El) {
@@ -236,10 +111,9 @@ __device__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
     S.mb[v] = ceil_div(rows, BM);
   }
   __syncthreads();
-  // group sizes in queue order: chunk, then phase (GEMM0, GEMM1), then segment
-  for (int gi = tid; gi < S.G; gi += NTH) {
+  for (int gi = tid; gi < S.G; gi += FNTH) {
     int q = gi / (2 * nseg), ph = (gi / nseg) & 1, seg = gi % nseg;
-    S.gstart[gi] = S.mb[q * nseg + seg] * (ph ? a.nt1 : a.nt0);
+    S.gstart[gi] = S.mb[q * nseg + seg] * (ph ? g1tiles : a.nt0);
   }
   if (tid == 0) S.gstart[S.G] = 0;
   if (tid < K) {
@@ -259,39 +133,40 @@ __device__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
 // once and written to all its local slots) and combine (weighted sum of the
 // expert outputs of each token into the output staging region).
 // ===========================================================================
-__device__ void dispatch_unit(const FwdArgs& a, const Sched* S, Scratch& W, int u, bool signal) {
+__device__ __forceinline__ void dispatch_unit(const FwdArgs& a, const Sched* S, Scratch& W, int u, bool signal) {
   const int tid = threadIdx.x;
   const int g0 = u * DT;
   const int nt = min(DT, a.T - g0);
   const int k = a.k;
-  for (int i = tid; i < nt * k; i += NTH) W.sl[i] = a.slot[(size_t)g0 * k + i];
+  for (int i = tid; i < nt * k; i += FNTH) W.sl[i] = a.slot[(size_t)g0 * k + i];
   __syncthreads();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
-  for (int v0 = tid; v0 < total; v0 += 4 * NTH) {
-    u32x4_t val[4];
-    int tt[4], cc[4];
+  constexpr int VB = 16;  // 16-byte vectors per thread in flight (a whole unit for H <= 8192)
+  for (int v0 = tid; v0 < total; v0 += VB * FNTH) {
+    u32x4_t val[VB];
+    int tt[VB], cc[VB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int v = v0 + i * NTH;
+    for (int i = 0; i < VB; ++i) {
+      const int v = v0 + i * FNTH;
       tt[i] = -1;
       if (v < total) {
-        int t = v / VPR;
-        int c = v - t * VPR;
+        const int t = v / VPR;
+        const int c = v - t * VPR;
         bool any = false;
         for (int j = 0; j < k; ++j) any |= (unsigned)W.sl[t * k + j] < (unsigned)a.xmax;
         if (any) {
           tt[i] = t;
           cc[i] = c;
-          val[i] = *reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + t) * a.H + c * 8);
+          val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + t) * a.H + c * 8));
         }
       }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < VB; ++i) {
       if (tt[i] < 0) continue;
       for (int j = 0; j < k; ++j) {
-        int s = W.sl[tt[i] * k + j];
+        const int s = W.sl[tt[i] * k + j];
         if ((unsigned)s < (unsigned)a.xmax) *reinterpret_cast<u32x4_t*>(a.A + (size_t)s * a.H + cc[i] * 8) = val[i];
       }
     }
@@ -316,40 +191,46 @@ __device__ void dispatch_unit(const FwdArgs& a, const Sched* S, Scratch& W, int 
   __syncthreads();
 }
 
-__device__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
+__device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
   const int tid = threadIdx.x;
   const int k = a.k;
-  for (int i = tid; i < nt * k; i += NTH) {
+  for (int i = tid; i < nt * k; i += FNTH) {
     W.sl[i] = a.slot[(size_t)g0 * k + i];
     W.wt[i] = a.topk_w[(size_t)g0 * k + i];
   }
   __syncthreads();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
-  for (int v = tid; v < total; v += NTH) {
+  for (int v = tid; v < total; v += FNTH) {
     int t = v / VPR, c = v - t * VPR;
     int g = g0 + t;
+    u32x4_t o[MAX_TOPK];
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) {
+      const int s = j < k ? W.sl[t * k + j] : -1;
+      if ((unsigned)s < (unsigned)a.xmax) o[j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + c * 8);
+    }
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-    for (int j = 0; j < k; ++j) {
-      int s = W.sl[t * k + j];
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) {
+      const int s = j < k ? W.sl[t * k + j] : -1;
       if ((unsigned)s >= (unsigned)a.xmax) continue;
-      float w = W.wt[t * k + j];
-      u32x4_t o = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + c * 8);
+      const float w = W.wt[t * k + j];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += w * bf16_lo(o[q]);
-        acc[2 * q + 1] += w * bf16_hi(o[q]);
+        acc[2 * q] += w * bf16_lo(o[j][q]);
+        acc[2 * q + 1] += w * bf16_hi(o[j][q]);
       }
     }
     if (g < a.Tr) {
       for (int s = 0; s < a.S; ++s) {
-        u32x4_t o = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)(a.xmax + s * a.Tr + g) * a.H + c * 8);
+        u32x4_t os = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)(a.xmax + s * a.Tr + g) * a.H + c * 8);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += bf16_lo(o[q]);
-          acc[2 * q + 1] += bf16_hi(o[q]);
+          acc[2 * q] += bf16_lo(os[q]);
+          acc[2 * q + 1] += bf16_hi(os[q]);
         }
       }
     }
@@ -362,16 +243,14 @@ __device__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
 }
 
 // ===========================================================================
-// Compute work: one tile of GEMM0 (+SiLU*up) or GEMM1 for (chunk, segment,
-// row tile, column tile).  Within a group the row tile runs fastest, so
-// consecutive claims share the same weight columns.
+// Compute work: one tile of GEMM0 (+SiLU*up) or one split of a GEMM1 tile.
 // ===========================================================================
 struct TileRef {
-  int q, ph, seg, mt, nt, rows;
+  int q, ph, seg, mt, nt, ks, rows;
 };
 
 __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S, int t) {
-  int lo = 0, hi = S.G;  // find last gi with gstart[gi] <= t
+  int lo = 0, hi = S.G;  // the group gi with gstart[gi] <= t < gstart[gi+1]
   while (hi - lo > 1) {
     int mid = (lo + hi) >> 1;
     if (S.gstart[mid] <= t) lo = mid; else hi = mid;
@@ -383,37 +262,86 @@ __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S,
   int local = t - S.gstart[lo];
   const int rows = S.rows[r.q * S.nseg + r.seg];
   const int nmt = ceil_div(rows, BM);
+  if (r.ph == 0) {
+    r.ks = 0;
+  } else {
+    r.ks = local % a.nsplit;
+    local /= a.nsplit;
+  }
   r.mt = local % nmt;
   r.nt = local / nmt;
   r.rows = min(BM, rows - r.mt * BM);
   return r;
 }
 
-__device__ void run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* smem) {
+__device__ __forceinline__ void signal_done(int* p) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Runs the tile; returns true when it completed an output tile (GEMM0 tile,
+// or the last-arriving split of a GEMM1 tile, which did the reduction).
+// One mainloop instance serves both GEMMs; only the operands and the
+// epilogue differ.
+__device__ __forceinline__ bool run_gemm(const FwdArgs& a, const Sched& S, Scratch& W, const TileRef& r, int mtile_id,
+                                         char* ring) {
   const int qs = r.q * S.nseg + r.seg;
   const size_t orow = (size_t)S.row0[qs] + (size_t)r.mt * BM;
   const int n0 = r.nt * BN;
+  const uint16_t* Aop;
+  const uint16_t* Bop;
+  int ld, b_rows, Kd;
   if (r.ph == 0) {
     const size_t arow = (size_t)S.arow0[qs] + (size_t)r.mt * BM;
-    const uint16_t* Aop = (r.seg < a.El ? a.A : a.x) + arow * a.H;
-    const size_t two_f = 2 * (size_t)a.F;
-    const uint16_t* Bop = a.w13 + (size_t)r.seg * two_f * a.H + (size_t)n0 * a.H;
-    uint16_t* out = a.Hb + orow * a.F + n0 / 2;
-    gemm_tile<0>(Aop, a.H, r.rows, Bop, a.H, (int)(two_f - n0), a.H, out, a.F, r.rows, a.F - n0 / 2,
-                 smem);
+    Aop = (r.seg < a.El ? a.A : a.x) + arow * a.H;
+    Bop = a.w13 + ((size_t)r.seg * 2 * a.F + n0) * a.H;
+    ld = a.H;
+    b_rows = 2 * a.F - n0;
+    Kd = a.H;
   } else {
-    const uint16_t* Aop = a.Hb + orow * a.F;
-    const uint16_t* Bop = a.w2t + (size_t)r.seg * a.H * a.F + (size_t)n0 * a.F;
-    uint16_t* out = a.O + orow * a.H + n0;
-    gemm_tile<1>(Aop, a.F, r.rows, Bop, a.F, a.H - n0, a.F, out, a.H, r.rows, a.H - n0, smem);
+    const int kl = a.F / a.nsplit;
+    Aop = a.Hb + orow * a.F + (size_t)r.ks * kl;
+    Bop = a.w2t + ((size_t)r.seg * a.H + n0) * a.F + (size_t)r.ks * kl;
+    ld = a.F;
+    b_rows = a.H - n0;
+    Kd = kl;
   }
+  gemm::Acc acc;
+  gemm::zero(acc);
+  gemm::mainloop(acc, Aop, ld, r.rows, Bop, ld, b_rows, Kd, ring);
+  if (r.ph == 0) {
+    gemm::store_silu_mul(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
+    return true;
+  }
+  uint16_t* out = a.O + orow * a.H + n0;
+  if (a.nsplit == 1) {
+    gemm::store_bf16(acc, out, a.H, r.rows, a.H - n0);
+    return true;
+  }
+  // split-K: publish this split's partial; the last arrival reduces in order
+  const size_t tile = (size_t)mtile_id * a.nt1 + r.nt;
+  float* parts = a.part + tile * a.nsplit * (size_t)(BM * BN);
+  gemm::store_partial(acc, parts + (size_t)r.ks * (BM * BN));
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    W.bc[3] = __hip_atomic_fetch_add(&a.ctl[CTL_READY + 2 * a.mt_max + tile], 1, __ATOMIC_RELEASE,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const bool last = W.bc[3] == a.nsplit - 1;
+  __syncthreads();
+  if (!last) return false;
+  if (a.nsplit == 2) gemm::reduce_store<2>(parts, (size_t)(BM * BN), out, a.H, r.rows, a.H - n0);
+  else gemm::reduce_store<4>(parts, (size_t)(BM * BN), out, a.H, r.rows, a.H - n0);
+  return true;
 }
 
 // ===========================================================================
 // Prologue: the routing-derived workload and the plan (sections 3.1-3.3),
 // computed redundantly by every workgroup from a small read of the stats.
 // ===========================================================================
-__device__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
+__device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   const int tid = threadIdx.x;
   const int nseg = a.El + a.S;
   if (tid < KOPT) W.ntk[tid] = 0;
@@ -422,7 +350,7 @@ __device__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   for (int ki = 0; ki < KOPT; ++ki) {
     const int K = kopt_value(ki);
     long long part = 0;
-    for (int v = tid; v < K * nseg; v += NTH) {
+    for (int v = tid; v < K * nseg; v += FNTH) {
       int q = v / nseg, seg = v % nseg;
       int rows;
       if (seg < a.El) {
@@ -433,7 +361,7 @@ __device__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
         int t1 = min((int)(((long long)(q + 1) * a.T + K - 1) / K), a.Tr);
         rows = max(0, t1 - t0);
       }
-      part += (long long)ceil_div(rows, BM) * (a.nt0 + a.nt1);
+      part += (long long)ceil_div(rows, BM) * (a.nt0 + a.nt1 * a.nsplit);
     }
     if (part) atomicAdd((unsigned long long*)&W.ntk[ki], (unsigned long long)part);
   }
@@ -464,13 +392,21 @@ __device__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   __syncthreads();
 }
 
-__device__ bool wait_geq(const FwdArgs& a, Scratch& W, const int* p, int target) {
+// Waits until *p >= target.  Thread 0 polls with relaxed agent-scope loads
+// (coherent across XCDs, no cache invalidation: an acquire here would
+// invalidate this XCD's L2 on every poll, under the GEMM tiles of the other
+// workgroups).  No acquire is needed for the data that follows: producers
+// write back their L2 before publishing (release), and no CU reads a
+// dispatched row, an Hbuf/O row or a partial before it is published, so no
+// stale copy of those lines can sit in the consumer's L1 or L2 (caches are
+// invalidated at kernel start).
+__device__ __forceinline__ bool wait_geq(const FwdArgs& a, Scratch& W, const int* p, int target) {
   if (a.inject_stall) target += 1 << 30;
   if (threadIdx.x == 0) {
     int ok = 1;
-    if (ld_acquire(p) < target) {
+    if (ld_relaxed(p) < target) {
       const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
-      while (ld_acquire(p) < target) {
+      while (ld_relaxed(p) < target) {
         if (ld_relaxed(&a.ctl[CTL_ABORT])) { ok = 0; break; }
         if (now_ticks() > deadline) {
           st_relaxed(&a.ctl[CTL_ABORT], 1);
@@ -497,29 +433,22 @@ __device__ __forceinline__ int claim(Scratch& W, int* q) {
   return r;
 }
 
-__device__ __forceinline__ void signal_done(int* p) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // returns false when the launch was aborted
-__device__ bool run_compute_tile(const FwdArgs& a, const Sched& S, Scratch& W, int t, char* smem) {
+__device__ __forceinline__ bool run_compute_tile(const FwdArgs& a, const Sched& S, Scratch& W, int t, char* ring) {
   TileRef r = decode_tile(a, S, t);
   const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
   if (r.ph == 0) {
     if (r.seg < a.El && !wait_geq(a, W, &a.ctl[CTL_READY + id], r.rows)) return false;
-    run_gemm(a, S, r, smem);
+    run_gemm(a, S, W, r, id, ring);
     signal_done(&a.ctl[CTL_READY + a.mt_max + id]);
   } else {
     if (!wait_geq(a, W, &a.ctl[CTL_READY + a.mt_max + id], a.nt0)) return false;
-    run_gemm(a, S, r, smem);
-    signal_done(&a.ctl[CTL_G1DONE + r.q]);
+    if (run_gemm(a, S, W, r, id, ring)) signal_done(&a.ctl[CTL_G1DONE + r.q]);
   }
   return true;
 }
 
-__device__ bool combine_loop(const FwdArgs& a, const Sched& S, Scratch& W) {
+__device__ __forceinline__ bool combine_loop(const FwdArgs& a, const Sched& S, Scratch& W) {
   for (;;) {
     int u = claim(W, &a.ctl[CTL_Q_COMB]);
     if (u >= S.n_comb) return true;
@@ -536,14 +465,14 @@ __device__ bool combine_loop(const FwdArgs& a, const Sched& S, Scratch& W) {
 // The persistent megakernel: one workgroup per CU, co-resident (cooperative
 // launch).  The first c workgroups to arrive become movement workers.
 // ===========================================================================
-__global__ void __launch_bounds__(NTH, 1) moe_megakernel(FwdArgs a) {
+__global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   __shared__ Sched S;
   __shared__ Scratch W;
-  __shared__ __attribute__((aligned(16))) char smem[GEMM_SMEM];
+  __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
   const int tid = threadIdx.x;
 
   if (blockIdx.x == 0)
-    for (int i = tid; i < a.ctl_words; i += NTH) a.ctl_next[i] = 0;
+    for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
 
   prologue_plan(a, S, W);
   build_sched(a, S, W, S.K);
@@ -564,14 +493,14 @@ __global__ void __launch_bounds__(NTH, 1) moe_megakernel(FwdArgs a) {
     for (int i = 0; i < S.n_steal; ++i) {
       int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, smem)) return;
+      if (!run_compute_tile(a, S, W, t, ring)) return;
     }
     combine_loop(a, S, W);
   } else {
     for (;;) {
       int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, smem)) return;
+      if (!run_compute_tile(a, S, W, t, ring)) return;
     }
     // final combine on every worker (section 4)
     if (S.final_all) combine_loop(a, S, W);
@@ -581,11 +510,11 @@ __global__ void __launch_bounds__(NTH, 1) moe_megakernel(FwdArgs a) {
 // ===========================================================================
 // Serial baseline: four kernels, each on every CU, no overlap.
 // ===========================================================================
-__global__ void __launch_bounds__(NTH, 1) serial_dispatch_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {
   __shared__ Scratch W;
   const int tid = threadIdx.x;
   if (blockIdx.x == 0)
-    for (int i = tid; i < a.ctl_words; i += NTH) a.ctl_next[i] = 0;
+    for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
   const int n = ceil_div(a.T, DT);
   for (;;) {
     int u = claim(W, &a.ctl[CTL_SQ + 0]);
@@ -595,10 +524,10 @@ __global__ void __launch_bounds__(NTH, 1) serial_dispatch_kernel(FwdArgs a) {
 }
 
 template <int PH>
-__device__ void serial_gemm(const FwdArgs& a, int qslot) {
+__device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
   __shared__ Sched S;
   __shared__ Scratch W;
-  __shared__ __attribute__((aligned(16))) char smem[GEMM_SMEM];
+  __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
   build_sched(a, S, W, 1);
   const int first = S.gstart[PH * S.nseg];
   const int count = S.gstart[(PH + 1) * S.nseg] - first;
@@ -606,14 +535,14 @@ __device__ void serial_gemm(const FwdArgs& a, int qslot) {
     int t = claim(W, &a.ctl[CTL_SQ + 64 * qslot]);
     if (t >= count) break;
     TileRef r = decode_tile(a, S, first + t);
-    run_gemm(a, S, r, smem);
+    run_gemm(a, S, W, r, S.mb[r.q * S.nseg + r.seg] + r.mt, ring);
   }
 }
 
-__global__ void __launch_bounds__(NTH, 1) serial_gemm0_kernel(FwdArgs a) { serial_gemm<0>(a, 1); }
-__global__ void __launch_bounds__(NTH, 1) serial_gemm1_kernel(FwdArgs a) { serial_gemm<1>(a, 2); }
+__global__ void __launch_bounds__(FNTH, 1) serial_gemm0_kernel(FwdArgs a) { serial_gemm<0>(a, 1); }
+__global__ void __launch_bounds__(FNTH, 1) serial_gemm1_kernel(FwdArgs a) { serial_gemm<1>(a, 2); }
 
-__global__ void __launch_bounds__(NTH, 1) serial_combine_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   __shared__ Scratch W;
   const int n = ceil_div(a.T, CT);
   for (;;) {

@@ -1,0 +1,323 @@
+// Grouped-GEMM tile for gfx950: C[256 x 256] = A[256 x K] * B[256 x K]^T on
+// bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
+//
+// Workgroup of 8 wave64s (2 per SIMD), wave grid 2 (rows) x 4 (columns), each
+// wave owns 128 x 64 outputs = 4 x 2 MFMA blocks (128 accumulator registers).
+// A and B stream through a 4-stage LDS ring of BK = 32 deep stages filled by
+// direct global->LDS loads (global_load_lds_dwordx4), issued 3 stages ahead.
+// Rows are 64 bytes; their 16-byte granules are XOR-swizzled by (row >> 1) & 3
+// so fragment reads are free of bank conflicts.  The fragments of the second
+// 16-deep slice of a stage are read while the MFMAs of the first run, and the
+// next stage's barrier sits between the two slices.
+//
+// Ragged tiles: rows past the valid count are loaded from the last valid row
+// (never out of bounds) and their outputs are not stored; every output
+// element depends only on its own A row and B row.
+#pragma once
+
+#include "common.h"
+
+namespace moe {
+
+namespace gemm {
+
+constexpr int TILE_M = 256, TILE_N = 256, KSTEP = 32, NSTAGE = 4;
+constexpr int NWAVE = 8, WM = 2, WN = 4;
+constexpr int TM = TILE_M / WM, TN = TILE_N / WN;   // 128 x 64 per wave
+constexpr int MB = TM / 32, NB = TN / 32;           // 4 x 2 MFMA blocks
+constexpr int A_BYTES = TILE_M * KSTEP * 2, B_BYTES = TILE_N * KSTEP * 2;
+constexpr int STAGE_BYTES = A_BYTES + B_BYTES;      // 32 KiB
+constexpr int RING_BYTES = NSTAGE * STAGE_BYTES;    // 128 KiB
+constexpr int A_INSTR = A_BYTES / 1024 / NWAVE;     // DMA instructions per wave per stage
+constexpr int B_INSTR = B_BYTES / 1024 / NWAVE;
+constexpr int INSTR = A_INSTR + B_INSTR;
+
+typedef f32x16_t Acc[MB][NB];
+
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 1) & 3)); }
+
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// one 16-byte-per-lane DMA: M0 = wave's LDS destination, lane address =
+// uniform base + 32-bit offset.  Issued through asm so that the waits stay
+// under the mainloop's explicit control (the compiler would otherwise drain
+// every outstanding DMA before each LDS read it cannot disambiguate).  No
+// other code of these kernels keeps a value in M0 across this statement.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const char* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// values that are uniform by construction, made visibly uniform (SGPRs)
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const char*>(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// Uniform, opaque copy of a scalar: broadcast from the first lane (the value
+// is uniform by construction) and hidden from the optimiser, so expressions
+// built from it cannot be hoisted above this point.  Used on the scalars of
+// each tile so that a persistent loop does not keep the address arithmetic of
+// every epilogue live across the mainloop.
+__device__ __forceinline__ int opaque(int v) {
+  v = __builtin_amdgcn_readfirstlane(v);
+  asm volatile("" : "+s"(v));
+  return v;
+}
+__device__ __forceinline__ size_t opaque(size_t v) {
+  uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  asm volatile("" : "+s"(lo), "+s"(hi));
+  return ((size_t)hi << 32) | lo;
+}
+template <typename T>
+__device__ __forceinline__ T* opaque(T* p) {
+  return reinterpret_cast<T*>(opaque((size_t)p));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+struct DmaOff {
+  uint32_t a[A_INSTR], b[B_INSTR];
+};
+
+__device__ __forceinline__ void dma_offsets(DmaOff& o, int lda, int a_rows, int ldb, int b_rows) {
+  lda = opaque(lda);
+  ldb = opaque(ldb);
+  a_rows = opaque(a_rows);
+  b_rows = opaque(b_rows);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < A_INSTR; ++i) {
+    const int g = (wave * A_INSTR + i) * 64 + lane;
+    const int row = g >> 2, c = (g & 3) ^ ((row >> 1) & 3);
+    const int r = row < a_rows ? row : a_rows - 1;
+    o.a[i] = (uint32_t)(r * lda + c * 8) * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INSTR; ++i) {
+    const int g = (wave * B_INSTR + i) * 64 + lane;
+    const int row = g >> 2, c = (g & 3) ^ ((row >> 1) & 3);
+    const int r = row < b_rows ? row : b_rows - 1;
+    o.b[i] = (uint32_t)(r * ldb + c * 8) * 2u;
+  }
+}
+
+__device__ __forceinline__ void issue_stage(char* stage, const char* A, const char* B, const DmaOff& o, int k0) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const char* Ak = uniform_ptr(A + (size_t)k0 * 2);
+  const char* Bk = uniform_ptr(B + (size_t)k0 * 2);
+  const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds_u32(stage));
+#pragma unroll
+  for (int i = 0; i < A_INSTR; ++i) dma16(Ak, o.a[i], l0 + (wave * A_INSTR + i) * 1024);
+#pragma unroll
+  for (int i = 0; i < B_INSTR; ++i) dma16(Bk, o.b[i], l0 + A_BYTES + (wave * B_INSTR + i) * 1024);
+}
+
+struct FragOff {
+  uint32_t a[2], b[2];
+};
+
+__device__ __forceinline__ FragOff frag_offsets() {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int ra = wm * TM + (lane & 31), rb = wn * TN + (lane & 31);
+  FragOff f;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int c = kk * 2 + (lane >> 5);
+    f.a[kk] = (uint32_t)swz(ra, c) * 16u;
+    f.b[kk] = (uint32_t)(A_BYTES + swz(rb, c) * 16);
+  }
+  return f;
+}
+
+// 32-row blocks are 2048 bytes apart and keep the same swizzle, so every
+// fragment of a slice is a constant offset from the lane's base
+__device__ __forceinline__ void load_frags(const char* stage, int kk, const FragOff& fo, bf16x8_t (&af)[MB],
+                                           bf16x8_t (&bfr)[NB]) {
+  const char* pa = stage + fo.a[kk];
+  const char* pb = stage + fo.b[kk];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(pa + mb * 2048);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(pb + nb * 2048);
+}
+
+__device__ __forceinline__ void mfma_block(Acc& acc, const bf16x8_t (&af)[MB], const bf16x8_t (&bfr)[NB]) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
+}
+
+// acc += A[0..a_rows) . B[0..b_rows)^T over k in [0, Kd); Kd % 32 == 0.
+// ring: RING_BYTES of LDS.  Ends with a barrier (the ring may be reused).
+__device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int ldb,
+                                         int b_rows, int Kd, char* ring) {
+  const int nk = Kd / KSTEP;
+  DmaOff o;
+  dma_offsets(o, lda, a_rows, ldb, b_rows);
+  const char* Ab = reinterpret_cast<const char*>(A);
+  const char* Bb = reinterpret_cast<const char*>(B);
+  auto st = [&](int s) { return ring + (s & (NSTAGE - 1)) * STAGE_BYTES; };
+  issue_stage(st(0), Ab, Bb, o, 0);
+  if (nk > 1) issue_stage(st(1), Ab, Bb, o, KSTEP);
+  if (nk > 2) issue_stage(st(2), Ab, Bb, o, 2 * KSTEP);
+  if (nk > 2) wait_vm<2 * INSTR>(); else if (nk > 1) wait_vm<INSTR>(); else wait_vm<0>();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+  bf16x8_t fa0[MB], fb0[NB], fa1[MB], fb1[NB];
+  const FragOff fo = frag_offsets();
+  load_frags(st(0), 0, fo, fa0, fb0);
+  int s = 0;
+  for (; s < nk - 3; ++s) {  // steady state: the stage 3 ahead is always issued
+    load_frags(st(s), 1, fo, fa1, fb1);
+    mfma_block(acc, fa0, fb0);
+    wait_vm<INSTR>();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue_stage(st(s + 3), Ab, Bb, o, (s + 3) * KSTEP);
+    load_frags(st(s + 1), 0, fo, fa0, fb0);
+    mfma_block(acc, fa1, fb1);
+  }
+  for (; s < nk; ++s) {  // drain
+    load_frags(st(s), 1, fo, fa1, fb1);
+    mfma_block(acc, fa0, fb0);
+    if (s + 1 < nk) {
+      if (s + 2 < nk) wait_vm<INSTR>(); else wait_vm<0>();
+      __builtin_amdgcn_s_barrier();
+      compiler_fence();
+      load_frags(st(s + 1), 0, fo, fa0, fb0);
+    }
+    mfma_block(acc, fa1, fb1);
+  }
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+}
+
+__device__ __forceinline__ void zero(Acc& acc) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.0f;
+}
+
+// Output coordinates of accumulator element r of block (mb, nb): column
+// col_l + nb*32 and row row_l + dr(mb, r) of the tile.
+struct OutMap {
+  int row_l, col_l;
+};
+__device__ __forceinline__ OutMap out_map(int cols_per_wave) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  return {wm * TM + 4 * (lane >> 5), wn * cols_per_wave + (lane & 31)};
+}
+__device__ __forceinline__ int out_dr(int mb, int r) { return mb * 32 + 8 * (r >> 2) + (r & 3); }
+
+// GEMM0 epilogue: gate/up 32-column pairs -> bf16(silu(gate) * up); the tile
+// writes TILE_N/2 output columns
+__device__ __forceinline__ void store_silu_mul(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
+  ldo = opaque(ldo);
+  const OutMap m = out_map(TN / 2);
+  const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int dr = out_dr(mb, r);
+      if (m.row_l + dr < out_rows && m.col_l < out_cols) {
+        const float g = acc[mb][0][r], u = acc[mb][1][r];
+        const float hv = (g / (1.0f + __expf(-g))) * u;
+        out[base + (uint32_t)(dr * ldo)] = (uint16_t)f32_to_bf16(hv);
+      }
+    }
+}
+
+// GEMM1 epilogue: bf16(acc) into the tile
+__device__ __forceinline__ void store_bf16(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
+  ldo = opaque(ldo);
+  const OutMap m = out_map(TN);
+  const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int dr = out_dr(mb, r);
+      if (m.row_l + dr < out_rows) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          if (m.col_l + nb * 32 < out_cols)
+            out[base + (uint32_t)(dr * ldo) + nb * 32] = (uint16_t)f32_to_bf16(acc[mb][nb][r]);
+      }
+    }
+}
+
+// split-K partial: fp32 tile in the lane-natural order (tile-contiguous,
+// 256 x 256 floats), read back by store_reduce with the same map
+__device__ __forceinline__ void store_partial(const Acc& acc, float* part) {
+  part = opaque(part);
+  const OutMap m = out_map(TN);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m.row_l + out_dr(mb, r);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) part[row * TILE_N + m.col_l + nb * 32] = acc[mb][nb][r];
+    }
+}
+
+// split-K reduction in fixed order: P_0 + P_1 + ... + P_{S-1}, every partial
+// read back from memory (this split's own included, so the accumulators are
+// dead here), one 32-row block at a time; then bf16 into the tile
+template <int S>
+__device__ __forceinline__ void reduce_store(const float* parts, size_t part_stride, uint16_t* out, int ldo,
+                                             int out_rows, int out_cols) {
+  parts = opaque(parts);
+  part_stride = opaque(part_stride);
+  ldo = opaque(ldo);
+  const OutMap m = out_map(TN);
+  const uint32_t lbase = (uint32_t)(m.row_l * TILE_N + m.col_l);
+  const uint32_t obase = (uint32_t)(m.row_l * ldo + m.col_l);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    float v[S][16][NB];
+#pragma unroll
+    for (int k = 0; k < S; ++k)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) v[k][r][nb] = parts[k * part_stride + lbase + out_dr(mb, r) * TILE_N + nb * 32];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int dr = out_dr(mb, r);
+      if (m.row_l + dr < out_rows) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          float t = v[0][r][nb];
+#pragma unroll
+          for (int k = 1; k < S; ++k) t += v[k][r][nb];
+          if (m.col_l + nb * 32 < out_cols) out[obase + (uint32_t)(dr * ldo) + nb * 32] = (uint16_t)f32_to_bf16(t);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace gemm
+}  // namespace moe

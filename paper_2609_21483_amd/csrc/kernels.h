@@ -58,6 +58,7 @@ struct FwdArgs {
   // shape
   int T, Tr, R, H, F, k, El, S, e0, N;
   int nt0, nt1;   // column tiles of GEMM0 (over 2F) and GEMM1 (over H)
+  int nsplit;     // split-K factor of GEMM1 (1, 2 or 4)
   int xmax;       // rows reserved for routed pairs in A / Hbuf / O
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
@@ -76,6 +77,7 @@ struct FwdArgs {
   uint16_t* A;
   uint16_t* Hb;
   uint16_t* O;
+  float* part;    // split-K partials (nsplit > 1)
   // control
   int32_t* ctl;       // this launch's control set
   int32_t* ctl_next;  // cleared for the next launch
