@@ -32,21 +32,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_ep4")
     ap.add_argument("--layer", type=int, default=0)
-    ap.add_argument("--calib", default=os.path.join(ROOT, "paper_2609_21483_amd", "calib_mi355x.json"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128)
     ap.add_argument("--modes", default="static,serial", help="baselines timed next to the dynamic mode")
     return ap.parse_args()
-
-
-def load_calib(B, path, N):
-    if not path or not os.path.exists(path):
-        return None
-    d = json.load(open(path))
-    if int(d.get("N", N)) != N:
-        return None
-    return B.make_calib(d["c"], d["bw"], d["flops"], d["K"], d["eff"], d["alpha"], d["static_c"],
-                        d.get("literal", 0))
 
 
 def time_forward(B, layer, x, idx, w, y, mode, steps, warmup, stream):
@@ -113,7 +102,8 @@ def main():
     c = {"x": W.tokens(shape), "wg": W.gate(shape, layer_id), "bias": W.zipf_log_prior(shape, layer_id)}
     c["w1"], c["w3"], c["w2"] = W.experts(shape, layer_id)
     c["ws1"], c["ws3"], c["ws2"] = W.shared_experts(shape, layer_id)
-    calib = load_calib(B, args.calib, N)
+    from paper_2609_21483_amd.calibrate import load_calib
+    calib = load_calib(shape.name, N)
     layer = B.MoeLayer(shape, c["w1"], c["w3"], c["w2"], c["ws1"], c["ws3"], c["ws2"], calib=calib)
     stream = torch.cuda.current_stream()
     x = c["x"].cuda()
@@ -194,7 +184,7 @@ def main():
         "layer_tokens_per_s": shape.T / (lat * 1e-6),
         "route_us": route_us,
         "plan": {"c": plan.c, "K": plan.K, "n_steal": plan.n_steal, "final_all": plan.final_all,
-                 "t_pred_us": plan.t_pred_s * 1e6, "N": N},
+                 "t_pred_us": plan.t_pred_s * 1e6, "N": N, "calibrated": calib is not None},
         "baselines": baselines,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,

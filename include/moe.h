@@ -206,6 +206,17 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
                        const float* topk_w, const void* packed, uint16_t* y,
                        int32_t mode, const moe_plan* forced, void* stream);
 
+/* Calibration of the cost model's hardware curves (BW(c), TFLOPS(N-c),
+ * eff_chunk(K); Fig 4a/b, Fig 7a): runs the selected stages of the layer as
+ * separate kernels on n_workers workgroups.  stages: bit 0 dispatch, bit 1
+ * GEMM0 + SiLU*up, bit 2 GEMM1, bit 3 combine; the GEMMs use the tiling of K
+ * chunks.  A stage reads what the earlier stages wrote, so a partial mask is
+ * meant for timing (after a full run), not for producing y.  Same arguments
+ * and table requirement as moe_forward. */
+moe_status moe_run_stages(moe_handle* h, const uint16_t* x, const int32_t* topk_idx,
+                          const float* topk_w, const void* packed, uint16_t* y,
+                          int32_t stages, int32_t n_workers, int32_t K, void* stream);
+
 /* Copies the plan of the last megakernel launch to *out (host).  Synchronises
  * the stream. */
 moe_status moe_get_plan(moe_handle* h, moe_plan* out, void* stream);

@@ -93,6 +93,7 @@ _SIGS = {
     "moe_route": ([_H, _P, _P, _P, C.c_int32, _P, _P, _P], C.c_int),
     "moe_build_tables": ([_H, _P, _P], C.c_int),
     "moe_forward": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.POINTER(moe_plan), _P], C.c_int),
+    "moe_run_stages": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P], C.c_int),
     "moe_get_plan": ([_H, C.POINTER(moe_plan), _P], C.c_int),
     "moe_sync_status": ([_H, _P], C.c_int),
     "moe_plan_host": ([_H, C.c_double, C.c_double, C.c_double, C.POINTER(C.c_int64), C.POINTER(moe_plan)], C.c_int),
@@ -204,6 +205,12 @@ def moe_forward(h: int, x, topk_idx, topk_w, packed, y, mode: int = MOE_MODE_DYN
     _check("moe_forward", _lib.moe_forward(h, _ptr(x), _ptr(topk_idx), _ptr(topk_w), _ptr(packed), _ptr(y),
                                            int(mode), C.byref(forced) if forced is not None else None,
                                            _stream(stream)))
+
+
+def moe_run_stages(h: int, x, topk_idx, topk_w, packed, y, stages: int, n_workers: int, K: int = 1,
+                   stream=None) -> None:
+    _check("moe_run_stages", _lib.moe_run_stages(h, _ptr(x), _ptr(topk_idx), _ptr(topk_w), _ptr(packed), _ptr(y),
+                                                 int(stages), int(n_workers), int(K), _stream(stream)))
 
 
 def moe_get_plan(h: int, stream=None) -> moe_plan:

@@ -204,6 +204,57 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
 
 }  // namespace
 
+
+namespace {
+FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, const float* topk_w, const void* packed,
+                 uint16_t* y, int32_t mode, const moe_plan* forced) {
+  const moe_config& c = h->cfg;
+  const int cur = (int)(h->launch_seq & 1ULL);
+  FwdArgs a{};
+  a.T = h->T;
+  a.Tr = c.tokens_per_rank;
+  a.R = c.n_src_ranks;
+  a.H = c.hidden;
+  a.F = c.ffn;
+  a.k = c.top_k;
+  a.El = c.n_local_experts;
+  a.S = c.n_shared_experts;
+  a.e0 = c.first_local_expert;
+  a.N = h->N;
+  a.nt0 = h->nt0;
+  a.nt1 = h->nt1;
+  a.nsplit = h->nsplit;
+  a.xmax = h->xmax;
+  a.mt_max = h->mt_max;
+  a.ctl_words = h->ctl_words;
+  a.x = x;
+  a.topk_idx = topk_idx;
+  a.topk_w = topk_w;
+  a.w13 = static_cast<const uint16_t*>(packed);
+  a.w2t = a.w13 + (size_t)h->nseg * 2 * c.ffn * c.hidden;
+  a.y = y;
+  a.slot = at<int32_t>(h, h->lay.slot);
+  a.sub_off = at<int32_t>(h, h->lay.sub_off);
+  a.stats = at<int32_t>(h, h->lay.stats);
+  a.A = at<uint16_t>(h, h->lay.A);
+  a.Hb = at<uint16_t>(h, h->lay.Hbuf);
+  a.O = at<uint16_t>(h, h->lay.O);
+  a.part = h->nsplit > 1 ? at<float>(h, h->off_part) : nullptr;
+  a.ctl = at<int32_t>(h, h->off_ctl[cur]);
+  a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
+  a.err = at<int32_t>(h, h->lay.err);
+  a.plan_out = at<moe_plan>(h, h->lay.plan);
+  a.calib = at<DevCalib>(h, h->off_calib);
+  a.mode = mode;
+  a.forced = forced ? 1 : 0;
+  if (forced) a.fplan = *forced;
+  a.timeout_ticks = h->timeout_ticks;
+  a.inject_stall = h->inject_stall;
+  a.serial_K = 1;
+  return a;
+}
+}  // namespace
+
 extern "C" {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
@@ -378,10 +429,28 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   g.H = h->cfg.hidden;
   g.E = h->cfg.n_experts;
   g.k = top_k;
-  const int EQ = (g.E + 3) / 4;
-  g.tq = std::max(1, std::min(64, NTH / EQ));
-  const int TT = 4 * g.tq;
-  gate_topk_kernel<<<(h->T + TT - 1) / TT, NTH, 0, s>>>(g);
+  // per-thread block of logits: the largest of 4x4, 2x2, 1x1 (tokens x
+  // experts) that still gives the grid enough workgroups
+  auto groups = [&](int tpt, int ept, int* tq) {
+    const int eq = (g.E + ept - 1) / ept;
+    if (eq > NTH) return -1;
+    int t = std::max(1, NTH / eq);
+    while (t * tpt > 256) --t;
+    *tq = t;
+    return (h->T + t * tpt - 1) / (t * tpt);
+  };
+  int tq44, tq22, tq11;
+  const int n44 = groups(4, 4, &tq44), n22 = groups(2, 2, &tq22), n11 = groups(1, 1, &tq11);
+  if (n44 >= 512 || (n22 < 0 && n11 < 0)) {
+    g.tq = tq44;
+    gate_topk_kernel<4, 4><<<n44, NTH, 0, s>>>(g);
+  } else if (n22 >= 256 || n11 < 0) {
+    g.tq = tq22;
+    gate_topk_kernel<2, 2><<<n22, NTH, 0, s>>>(g);
+  } else {
+    g.tq = tq11;
+    gate_topk_kernel<1, 1><<<n11, NTH, 0, s>>>(g);
+  }
   HIP_TRY(hipGetLastError());
   return moe_build_tables(h, topk_idx, stream);
 }
@@ -403,48 +472,7 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     if (forced->final_all != 0 && forced->final_all != 1) return fail(MOE_ERR_INVALID_ARG, "forced final_all must be 0 or 1");
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const moe_config& c = h->cfg;
-  const int cur = (int)(h->launch_seq & 1ULL);
-  FwdArgs a{};
-  a.T = h->T;
-  a.Tr = c.tokens_per_rank;
-  a.R = c.n_src_ranks;
-  a.H = c.hidden;
-  a.F = c.ffn;
-  a.k = c.top_k;
-  a.El = c.n_local_experts;
-  a.S = c.n_shared_experts;
-  a.e0 = c.first_local_expert;
-  a.N = h->N;
-  a.nt0 = h->nt0;
-  a.nt1 = h->nt1;
-  a.nsplit = h->nsplit;
-  a.xmax = h->xmax;
-  a.mt_max = h->mt_max;
-  a.ctl_words = h->ctl_words;
-  a.x = x;
-  a.topk_idx = topk_idx;
-  a.topk_w = topk_w;
-  a.w13 = static_cast<const uint16_t*>(packed);
-  a.w2t = a.w13 + (size_t)h->nseg * 2 * c.ffn * c.hidden;
-  a.y = y;
-  a.slot = at<int32_t>(h, h->lay.slot);
-  a.sub_off = at<int32_t>(h, h->lay.sub_off);
-  a.stats = at<int32_t>(h, h->lay.stats);
-  a.A = at<uint16_t>(h, h->lay.A);
-  a.Hb = at<uint16_t>(h, h->lay.Hbuf);
-  a.O = at<uint16_t>(h, h->lay.O);
-  a.part = h->nsplit > 1 ? at<float>(h, h->off_part) : nullptr;
-  a.ctl = at<int32_t>(h, h->off_ctl[cur]);
-  a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
-  a.err = at<int32_t>(h, h->lay.err);
-  a.plan_out = at<moe_plan>(h, h->lay.plan);
-  a.calib = at<DevCalib>(h, h->off_calib);
-  a.mode = mode;
-  a.forced = forced ? 1 : 0;
-  if (forced) a.fplan = *forced;
-  a.timeout_ticks = h->timeout_ticks;
-  a.inject_stall = h->inject_stall;
+  FwdArgs a = fwd_args(h, x, topk_idx, topk_w, packed, y, mode, forced);
   if (mode == MOE_MODE_SERIAL) {
     serial_dispatch_kernel<<<h->N, FNTH, 0, s>>>(a);
     serial_gemm0_kernel<<<h->N, FNTH, 0, s>>>(a);
@@ -455,6 +483,36 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     void* args[] = {&a};
     HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(FNTH), args, 0, s));
   }
+  h->launch_seq++;
+  return MOE_OK;
+}
+
+moe_status moe_run_stages(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, const float* topk_w,
+                          const void* packed, uint16_t* y, int32_t stages, int32_t n_workers, int32_t K, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!x || !topk_idx || !topk_w || !packed || !y) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (stages <= 0 || stages > 15) return fail(MOE_ERR_INVALID_ARG, "stages must be a non-empty mask of bits 0..3");
+  if (n_workers < 1 || n_workers > h->N) return fail(MOE_ERR_INVALID_ARG, "n_workers must be in [1, N]");
+  if (K != 1 && K != 2 && K != 4 && K != 8) return fail(MOE_ERR_INVALID_ARG, "K must be 1, 2, 4 or 8");
+  if (h->tables_from != topk_idx)
+    return fail(MOE_ERR_STATE, "routing tables were not built from this topk_idx (call moe_route or moe_build_tables)");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FwdArgs a = fwd_args(h, x, topk_idx, topk_w, packed, y, MOE_MODE_SERIAL, nullptr);
+  a.serial_K = K;
+  // the first kernel clears the next control set; run it even when not asked
+  // for, on zero tokens, so the control sets keep alternating
+  if (stages & 1) {
+    serial_dispatch_kernel<<<n_workers, FNTH, 0, s>>>(a);
+  } else {
+    FwdArgs z = a;
+    z.T = 0;
+    serial_dispatch_kernel<<<1, FNTH, 0, s>>>(z);
+  }
+  if (stages & 2) serial_gemm0_kernel<<<n_workers, FNTH, 0, s>>>(a);
+  if (stages & 4) serial_gemm1_kernel<<<n_workers, FNTH, 0, s>>>(a);
+  if (stages & 8) serial_combine_kernel<<<n_workers, FNTH, 0, s>>>(a);
+  HIP_TRY(hipGetLastError());
   h->launch_seq++;
   return MOE_OK;
 }

@@ -19,8 +19,8 @@ constexpr int BM = 256;
 constexpr int BN = 256;
 constexpr int MAX_SPLIT = 4;    // split-K factor limit of GEMM1
 
-constexpr int DT = 16;          // tokens per dispatch unit
-constexpr int CT = 16;          // tokens per combine unit
+constexpr int DT = 4;           // tokens per dispatch unit (one wavefront)
+constexpr int CT = 4;           // tokens per combine unit (one wavefront)
 
 constexpr int MAX_EL = 64;      // local experts
 constexpr int MAX_S = 8;        // shared experts

@@ -45,8 +45,8 @@ struct Scratch {
   int bc[8];
   long long ntk[KOPT];
   int part[NWF];
-  int sl[DT * MAX_TOPK];
-  float wt[CT * MAX_TOPK];
+  int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
+  float wwt[NWF][WAVE];  // per wavefront: their weights
 };
 
 // block-wide exclusive scan of n ints in LDS (all threads call): each thread
@@ -129,32 +129,45 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
 }
 
 // ===========================================================================
-// Movement work: dispatch (x rows -> expert-contiguous A slots, each row read
-// once and written to all its local slots) and combine (weighted sum of the
-// expert outputs of each token into the output staging region).
+// Movement work, one wavefront per unit (no workgroup barriers, so the eight
+// wavefronts of a movement worker overlap their latency chains):
+// dispatch copies the rows of DT tokens into their expert-contiguous A slots
+// (each row read once, written to every local slot); combine writes the
+// weighted sum of the expert outputs of CT tokens into the output staging
+// region.
 // ===========================================================================
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+
+__device__ __forceinline__ int wave_claim(int* q) {
+  int v = 0;
+  if (lane_id() == 0) v = fetch_add_relaxed(q, 1);
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
 __device__ __forceinline__ void dispatch_unit(const FwdArgs& a, const Sched* S, Scratch& W, int u, bool signal) {
-  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  int* sl = W.wsl[wave_id()];
   const int g0 = u * DT;
   const int nt = min(DT, a.T - g0);
   const int k = a.k;
-  for (int i = tid; i < nt * k; i += FNTH) W.sl[i] = a.slot[(size_t)g0 * k + i];
-  __syncthreads();
+  sl[lane] = lane < nt * k ? a.slot[(size_t)g0 * k + lane] : -1;
+  __builtin_amdgcn_wave_barrier();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
-  constexpr int VB = 16;  // 16-byte vectors per thread in flight (a whole unit for H <= 8192)
-  for (int v0 = tid; v0 < total; v0 += VB * FNTH) {
+  constexpr int VB = 16;  // 16-byte vectors per lane in flight
+  for (int v0 = lane; v0 < total; v0 += VB * WAVE) {
     u32x4_t val[VB];
     int tt[VB], cc[VB];
 #pragma unroll
     for (int i = 0; i < VB; ++i) {
-      const int v = v0 + i * FNTH;
+      const int v = v0 + i * WAVE;
       tt[i] = -1;
       if (v < total) {
         const int t = v / VPR;
         const int c = v - t * VPR;
         bool any = false;
-        for (int j = 0; j < k; ++j) any |= (unsigned)W.sl[t * k + j] < (unsigned)a.xmax;
+        for (int j = 0; j < k; ++j) any |= (unsigned)sl[t * k + j] < (unsigned)a.xmax;
         if (any) {
           tt[i] = t;
           cc[i] = c;
@@ -166,80 +179,110 @@ __device__ __forceinline__ void dispatch_unit(const FwdArgs& a, const Sched* S, 
     for (int i = 0; i < VB; ++i) {
       if (tt[i] < 0) continue;
       for (int j = 0; j < k; ++j) {
-        const int s = W.sl[tt[i] * k + j];
+        const int s = sl[tt[i] * k + j];
         if ((unsigned)s < (unsigned)a.xmax) *reinterpret_cast<u32x4_t*>(a.A + (size_t)s * a.H + cc[i] * 8) = val[i];
       }
     }
   }
   if (signal) {
+    // this wavefront's rows are complete and written back before it counts
+    // them in the readiness counters of their row tiles
     __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid < WAVE) {
-      fence_release_agent();
-      for (int i = tid; i < nt * k; i += WAVE) {
-        int s = W.sl[i];
-        if ((unsigned)s >= (unsigned)a.xmax) continue;
-        int g = g0 + i / k;
-        int le = a.topk_idx[(size_t)g * k + (i % k)] - a.e0;
-        if ((unsigned)le >= (unsigned)a.El) continue;
-        int q = (int)(((long long)g * S->K) / a.T);
-        int id = S->mb[q * S->nseg + le] + (s - S->row0[q * S->nseg + le]) / BM;
+    fence_release_agent();
+    if (lane < nt * k) {
+      const int s = sl[lane];
+      const int g = g0 + lane / k;
+      const int le = (unsigned)s < (unsigned)a.xmax ? a.topk_idx[(size_t)g * k + (lane % k)] - a.e0 : -1;
+      if ((unsigned)le < (unsigned)a.El) {
+        const int q = (int)(((long long)g * S->K) / a.T);
+        const int id = S->mb[q * S->nseg + le] + (s - S->row0[q * S->nseg + le]) / BM;
         if ((unsigned)id < (unsigned)a.mt_max) fetch_add_relaxed(&a.ctl[CTL_READY + id], 1);
       }
     }
   }
-  __syncthreads();
+  __builtin_amdgcn_wave_barrier();
+}
+
+// One wavefront combines nt <= CT tokens.  Each token has KS = k + S source
+// rows in O: its k routed slots (weight w, absent when the expert is not
+// local) followed by its S shared-expert rows (weight 1, present for tokens of
+// rank 0).  They are summed in that order in fp32.  KS is a template constant
+// so that every lane keeps about 16 row vectors in flight.
+template <int KS>
+__device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
+  constexpr int P = KS >= 16 ? 1 : 16 / KS;  // positions per lane per pass
+  const int lane = lane_id();
+  const int VPR = a.H >> 3;
+  const int total = nt * VPR;
+  for (int v0 = lane; v0 < total; v0 += P * WAVE) {
+    u32x4_t o[P][KS];
+    int tt[P], cc[P];
+#pragma unroll
+    for (int i = 0; i < P; ++i) {
+      const int v = v0 + i * WAVE;
+      tt[i] = v < total ? v / VPR : -1;
+      cc[i] = v < total ? v - tt[i] * VPR : 0;
+#pragma unroll
+      for (int j = 0; j < KS; ++j) {
+        const int s = tt[i] >= 0 ? sl[tt[i] * KS + j] : -1;
+        if (s >= 0) o[i][j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < P; ++i) {
+      if (tt[i] < 0) continue;
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+#pragma unroll
+      for (int j = 0; j < KS; ++j) {
+        if (sl[tt[i] * KS + j] < 0) continue;
+        const float w = wt[tt[i] * KS + j];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[2 * q] += w * bf16_lo(o[i][j][q]);
+          acc[2 * q + 1] += w * bf16_hi(o[i][j][q]);
+        }
+      }
+      u32x4_t r;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
+      __builtin_nontemporal_store(r, reinterpret_cast<u32x4_t*>(a.y + (size_t)(g0 + tt[i]) * a.H + cc[i] * 8));
+    }
+  }
 }
 
 __device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
-  const int tid = threadIdx.x;
-  const int k = a.k;
-  for (int i = tid; i < nt * k; i += FNTH) {
-    W.sl[i] = a.slot[(size_t)g0 * k + i];
-    W.wt[i] = a.topk_w[(size_t)g0 * k + i];
+  const int lane = lane_id();
+  int* sl = W.wsl[wave_id()];
+  float* wt = W.wwt[wave_id()];
+  const int k = a.k, ks = a.k + a.S;
+  // source rows of token g0 + lane / ks, entry lane % ks
+  if (lane < nt * ks) {
+    const int t = lane / ks, j = lane - t * ks, g = g0 + t;
+    int s = -1;
+    float w = 1.0f;
+    if (j < k) {
+      s = a.slot[(size_t)g * k + j];
+      w = a.topk_w[(size_t)g * k + j];
+      if ((unsigned)s >= (unsigned)a.xmax) s = -1;
+    } else if (g < a.Tr) {
+      s = a.xmax + (j - k) * a.Tr + g;
+    }
+    sl[lane] = s;
+    wt[lane] = w;
   }
-  __syncthreads();
-  const int VPR = a.H >> 3;
-  const int total = nt * VPR;
-  for (int v = tid; v < total; v += FNTH) {
-    int t = v / VPR, c = v - t * VPR;
-    int g = g0 + t;
-    u32x4_t o[MAX_TOPK];
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j) {
-      const int s = j < k ? W.sl[t * k + j] : -1;
-      if ((unsigned)s < (unsigned)a.xmax) o[j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + c * 8);
-    }
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j) {
-      const int s = j < k ? W.sl[t * k + j] : -1;
-      if ((unsigned)s >= (unsigned)a.xmax) continue;
-      const float w = W.wt[t * k + j];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += w * bf16_lo(o[j][q]);
-        acc[2 * q + 1] += w * bf16_hi(o[j][q]);
-      }
-    }
-    if (g < a.Tr) {
-      for (int s = 0; s < a.S; ++s) {
-        u32x4_t os = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)(a.xmax + s * a.Tr + g) * a.H + c * 8);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += bf16_lo(os[q]);
-          acc[2 * q + 1] += bf16_hi(os[q]);
-        }
-      }
-    }
-    u32x4_t r;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) r[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
-    *reinterpret_cast<u32x4_t*>(a.y + (size_t)g * a.H + c * 8) = r;
+  __builtin_amdgcn_wave_barrier();
+  switch (ks) {
+#define MOE_COMBINE_CASE(n) case n: combine_body<n>(a, sl, wt, g0, nt); break;
+    MOE_COMBINE_CASE(1) MOE_COMBINE_CASE(2) MOE_COMBINE_CASE(3) MOE_COMBINE_CASE(4)
+    MOE_COMBINE_CASE(5) MOE_COMBINE_CASE(6) MOE_COMBINE_CASE(7) MOE_COMBINE_CASE(8)
+    MOE_COMBINE_CASE(9) MOE_COMBINE_CASE(10) MOE_COMBINE_CASE(11) MOE_COMBINE_CASE(12)
+    MOE_COMBINE_CASE(13) MOE_COMBINE_CASE(14) MOE_COMBINE_CASE(15) MOE_COMBINE_CASE(16)
+#undef MOE_COMBINE_CASE
+    default: break;
   }
-  __syncthreads();
+  __builtin_amdgcn_wave_barrier();
 }
 
 // ===========================================================================
@@ -448,16 +491,37 @@ __device__ __forceinline__ bool run_compute_tile(const FwdArgs& a, const Sched& 
   return true;
 }
 
+// wavefront-level wait: lane 0 polls like wait_geq, the others follow
+__device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target) {
+  if (a.inject_stall) target += 1 << 30;
+  int ok = 1;
+  if (lane_id() == 0 && ld_relaxed(p) < target) {
+    const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
+    while (ld_relaxed(p) < target) {
+      if (ld_relaxed(&a.ctl[CTL_ABORT])) { ok = 0; break; }
+      if (now_ticks() > deadline) {
+        st_relaxed(&a.ctl[CTL_ABORT], 1);
+        atomicOr(a.err, ERR_TIMEOUT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  return __builtin_amdgcn_readfirstlane(ok) != 0;
+}
+
+// combine units in chunk order, claimed per wavefront; chunk q's units wait
+// until every GEMM1 tile of chunk q is done
 __device__ __forceinline__ bool combine_loop(const FwdArgs& a, const Sched& S, Scratch& W) {
   for (;;) {
-    int u = claim(W, &a.ctl[CTL_Q_COMB]);
+    const int u = wave_claim(&a.ctl[CTL_Q_COMB]);
     if (u >= S.n_comb) return true;
     int q = 0;
     while (q + 1 < S.K && S.cstart[q + 1] <= u) ++q;
-    if (!wait_geq(a, W, &a.ctl[CTL_G1DONE + q], S.g1need[q])) return false;
-    int g0 = S.bnd[q] + (u - S.cstart[q]) * CT;
-    int nt = min(CT, S.bnd[q + 1] - g0);
-    combine_tokens(a, W, g0, nt);
+    if (!wave_wait_geq(a, &a.ctl[CTL_G1DONE + q], S.g1need[q])) return false;
+    const int g0 = S.bnd[q] + (u - S.cstart[q]) * CT;
+    combine_tokens(a, W, g0, min(CT, S.bnd[q + 1] - g0));
   }
 }
 
@@ -482,28 +546,30 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   const bool mover = W.bc[0] < S.c;
   __syncthreads();
 
+  bool ok = true;
   if (mover) {
-    // dispatch: every token row, in token (hence chunk) order
+    // dispatch: every token row, in token (hence chunk) order, per wavefront
     for (;;) {
-      int u = claim(W, &a.ctl[CTL_Q_DISP]);
+      const int u = wave_claim(&a.ctl[CTL_Q_DISP]);
       if (u >= S.n_disp) break;
       dispatch_unit(a, &S, W, u, true);
     }
+    __syncthreads();
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
-    for (int i = 0; i < S.n_steal; ++i) {
-      int t = claim(W, &a.ctl[CTL_Q_COMP]);
+    for (int i = 0; i < S.n_steal && ok; ++i) {
+      const int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, ring)) return;
+      ok = run_compute_tile(a, S, W, t, ring);
     }
-    combine_loop(a, S, W);
+    if (ok) combine_loop(a, S, W);
   } else {
     for (;;) {
-      int t = claim(W, &a.ctl[CTL_Q_COMP]);
+      const int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, ring)) return;
+      if (!run_compute_tile(a, S, W, t, ring)) { ok = false; break; }
     }
     // final combine on every worker (section 4)
-    if (S.final_all) combine_loop(a, S, W);
+    if (ok && S.final_all) combine_loop(a, S, W);
   }
 }
 
@@ -517,7 +583,7 @@ __global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
   const int n = ceil_div(a.T, DT);
   for (;;) {
-    int u = claim(W, &a.ctl[CTL_SQ + 0]);
+    const int u = wave_claim(&a.ctl[CTL_SQ + 0]);
     if (u >= n) break;
     dispatch_unit(a, nullptr, W, u, false);
   }
@@ -528,13 +594,21 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
-  build_sched(a, S, W, 1);
-  const int first = S.gstart[PH * S.nseg];
-  const int count = S.gstart[(PH + 1) * S.nseg] - first;
+  build_sched(a, S, W, a.serial_K);
+  // the tiles of phase PH in every chunk, in queue order
+  int count = 0;
+  for (int q = 0; q < S.K; ++q)
+    count += S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
   for (;;) {
     int t = claim(W, &a.ctl[CTL_SQ + 64 * qslot]);
     if (t >= count) break;
-    TileRef r = decode_tile(a, S, first + t);
+    int q = 0;
+    for (;; ++q) {
+      const int n = S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
+      if (t < n) break;
+      t -= n;
+    }
+    TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + t);
     run_gemm(a, S, W, r, S.mb[r.q * S.nseg + r.seg] + r.mt, ring);
   }
 }
@@ -546,9 +620,9 @@ __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   __shared__ Scratch W;
   const int n = ceil_div(a.T, CT);
   for (;;) {
-    int u = claim(W, &a.ctl[CTL_SQ + 192]);
+    const int u = wave_claim(&a.ctl[CTL_SQ + 192]);
     if (u >= n) break;
-    int g0 = u * CT;
+    const int g0 = u * CT;
     combine_tokens(a, W, g0, min(CT, a.T - g0));
   }
 }

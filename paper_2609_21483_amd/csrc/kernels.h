@@ -13,7 +13,7 @@ struct GateArgs {
   int32_t* topk_idx;
   float* topk_w;
   int T, H, E, k;
-  int tq;  // token quads per workgroup
+  int tq;  // token groups per workgroup
 };
 
 struct TableArgs {
@@ -89,6 +89,7 @@ struct FwdArgs {
   moe_plan fplan;
   long long timeout_ticks;  // per wait, 100 MHz ticks
   int inject_stall;         // test hook: every wait targets an unreachable value
+  int serial_K;             // chunk tiling used by the separate-kernel GEMMs
 };
 
 // ---- cost model (sections 3.1-3.3) ------------------------------------------
@@ -158,6 +159,7 @@ __host__ __device__ inline void cm_volumes(const int32_t* stats, int H, int F, i
 }
 
 // ---- launch prototypes ---------------------------------------------------------
+template <int TPT, int EPT>
 __global__ void gate_topk_kernel(GateArgs a);
 __global__ void tab_count_kernel(TableArgs a);
 __global__ void tab_scan_kernel(TableArgs a);

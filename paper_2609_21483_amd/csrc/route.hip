@@ -13,65 +13,77 @@ namespace moe {
 
 // ---------------------------------------------------------------------------
 // Gate: logits -> softmax -> top-k (on logits, ties -> smaller id) -> renormalise
-// Each thread owns a 4-token x 4-expert block of logits; x and Wg are staged
-// through LDS as fp32 in chunks of GH hidden values.
+// Each thread owns a TPT-token x EPT-expert block of logits (one fp32
+// accumulator per (token, expert), ascending h).  x and Wg are staged
+// through LDS as fp32 in chunks of GH hidden values, token-major and
+// expert-major rows padded to GHP floats so float4 reads are conflict-free.
+// The host picks the block size so that the grid has enough workgroups.
 // ---------------------------------------------------------------------------
 constexpr int GH = 16;
+constexpr int GHP = GH + 4;
 constexpr int GATE_MAX_TT = 256;
 
+template <int TPT, int EPT>
 __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
-  __shared__ float xs[GH][GATE_MAX_TT];
-  __shared__ float ws[GH][MAX_E];
-  __shared__ float lg[4096];
+  __shared__ __attribute__((aligned(16))) float xs[GATE_MAX_TT * GHP];
+  __shared__ __attribute__((aligned(16))) float ws[MAX_E * GHP];
+  __shared__ float lg[NTH * 16];
 
   const int tid = threadIdx.x;
-  const int EQ = (a.E + 3) >> 2;
-  const int EP = EQ * 4;
-  const int TQ = a.tq;           // token quads per workgroup
-  const int TT = TQ * 4;
+  const int EQ = (a.E + EPT - 1) / EPT;
+  const int EP = EQ * EPT;
+  const int TQ = a.tq;  // token groups per workgroup
+  const int TT = TQ * TPT;
   const int g0 = blockIdx.x * TT;
   const bool active = tid < TQ * EQ;
   const int tq = active ? tid / EQ : 0;
   const int eq = active ? tid % EQ : 0;
 
-  float acc[4][4];
+  float acc[TPT][EPT];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TPT; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+    for (int j = 0; j < EPT; ++j) acc[i][j] = 0.0f;
 
   for (int h0 = 0; h0 < a.H; h0 += GH) {
-    // stage x[g0 .. g0+TT)[h0 .. h0+GH) transposed: xs[h][t]
+    // stage x[g0 .. g0+TT)[h0 .. h0+GH) as xs[t][h]
     for (int v = tid; v < TT * (GH / 8); v += NTH) {
-      int t = v / (GH / 8), part = v % (GH / 8);
-      int g = g0 + t;
+      const int t = v / (GH / 8), part = v % (GH / 8);
+      const int g = g0 + t;
       u32x4_t w = {0u, 0u, 0u, 0u};
       if (g < a.T) w = *reinterpret_cast<const u32x4_t*>(a.x + (size_t)g * a.H + h0 + part * 8);
+      float* d = xs + t * GHP + part * 8;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        xs[part * 8 + 2 * q][t] = bf16_lo(w[q]);
-        xs[part * 8 + 2 * q + 1][t] = bf16_hi(w[q]);
+        d[2 * q] = bf16_lo(w[q]);
+        d[2 * q + 1] = bf16_hi(w[q]);
       }
     }
-    // stage Wg[h0 .. h0+GH)[0 .. E): ws[h][e]
+    // stage Wg[h0 .. h0+GH)[0 .. E) as ws[e][h]
     for (int v = tid; v < GH * EP; v += NTH) {
-      int h = v / EP, e = v % EP;
-      ws[h][e] = e < a.E ? bf16_to_f32(a.wg[(size_t)(h0 + h) * a.E + e]) : 0.0f;
+      const int h = v / EP, e = v % EP;
+      ws[e * GHP + h] = e < a.E ? bf16_to_f32(a.wg[(size_t)(h0 + h) * a.E + e]) : 0.0f;
     }
     __syncthreads();
     if (active) {
 #pragma unroll
-      for (int h = 0; h < GH; ++h) {
-        float4 xv = *reinterpret_cast<const float4*>(&xs[h][4 * tq]);
-        float4 wv = *reinterpret_cast<const float4*>(&ws[h][4 * eq]);
-        float xa[4] = {xv.x, xv.y, xv.z, xv.w};
-        float wa[4] = {wv.x, wv.y, wv.z, wv.w};
+      for (int h = 0; h < GH; h += 4) {
+        float4 xv[TPT], wv[EPT];
+#pragma unroll
+        for (int i = 0; i < TPT; ++i) xv[i] = *reinterpret_cast<const float4*>(xs + (tq * TPT + i) * GHP + h);
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) wv[j] = *reinterpret_cast<const float4*>(ws + (eq * EPT + j) * GHP + h);
         // products of two bf16 values are exact in fp32, so a fused or an
-        // unfused multiply-add gives the same rounded sum
+        // unfused multiply-add gives the same rounded sum; h ascends
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TPT; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] + xa[i] * wa[j];
+          for (int j = 0; j < EPT; ++j) {
+            acc[i][j] = acc[i][j] + xv[i].x * wv[j].x;
+            acc[i][j] = acc[i][j] + xv[i].y * wv[j].y;
+            acc[i][j] = acc[i][j] + xv[i].z * wv[j].z;
+            acc[i][j] = acc[i][j] + xv[i].w * wv[j].w;
+          }
       }
     }
     __syncthreads();
@@ -79,14 +91,14 @@ __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
 
   if (active) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TPT; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int e = 4 * eq + j;
+      for (int j = 0; j < EPT; ++j) {
+        const int e = eq * EPT + j;
         if (e < a.E) {
           float l = acc[i][j];
           if (a.bias) l = l + a.bias[e];
-          lg[(4 * tq + i) * EP + e] = l;
+          lg[(tq * TPT + i) * EP + e] = l;
         }
       }
   }
@@ -94,7 +106,7 @@ __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
 
   // one thread per token: softmax statistics, top-k insertion, renormalise
   for (int t = tid; t < TT; t += NTH) {
-    int g = g0 + t;
+    const int g = g0 + t;
     if (g >= a.T) break;
     const float* l = lg + t * EP;
     float m = l[0];
@@ -107,7 +119,7 @@ __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
 #pragma unroll
     for (int j = 0; j < MAX_TOPK; ++j) { tv[j] = -INFINITY; ti[j] = -1; }
     for (int e = 0; e < a.E; ++e) {
-      float v = l[e];
+      const float v = l[e];
       // insert e if it beats the current k-th entry; equal logits keep the
       // earlier (smaller) expert id in front
       if (ti[a.k - 1] >= 0 && !(v > tv[a.k - 1])) continue;
@@ -117,10 +129,10 @@ __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
 #pragma unroll
       for (int j = 0; j < MAX_TOPK; ++j) {
         if (j < a.k) {
-          bool go = placed || ti[j] < 0 || carry_v > tv[j];
+          const bool go = placed || ti[j] < 0 || carry_v > tv[j];
           if (go) {
-            float sv = tv[j];
-            int si = ti[j];
+            const float sv = tv[j];
+            const int si = ti[j];
             tv[j] = carry_v;
             ti[j] = carry_i;
             carry_v = sv;
@@ -144,6 +156,10 @@ __global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
       }
   }
 }
+
+template __global__ void gate_topk_kernel<4, 4>(GateArgs);
+template __global__ void gate_topk_kernel<2, 2>(GateArgs);
+template __global__ void gate_topk_kernel<1, 1>(GateArgs);
 
 // ---------------------------------------------------------------------------
 // Routing tables.  A pair (g, j) is local when id = topk_idx[g,j] is in
