@@ -74,6 +74,7 @@ typedef struct {
   int32_t first_local_expert; /* e0, 0 <= e0 <= E - E_l */
   int32_t n_shared_experts;   /* S, 0..8, always-on experts applied to rank-0 tokens */
   int32_t n_workers;          /* persistent workgroups N; 0 = one per CU */
+  int32_t gemm1_split;        /* split-K factor of GEMM1 (K = F): 1, 2 or 4; 0 = chosen from F/H */
 } moe_config;
 
 #define MOE_CALIB_MAX_C 32
@@ -153,6 +154,24 @@ moe_status moe_get_calib(const moe_handle* h, moe_calib* out);
  * so the next megakernel launch exercises this path and exits after ~ms.
  * Default: 2000 ms, no injection. */
 moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
+
+/* Timeline trace of the megakernel (a measurement aid for the schedule of
+ * sections 3-4: worker roles, tile waits, movement phases).  buf is caller-
+ * owned device memory of `bytes` bytes, or NULL to turn tracing off.  Each
+ * later moe_forward in a non-serial mode first clears the record counter, then
+ * every workgroup appends 32-byte records:
+ *   int64 word 0: kind | ticket << 8 | xcd << 20 | id << 32
+ *   int64 words 1-3: times t0, t1, t2 from the 100 MHz device clock
+ * kind 1 workgroup (id 1 = movement worker): entry, plan + schedule built, exit
+ * kind 2 compute tile (id = queue index): claimed, inputs ready, finished
+ * kind 3 dispatch by one movement worker: start, end
+ * kind 4 combine of one chunk by one wavefront (id = chunk | wave << 8):
+ *        start, inputs ready, end
+ * Word 0 of buf holds the number of records written (at most
+ * (bytes - 64) / 32 are stored); records start at byte 64.  The layout of a
+ * trace follows the handle's current plan; it changes nothing else.
+ * Errors: MOE_ERR_INVALID_ARG for a non-NULL buf with bytes < 96. */
+moe_status moe_set_trace(moe_handle* h, void* buf, int64_t bytes);
 
 /* Workspace size in bytes and its region offsets (host out-parameters). */
 moe_status moe_workspace_size(const moe_handle* h, size_t* bytes);

@@ -39,7 +39,8 @@ CALIB_MAX_K = 4
 class moe_config(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "n_src_ranks", "tokens_per_rank", "hidden", "ffn", "n_experts", "top_k",
-        "n_local_experts", "first_local_expert", "n_shared_experts", "n_workers")]
+        "n_local_experts", "first_local_expert", "n_shared_experts", "n_workers",
+                                    "gemm1_split")]
 
 
 class moe_calib(C.Structure):
@@ -85,6 +86,7 @@ _SIGS = {
     "moe_set_calib": ([_H, C.POINTER(moe_calib)], C.c_int),
     "moe_get_calib": ([_H, C.POINTER(moe_calib)], C.c_int),
     "moe_set_timeout_ms": ([_H, C.c_double, C.c_int32], C.c_int),
+    "moe_set_trace": ([_H, C.c_void_p, C.c_int64], C.c_int),
     "moe_workspace_size": ([_H, C.POINTER(C.c_size_t)], C.c_int),
     "moe_workspace_layout": ([_H, C.POINTER(moe_ws_layout)], C.c_int),
     "moe_set_workspace": ([_H, _P, C.c_size_t, _P], C.c_int),
@@ -158,6 +160,34 @@ def moe_get_calib(h: int) -> moe_calib:
     k = moe_calib()
     _check("moe_get_calib", _lib.moe_get_calib(h, C.byref(k)))
     return k
+
+
+def moe_set_trace(h: int, buf, nbytes: int = 0) -> None:
+    """Point the megakernel's timeline trace at a device buffer (None: off)."""
+    ptr = None if buf is None else _ptr(buf)
+    n = 0 if buf is None else int(nbytes or buf.numel() * buf.element_size())
+    _check("moe_set_trace", _lib.moe_set_trace(h, ptr, n))
+
+
+TRACE_KINDS = {1: "workgroup", 2: "tile", 3: "dispatch", 4: "combine"}
+
+
+def read_trace(buf) -> "np.ndarray":
+    """Decode a trace buffer into a structured array (kind, ticket, xcd, id,
+    t0, t1, t2), times in device-clock ticks of 10 ns."""
+    import numpy as np
+    raw = buf.cpu().numpy().view(np.int64)
+    n = min(int(raw[0]) & 0xFFFFFFFF, (raw.size * 8 - 64) // 32)
+    rec = raw[8:8 + 4 * n].reshape(n, 4)
+    w0 = rec[:, 0]
+    out = np.zeros(n, dtype=[("kind", "i4"), ("ticket", "i4"), ("xcd", "i4"), ("id", "i8"),
+                             ("t0", "i8"), ("t1", "i8"), ("t2", "i8")])
+    out["kind"] = w0 & 0xFF
+    out["ticket"] = (w0 >> 8) & 0xFFF
+    out["xcd"] = (w0 >> 20) & 0xFFF
+    out["id"] = w0 >> 32
+    out["t0"], out["t1"], out["t2"] = rec[:, 1], rec[:, 2], rec[:, 3]
+    return out
 
 
 def moe_set_timeout_ms(h: int, ms: float, inject_stall: int = 0) -> None:
@@ -240,9 +270,10 @@ def moe_tile_geometry(h: int):
 
 # ---- convenience --------------------------------------------------------------
 
-def make_config(shape, n_workers: int = 0, first_local_expert: int = 0) -> moe_config:
+def make_config(shape, n_workers: int = 0, first_local_expert: int = 0, gemm1_split: int = 0) -> moe_config:
     return moe_config(shape.n_src_ranks, shape.tokens_per_rank, shape.hidden, shape.ffn, shape.n_experts,
-                      shape.top_k, shape.n_local_experts, first_local_expert, shape.n_shared_experts, n_workers)
+                      shape.top_k, shape.n_local_experts, first_local_expert, shape.n_shared_experts, n_workers,
+                      gemm1_split)
 
 
 def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int = 0) -> moe_calib:
@@ -263,10 +294,10 @@ class MoeLayer:
     """Owns a handle plus torch-allocated workspace and packed weights on one device."""
 
     def __init__(self, shape, w1, w3, w2, ws1=None, ws3=None, ws2=None, calib: Optional[moe_calib] = None,
-                 device="cuda", n_workers: int = 0, stream=None):
+                 device="cuda", n_workers: int = 0, stream=None, gemm1_split: int = 0):
         self.shape = shape
         self.device = torch.device(device)
-        self.h = moe_init(make_config(shape, n_workers), calib)
+        self.h = moe_init(make_config(shape, n_workers, gemm1_split=gemm1_split), calib)
         self.ws = torch.empty(moe_workspace_size(self.h), dtype=torch.uint8, device=self.device)
         moe_set_workspace(self.h, self.ws, stream)
         self.packed = torch.empty(moe_packed_weights_size(self.h), dtype=torch.uint8, device=self.device)

@@ -50,6 +50,8 @@ struct moe_handle {
   unsigned long long launch_seq = 0;
   long long timeout_ticks = 200000000LL;  // 2 s at 100 MHz
   int inject_stall = 0;
+  long long* trace = nullptr;
+  int trace_cap = 0;
 };
 
 namespace {
@@ -74,9 +76,16 @@ moe_status validate_cfg(const moe_config* c) {
   if (c->n_shared_experts < 0 || c->n_shared_experts > MAX_S)
     return fail(MOE_ERR_INVALID_ARG, "n_shared_experts must be in [0, %d]", MAX_S);
   if (c->n_workers < 0) return fail(MOE_ERR_INVALID_ARG, "n_workers must be >= 0");
+  if (c->gemm1_split != 0 && c->gemm1_split != 1 && c->gemm1_split != 2 && c->gemm1_split != 4)
+    return fail(MOE_ERR_INVALID_ARG, "gemm1_split must be 0, 1, 2 or 4");
+  if (c->gemm1_split > 1 && c->ffn % (32 * c->gemm1_split))
+    return fail(MOE_ERR_INVALID_ARG, "ffn must be a multiple of 32 * gemm1_split");
   long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
   if (xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM > (1LL << 31) / 2)
     return fail(MOE_ERR_UNSUPPORTED, "too many routed rows");
+  // dispatch addresses the row buffer A with 32-bit byte offsets
+  if ((xmax + BM) * (long long)c->hidden * 2 >= (1LL << 32))
+    return fail(MOE_ERR_UNSUPPORTED, "dispatched rows (T * min(k, E_l) x H bf16) exceed 4 GiB");
   return MOE_OK;
 }
 
@@ -164,7 +173,8 @@ void compute_layout(moe_handle* h) {
   L.A = take(sizeof(uint16_t) * ((size_t)h->xmax + BM) * c.hidden);
   L.Hbuf = take(sizeof(uint16_t) * orows * c.ffn);
   L.O = take(sizeof(uint16_t) * orows * c.hidden);
-  h->off_part = h->nsplit > 1 ? take(sizeof(float) * (size_t)h->mt_max * h->nt1 * h->nsplit * BM * BN) : 0;
+  // split-K partials of GEMM1: fp32 [split][row][H], rows as in O
+  h->off_part = h->nsplit > 1 ? take(sizeof(float) * (size_t)h->nsplit * orows * c.hidden) : 0;
   L.total = o;
 }
 
@@ -240,6 +250,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.Hb = at<uint16_t>(h, h->lay.Hbuf);
   a.O = at<uint16_t>(h, h->lay.O);
   a.part = h->nsplit > 1 ? at<float>(h, h->off_part) : nullptr;
+  a.prow = (size_t)h->xmax + (size_t)h->cfg.n_shared_experts * h->cfg.tokens_per_rank + BM;
   a.ctl = at<int32_t>(h, h->off_ctl[cur]);
   a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
   a.err = at<int32_t>(h, h->lay.err);
@@ -250,6 +261,8 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   if (forced) a.fplan = *forced;
   a.timeout_ticks = h->timeout_ticks;
   a.inject_stall = h->inject_stall;
+  a.trace = h->trace;
+  a.trace_cap = h->trace_cap;
   a.serial_K = 1;
   return a;
 }
@@ -284,9 +297,13 @@ moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** 
   h->nt1 = (cfg->hidden + BN - 1) / BN;
   // split GEMM1 (K = F) when F is large against H, so its tiles are about as
   // long as GEMM0's (K = H) and there are enough of them to fill the CUs
-  h->nsplit = cfg->ffn >= 3 * cfg->hidden ? 4 : (2 * cfg->ffn >= 3 * cfg->hidden ? 2 : 1);
-  while (h->nsplit > 1 && cfg->ffn % (32 * h->nsplit)) h->nsplit /= 2;
-  h->ctl_words = CTL_READY + 2 * h->mt_max + h->mt_max * h->nt1;
+  if (cfg->gemm1_split) {
+    h->nsplit = cfg->gemm1_split;
+  } else {
+    h->nsplit = cfg->ffn >= 3 * cfg->hidden ? 4 : (2 * cfg->ffn >= 3 * cfg->hidden ? 2 : 1);
+    while (h->nsplit > 1 && cfg->ffn % (32 * h->nsplit)) h->nsplit /= 2;
+  }
+  h->ctl_words = CTL_READY + 2 * h->mt_max * CTL_PAD;
   if (calib) {
     st = validate_calib(calib, N);
     if (st != MOE_OK) { delete h; return st; }
@@ -455,6 +472,14 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   return moe_build_tables(h, topk_idx, stream);
 }
 
+moe_status moe_set_trace(moe_handle* h, void* buf, int64_t bytes) {
+  if (!h) return fail(MOE_ERR_INVALID_ARG, "handle is NULL");
+  if (buf && bytes < 96) return fail(MOE_ERR_INVALID_ARG, "trace buffer needs at least 96 bytes");
+  h->trace = static_cast<long long*>(buf);
+  h->trace_cap = buf ? (int)std::min<int64_t>((bytes - 64) / 32, 1 << 30) : 0;
+  return MOE_OK;
+}
+
 moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, const float* topk_w,
                        const void* packed, uint16_t* y, int32_t mode, const moe_plan* forced, void* stream) {
   moe_status st = need_ws(h);
@@ -480,6 +505,7 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     serial_combine_kernel<<<h->N, FNTH, 0, s>>>(a);
     HIP_TRY(hipGetLastError());
   } else {
+    if (h->trace) zero_i32_kernel<<<1, 64, 0, s>>>(reinterpret_cast<int32_t*>(h->trace), 2);
     void* args[] = {&a};
     HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(FNTH), args, 0, s));
   }

@@ -19,7 +19,7 @@ constexpr int BM = 256;
 constexpr int BN = 256;
 constexpr int MAX_SPLIT = 4;    // split-K factor limit of GEMM1
 
-constexpr int DT = 4;           // tokens per dispatch unit (one wavefront)
+constexpr int DT = 8;           // tokens per dispatch unit (one wavefront; DT * top_k <= 64)
 constexpr int CT = 4;           // tokens per combine unit (one wavefront)
 
 constexpr int MAX_EL = 64;      // local experts
@@ -37,16 +37,20 @@ __host__ __device__ inline int kopt_value(int i) { return 1 << i; }
 // ---- control block: queue heads, readiness counters (int32 words) ------------
 // Two sets are kept; launch n uses set n%2 and clears set (n+1)%2 for the next
 // launch, so the layer is a single kernel launch with no host-side reset.
+// Every counter has a 64-byte line of its own (CTL_PAD words), so pollers of
+// one counter do not share a line with updates of another.
+constexpr int CTL_PAD = 16;
 constexpr int CTL_Q_COMP = 0;     // compute-tile queue head
-constexpr int CTL_Q_DISP = 64;    // dispatch-unit queue head
-constexpr int CTL_Q_COMB = 128;   // combine-unit queue head
-constexpr int CTL_TICKET = 192;   // arrival ticket -> role
-constexpr int CTL_ABORT = 256;    // set once any wait times out
-constexpr int CTL_G1DONE = 320;   // [MAX_K] GEMM1 tiles finished per chunk
-constexpr int CTL_SQ = 384;       // [4] queue heads of the four serial kernels (stride 64)
-constexpr int CTL_READY = 640;    // [mt_max] dispatched rows per row tile
-// then [mt_max] GEMM0 column tiles finished per row tile,
-// then [mt_max * nt1] split-K arrivals per GEMM1 (row tile, column tile)
+constexpr int CTL_TICKET = 16;    // arrival ticket -> role
+constexpr int CTL_ABORT = 32;     // set once any wait times out
+constexpr int CTL_SQ = 48;        // queue heads of the serial GEMM kernels (CTL_PAD apart)
+constexpr int CTL_G1DONE = 128;   // [MAX_K] GEMM1 tiles finished per chunk (CTL_PAD apart)
+constexpr int NSHARD = 8;         // dispatch-unit queue shards
+constexpr int CTL_QD = 256;       // [NSHARD] dispatch-unit queue heads (CTL_PAD apart)
+constexpr int CTL_READY = 384;    // [mt_max] dispatched rows per row tile (CTL_PAD apart),
+// then [mt_max] GEMM0 column tiles finished per row tile (CTL_PAD apart)
+static_assert(CTL_G1DONE + MAX_K * CTL_PAD <= CTL_QD, "control block overlap");
+static_assert(CTL_QD + NSHARD * CTL_PAD <= CTL_READY, "control block overlap");
 
 // stats words written by the table builder
 constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;

@@ -7,10 +7,12 @@
 //   A    bf16 [X+pad][H]    dispatched rows, expert-contiguous (slot order)
 //   Hbuf bf16 [X+S*Tr+pad][F]  SiLU(gate)*up per row (shared experts after X)
 //   O    bf16 [X+S*Tr+pad][H]  expert outputs per row
-//   part fp32 [row tile][col tile][split][256*256]  split-K partials of GEMM1
+//   part fp32 [split][X+S*Tr+pad][H]  split-K partials of GEMM1 (when split)
 //   y    bf16 [T][H]        output staging regions
 //   w13  bf16 [E_l+S][2F][H] gate/up weights, k-contiguous, 32-col interleave
 //   w2t  bf16 [E_l+S][H][F]  down weights, k-contiguous
+#include <type_traits>
+
 #include "common.h"
 #include "gemm.h"
 #include "kernels.h"
@@ -32,7 +34,7 @@ struct Sched {
   int c, n_steal, final_all;
   int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
   int cstart[MAX_K + 1]; // combine units before chunk q
-  int g1need[MAX_K];     // GEMM1 (row, column) tiles of chunk q
+  int g1need[MAX_K];     // GEMM1 (row, column, split) tiles of chunk q
   // per (chunk q, segment) at index q*nseg + seg
   int rows[MAX_K * MAX_SEG];
   int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts)
@@ -46,6 +48,8 @@ struct Scratch {
   long long ntk[KOPT];
   int part[NWF];
   int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
+  int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
+  int dexh;              // every dispatch unit has been claimed (seen by this workgroup)
   float wwt[NWF][WAVE];  // per wavefront: their weights
 };
 
@@ -118,7 +122,7 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
   if (tid == 0) S.gstart[S.G] = 0;
   if (tid < K) {
     int s = 0;
-    for (int seg = 0; seg < nseg; ++seg) s += S.mb[tid * nseg + seg] * a.nt1;
+    for (int seg = 0; seg < nseg; ++seg) s += S.mb[tid * nseg + seg] * g1tiles;
     S.g1need[tid] = s;
   }
   __syncthreads();
@@ -137,119 +141,254 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
 // region.
 // ===========================================================================
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
-__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE); }
 
-__device__ __forceinline__ int wave_claim(int* q) {
-  int v = 0;
-  if (lane_id() == 0) v = fetch_add_relaxed(q, 1);
-  return __builtin_amdgcn_readfirstlane(v);
+// ---- timeline trace (off when a.trace is NULL) ------------------------------
+__device__ __forceinline__ int xcd_id() {
+  int v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(v));
+  return v;
 }
 
-__device__ __forceinline__ void dispatch_unit(const FwdArgs& a, const Sched* S, Scratch& W, int u, bool signal) {
+// one lane appends one record
+__device__ __forceinline__ void trace_rec(const FwdArgs& a, int kind, int ticket, long long id, uint64_t t0,
+                                          uint64_t t1, uint64_t t2) {
+  if (!a.trace) return;
+  const unsigned long long slot = atomicAdd(reinterpret_cast<unsigned long long*>(a.trace), 1ull);
+  if (slot >= (unsigned long long)a.trace_cap) return;
+  long long* r = a.trace + 8 + 4 * slot;
+  r[0] = (long long)kind | ((long long)ticket << 8) | ((long long)xcd_id() << 20) | (id << 32);
+  r[1] = (long long)t0;
+  r[2] = (long long)t1;
+  r[3] = (long long)t2;
+}
+
+// Movement units are assigned statically: worker w of n (a workgroup index)
+// takes units (i * n + w) * NWF + wave for i = 0, 1, ..., so the units are
+// issued in ascending (token, hence chunk) order across all workers and no
+// queue counter is contended.
+
+// Dispatch (section 4, with dedup): a wavefront copies the rows of tokens
+// [u*DT, u*DT + DT) of unit u; each token row is read once and written to
+// every local slot it has.  Only tokens with a local slot are read.
+// In the megakernel (SIG) the rows are written with agent-coherent (sc1)
+// 16-byte buffer stores, so once they have completed (vmcnt 0) they are
+// visible to every XCD and the readiness counters can be raised without an
+// L2 write-back; the serial kernel, which ends at a kernel boundary, uses
+// plain stores.  Either way the wavefront drains its stores before its next
+// unit, which measures faster on this GPU than letting them queue.
+
+// this lane's slot entry of unit u (lane = token * k + j), or -1
+__device__ __forceinline__ int unit_slot(const FwdArgs& a, int u) {
+  const int g = u * DT;
+  const int lane = lane_id();
+  return (g < a.T && lane < min(DT, a.T - g) * a.k) ? a.slot[(size_t)g * a.k + lane] : -1;
+}
+
+template <bool SIG>
+__device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, Scratch& W, int u, int cur) {
+  constexpr int VB = 32;  // 16-byte vectors per lane in flight
   const int lane = lane_id();
   int* sl = W.wsl[wave_id()];
+  int* act = W.wact[wave_id()];
+  const int k = a.k;
+  const int VPR = a.H >> 3;
   const int g0 = u * DT;
   const int nt = min(DT, a.T - g0);
-  const int k = a.k;
-  sl[lane] = lane < nt * k ? a.slot[(size_t)g0 * k + lane] : -1;
+  sl[lane] = cur;
+  // tokens with at least one local slot, compacted in token order
+  const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)a.xmax);
+  const bool tact = lane < nt && ((vm >> min(lane * k, 56)) & ((1ull << k) - 1)) != 0;
+  const uint64_t am = __builtin_amdgcn_ballot_w64(tact);
+  const int na = __builtin_popcountll(am);
+  if (tact) act[__builtin_amdgcn_mbcnt_hi((uint32_t)(am >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)am, 0))] = lane;
   __builtin_amdgcn_wave_barrier();
-  const int VPR = a.H >> 3;
-  const int total = nt * VPR;
-  constexpr int VB = 16;  // 16-byte vectors per lane in flight
+  // A spans less than 4 GiB (checked on the host), so 32-bit byte offsets
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(a.A, 0, -1, 0x00020000);
+  const int total = na * VPR;
   for (int v0 = lane; v0 < total; v0 += VB * WAVE) {
     u32x4_t val[VB];
-    int tt[VB], cc[VB];
 #pragma unroll
     for (int i = 0; i < VB; ++i) {
       const int v = v0 + i * WAVE;
-      tt[i] = -1;
       if (v < total) {
-        const int t = v / VPR;
+        int t = 0;
+#pragma unroll
+        for (int m = 1; m < DT; ++m) t += v >= m * VPR;
         const int c = v - t * VPR;
-        bool any = false;
-        for (int j = 0; j < k; ++j) any |= (unsigned)sl[t * k + j] < (unsigned)a.xmax;
-        if (any) {
-          tt[i] = t;
-          cc[i] = c;
-          val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + t) * a.H + c * 8));
-        }
+        val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + act[t]) * a.H) + c);
       }
     }
 #pragma unroll
     for (int i = 0; i < VB; ++i) {
-      if (tt[i] < 0) continue;
+      const int v = v0 + i * WAVE;
+      if (v >= total) continue;
+      int t = 0;
+#pragma unroll
+      for (int m = 1; m < DT; ++m) t += v >= m * VPR;
+      const int c = v - t * VPR;
+      const int tok = act[t];
       for (int j = 0; j < k; ++j) {
-        const int s = sl[tt[i] * k + j];
-        if ((unsigned)s < (unsigned)a.xmax) *reinterpret_cast<u32x4_t*>(a.A + (size_t)s * a.H + cc[i] * 8) = val[i];
+        const int s = sl[tok * k + j];
+        if ((unsigned)s >= (unsigned)a.xmax) continue;
+        if constexpr (SIG) {
+          const uint32_t off = ((uint32_t)s * (uint32_t)a.H + (uint32_t)c * 8u) * 2u;
+          __builtin_amdgcn_raw_buffer_store_b128(val[i], rA, off, 0, 16 /* sc1 */);
+        } else {
+          reinterpret_cast<u32x4_t*>(a.A + (size_t)s * a.H)[c] = val[i];
+        }
       }
     }
   }
-  if (signal) {
-    // this wavefront's rows are complete and written back before it counts
-    // them in the readiness counters of their row tiles
-    __builtin_amdgcn_s_waitcnt(0);
-    fence_release_agent();
-    if (lane < nt * k) {
-      const int s = sl[lane];
+  __builtin_amdgcn_s_waitcnt(0);
+  if constexpr (SIG) {
+    // this wavefront's rows have reached the coherence point: count them in
+    // the readiness counters of their row tiles
+    int id = -1;
+    if ((unsigned)cur < (unsigned)a.xmax) {
       const int g = g0 + lane / k;
-      const int le = (unsigned)s < (unsigned)a.xmax ? a.topk_idx[(size_t)g * k + (lane % k)] - a.e0 : -1;
+      const int le = a.topk_idx[(size_t)g * k + (lane % k)] - a.e0;
       if ((unsigned)le < (unsigned)a.El) {
         const int q = (int)(((long long)g * S->K) / a.T);
-        const int id = S->mb[q * S->nseg + le] + (s - S->row0[q * S->nseg + le]) / BM;
-        if ((unsigned)id < (unsigned)a.mt_max) fetch_add_relaxed(&a.ctl[CTL_READY + id], 1);
+        id = S->mb[q * S->nseg + le] + (cur - S->row0[q * S->nseg + le]) / BM;
+        if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
       }
+    }
+    // one counter update per distinct row tile of this unit
+    uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
+    while (pending) {
+      const int leader = __builtin_ctzll(pending);
+      const int tile = __builtin_amdgcn_readlane(id, leader);
+      const uint64_t same = __builtin_amdgcn_ballot_w64(id == tile);
+      if (lane == leader) fetch_add_relaxed(&a.ctl[CTL_READY + tile * CTL_PAD], (int)__builtin_popcountll(same));
+      pending &= ~same;
     }
   }
   __builtin_amdgcn_wave_barrier();
 }
 
+// serial kernel: units u0, u0 + ustride, ..., the next unit's slot entries
+// fetched while the current one is copied
+__device__ __forceinline__ void dispatch_static(const FwdArgs& a, Scratch& W, int u, int ustride) {
+  const int nu = ceil_div(a.T, DT);
+  int next = unit_slot(a, u);
+  for (; u < nu; u += ustride) {
+    const int cur = next;
+    next = unit_slot(a, u + ustride);
+    dispatch_one<false>(a, nullptr, W, u, cur);
+  }
+}
+
+// Megakernel: units are claimed per wavefront from NSHARD queues (unit u is
+// the (u / NSHARD)-th of shard u % NSHARD, so every shard advances in token
+// order).  Trying the shards from `shard` on, returns the next unit or -1
+// once all are exhausted.
+__device__ __forceinline__ int claim_unit(const FwdArgs& a, const Sched& S, int& shard) {
+  for (int tries = 0; tries < NSHARD; ++tries) {
+    int v = 0;
+    if (lane_id() == 0) v = fetch_add_relaxed(&a.ctl[CTL_QD + shard * CTL_PAD], 1);
+    const int u = __builtin_amdgcn_readfirstlane(v) * NSHARD + shard;
+    if (u < S.n_disp) return u;
+    shard = shard + 1 == NSHARD ? 0 : shard + 1;
+  }
+  return -1;
+}
+
+// movement worker: dispatch until every unit is claimed
+__device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& S, Scratch& W) {
+  int shard = wave_id();
+  for (;;) {
+    const int u = claim_unit(a, S, shard);
+    if (u < 0) break;
+    dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
+  }
+}
+
 // One wavefront combines nt <= CT tokens.  Each token has KS = k + S source
-// rows in O: its k routed slots (weight w, absent when the expert is not
-// local) followed by its S shared-expert rows (weight 1, present for tokens of
-// rank 0).  They are summed in that order in fp32.  KS is a template constant
-// so that every lane keeps about 16 row vectors in flight.
-template <int KS>
+// rows: its k routed slots (weight w, absent when the expert is not local)
+// followed by its S shared-expert rows (weight 1, present for tokens of rank
+// 0).  They are summed in that order in fp32.  A source row is O (bf16) or,
+// when GEMM1 is split NS ways, the bf16 rounding of its NS fp32 partials
+// added in split order.  KS and NS are template constants so that every lane
+// keeps about 16 row vectors in flight.
+template <int KS, int NS>
 __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
-  constexpr int P = KS >= 16 ? 1 : 16 / KS;  // positions per lane per pass
+  constexpr int NV = NS == 1 ? 1 : 2 * NS;                    // 16-byte loads per source row
+  constexpr int P = KS * NV >= 16 ? 1 : 16 / (KS * NV);       // positions per lane per pass
+  constexpr int JB = KS * NV <= 32 ? KS : (32 / NV);          // source rows per load batch
   const int lane = lane_id();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
   for (int v0 = lane; v0 < total; v0 += P * WAVE) {
-    u32x4_t o[P][KS];
     int tt[P], cc[P];
+    float acc[P][8];
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       const int v = v0 + i * WAVE;
       tt[i] = v < total ? v / VPR : -1;
       cc[i] = v < total ? v - tt[i] * VPR : 0;
 #pragma unroll
-      for (int j = 0; j < KS; ++j) {
-        const int s = tt[i] >= 0 ? sl[tt[i] * KS + j] : -1;
-        if (s >= 0) o[i][j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
-      }
+      for (int e = 0; e < 8; ++e) acc[i][e] = 0.0f;
+    }
+#pragma unroll
+    for (int j0 = 0; j0 < KS; j0 += JB) {
+      u32x4_t o[P][JB][NV];
+#pragma unroll
+      for (int i = 0; i < P; ++i)
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int j = j0 + jj;
+          const int s = (j < KS && tt[i] >= 0) ? sl[tt[i] * KS + j] : -1;
+          if (s < 0) continue;
+          if constexpr (NS == 1) {
+            o[i][jj][0] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
+          } else {
+#pragma unroll
+            for (int p = 0; p < NS; ++p) {
+              const u32x4_t* src =
+                  reinterpret_cast<const u32x4_t*>(a.part + ((size_t)p * a.prow + s) * a.H + cc[i] * 8);
+              o[i][jj][2 * p] = src[0];
+              o[i][jj][2 * p + 1] = src[1];
+            }
+          }
+        }
+#pragma unroll
+      for (int i = 0; i < P; ++i)
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int j = j0 + jj;
+          if (j >= KS || tt[i] < 0 || sl[tt[i] * KS + j] < 0) continue;
+          const float w = wt[tt[i] * KS + j];
+          float ov[8];
+          if constexpr (NS == 1) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              ov[2 * q] = bf16_lo(o[i][jj][0][q]);
+              ov[2 * q + 1] = bf16_hi(o[i][jj][0][q]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              float t = __uint_as_float(o[i][jj][e >> 2][e & 3]);
+#pragma unroll
+              for (int p = 1; p < NS; ++p) t += __uint_as_float(o[i][jj][2 * p + (e >> 2)][e & 3]);
+              ov[e] = bf16_to_f32(f32_to_bf16(t));
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[i][e] += w * ov[e];
+        }
     }
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       if (tt[i] < 0) continue;
-      float acc[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-#pragma unroll
-      for (int j = 0; j < KS; ++j) {
-        if (sl[tt[i] * KS + j] < 0) continue;
-        const float w = wt[tt[i] * KS + j];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += w * bf16_lo(o[i][j][q]);
-          acc[2 * q + 1] += w * bf16_hi(o[i][j][q]);
-        }
-      }
       u32x4_t r;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) r[q] = pack_bf16x2(acc[2 * q], acc[2 * q + 1]);
+      for (int q = 0; q < 4; ++q) r[q] = pack_bf16x2(acc[i][2 * q], acc[i][2 * q + 1]);
       __builtin_nontemporal_store(r, reinterpret_cast<u32x4_t*>(a.y + (size_t)(g0 + tt[i]) * a.H + cc[i] * 8));
     }
   }
+  __builtin_amdgcn_s_waitcnt(0);
 }
 
 __device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
@@ -273,8 +412,11 @@ __device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int
     wt[lane] = w;
   }
   __builtin_amdgcn_wave_barrier();
-  switch (ks) {
-#define MOE_COMBINE_CASE(n) case n: combine_body<n>(a, sl, wt, g0, nt); break;
+  switch (ks * 8 + a.nsplit) {
+#define MOE_COMBINE_CASE(n)                                       \
+  case n * 8 + 1: combine_body<n, 1>(a, sl, wt, g0, nt); break; \
+  case n * 8 + 2: combine_body<n, 2>(a, sl, wt, g0, nt); break; \
+  case n * 8 + 4: combine_body<n, 4>(a, sl, wt, g0, nt); break;
     MOE_COMBINE_CASE(1) MOE_COMBINE_CASE(2) MOE_COMBINE_CASE(3) MOE_COMBINE_CASE(4)
     MOE_COMBINE_CASE(5) MOE_COMBINE_CASE(6) MOE_COMBINE_CASE(7) MOE_COMBINE_CASE(8)
     MOE_COMBINE_CASE(9) MOE_COMBINE_CASE(10) MOE_COMBINE_CASE(11) MOE_COMBINE_CASE(12)
@@ -323,12 +465,9 @@ __device__ __forceinline__ void signal_done(int* p) {
   if (threadIdx.x == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Runs the tile; returns true when it completed an output tile (GEMM0 tile,
-// or the last-arriving split of a GEMM1 tile, which did the reduction).
-// One mainloop instance serves both GEMMs; only the operands and the
-// epilogue differ.
-__device__ __forceinline__ bool run_gemm(const FwdArgs& a, const Sched& S, Scratch& W, const TileRef& r, int mtile_id,
-                                         char* ring) {
+// Runs one GEMM0 tile or one split of a GEMM1 tile.  One mainloop instance
+// serves both GEMMs; only the operands and the epilogue differ.
+__device__ __forceinline__ void run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* ring) {
   const int qs = r.q * S.nseg + r.seg;
   const size_t orow = (size_t)S.row0[qs] + (size_t)r.mt * BM;
   const int n0 = r.nt * BN;
@@ -355,29 +494,13 @@ __device__ __forceinline__ bool run_gemm(const FwdArgs& a, const Sched& S, Scrat
   gemm::mainloop(acc, Aop, ld, r.rows, Bop, ld, b_rows, Kd, ring);
   if (r.ph == 0) {
     gemm::store_silu_mul(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
-    return true;
+    return;
   }
-  uint16_t* out = a.O + orow * a.H + n0;
   if (a.nsplit == 1) {
-    gemm::store_bf16(acc, out, a.H, r.rows, a.H - n0);
-    return true;
+    gemm::store_bf16(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0);
+  } else {
+    gemm::store_f32(acc, a.part + ((size_t)r.ks * a.prow + orow) * a.H + n0, a.H, r.rows, a.H - n0);
   }
-  // split-K: publish this split's partial; the last arrival reduces in order
-  const size_t tile = (size_t)mtile_id * a.nt1 + r.nt;
-  float* parts = a.part + tile * a.nsplit * (size_t)(BM * BN);
-  gemm::store_partial(acc, parts + (size_t)r.ks * (BM * BN));
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0)
-    W.bc[3] = __hip_atomic_fetch_add(&a.ctl[CTL_READY + 2 * a.mt_max + tile], 1, __ATOMIC_RELEASE,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  const bool last = W.bc[3] == a.nsplit - 1;
-  __syncthreads();
-  if (!last) return false;
-  if (a.nsplit == 2) gemm::reduce_store<2>(parts, (size_t)(BM * BN), out, a.H, r.rows, a.H - n0);
-  else gemm::reduce_store<4>(parts, (size_t)(BM * BN), out, a.H, r.rows, a.H - n0);
-  return true;
 }
 
 // ===========================================================================
@@ -443,29 +566,66 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
 // dispatched row, an Hbuf/O row or a partial before it is published, so no
 // stale copy of those lines can sit in the consumer's L1 or L2 (caches are
 // invalidated at kernel start).
-__device__ __forceinline__ bool wait_geq(const FwdArgs& a, Scratch& W, const int* p, int target) {
-  if (a.inject_stall) target += 1 << 30;
-  if (threadIdx.x == 0) {
-    int ok = 1;
-    if (ld_relaxed(p) < target) {
-      const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
-      while (ld_relaxed(p) < target) {
-        if (ld_relaxed(&a.ctl[CTL_ABORT])) { ok = 0; break; }
-        if (now_ticks() > deadline) {
-          st_relaxed(&a.ctl[CTL_ABORT], 1);
-          atomicOr(a.err, ERR_TIMEOUT);
-          ok = 0;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(2);
+// One lane polls *p until it reaches target, backing off exponentially up to
+// about 0.85 us between reads (many waiters poll the same few lines); the
+// abort word and the deadline are checked every eighth read.  Returns false
+// on abort or timeout.
+__device__ __forceinline__ bool poll_geq(const FwdArgs& a, const int* p, int target) {
+  if (ld_relaxed(p) >= target) return true;
+  const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
+  int backoff = 1;
+  for (int it = 1;; ++it) {
+    for (int i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(4);
+    if (ld_relaxed(p) >= target) return true;
+    backoff = min(backoff * 2, 8);
+    if ((it & 7) == 0) {
+      if (ld_relaxed(&a.ctl[CTL_ABORT])) return false;
+      if (now_ticks() > deadline) {
+        st_relaxed(&a.ctl[CTL_ABORT], 1);
+        atomicOr(a.err, ERR_TIMEOUT);
+        return false;
       }
     }
-    W.bc[2] = ok;
   }
+}
+
+__device__ __forceinline__ bool wait_geq(const FwdArgs& a, Scratch& W, const int* p, int target) {
+  if (a.inject_stall) target += 1 << 30;
+  if (threadIdx.x == 0) W.bc[2] = poll_geq(a, p, target) ? 1 : 0;
   __syncthreads();
   const int ok = W.bc[2];
   __syncthreads();
   return ok != 0;
+}
+
+// A compute worker whose GEMM0 row tile is not dispatched yet moves rows
+// itself instead of idling (movement stealing, the mirror image of the
+// section 3.2.2 bubble stealing): each wavefront claims and copies one
+// dispatch unit, then the workgroup checks the counter again.  Once every
+// unit is claimed it polls.
+__device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scratch& W, const int* p, int target) {
+  if (a.inject_stall) target += 1 << 30;
+  const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int st = ld_relaxed(p) >= target ? 1 : 0;
+      if (!st && W.dexh) st = poll_geq(a, p, target) ? 1 : -1;
+      else if (!st && (ld_relaxed(&a.ctl[CTL_ABORT]) || now_ticks() > deadline)) {
+        st_relaxed(&a.ctl[CTL_ABORT], 1);
+        atomicOr(a.err, ERR_TIMEOUT);
+        st = -1;
+      }
+      W.bc[2] = st;
+    }
+    __syncthreads();
+    const int st = W.bc[2];
+    __syncthreads();
+    if (st) return st > 0;
+    int shard = wave_id();
+    const int u = claim_unit(a, S, shard);
+    if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
+    else if (lane_id() == 0) W.dexh = 1;
+  }
 }
 
 __device__ __forceinline__ int claim(Scratch& W, int* q) {
@@ -477,52 +637,48 @@ __device__ __forceinline__ int claim(Scratch& W, int* q) {
 }
 
 // returns false when the launch was aborted
-__device__ __forceinline__ bool run_compute_tile(const FwdArgs& a, const Sched& S, Scratch& W, int t, char* ring) {
+__device__ __forceinline__ bool run_compute_tile(const FwdArgs& a, const Sched& S, Scratch& W, int t, char* ring,
+                                                 int ticket) {
+  const uint64_t t0 = a.trace ? now_ticks() : 0;
   TileRef r = decode_tile(a, S, t);
   const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
   if (r.ph == 0) {
-    if (r.seg < a.El && !wait_geq(a, W, &a.ctl[CTL_READY + id], r.rows)) return false;
-    run_gemm(a, S, W, r, id, ring);
-    signal_done(&a.ctl[CTL_READY + a.mt_max + id]);
+    if (r.seg < a.El && !wait_rows(a, S, W, &a.ctl[CTL_READY + id * CTL_PAD], r.rows)) return false;
   } else {
-    if (!wait_geq(a, W, &a.ctl[CTL_READY + a.mt_max + id], a.nt0)) return false;
-    if (run_gemm(a, S, W, r, id, ring)) signal_done(&a.ctl[CTL_G1DONE + r.q]);
+    if (!wait_geq(a, W, &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD], a.nt0)) return false;
   }
+  const uint64_t t1 = a.trace ? now_ticks() : 0;
+  run_gemm(a, S, r, ring);
+  signal_done(r.ph == 0 ? &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD] : &a.ctl[CTL_G1DONE + r.q * CTL_PAD]);
+  if (a.trace && threadIdx.x == 0) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
   return true;
 }
 
-// wavefront-level wait: lane 0 polls like wait_geq, the others follow
+// wavefront-level wait: lane 0 polls, the others follow
 __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target) {
   if (a.inject_stall) target += 1 << 30;
   int ok = 1;
-  if (lane_id() == 0 && ld_relaxed(p) < target) {
-    const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
-    while (ld_relaxed(p) < target) {
-      if (ld_relaxed(&a.ctl[CTL_ABORT])) { ok = 0; break; }
-      if (now_ticks() > deadline) {
-        st_relaxed(&a.ctl[CTL_ABORT], 1);
-        atomicOr(a.err, ERR_TIMEOUT);
-        ok = 0;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-  }
+  if (lane_id() == 0) ok = poll_geq(a, p, target) ? 1 : 0;
   return __builtin_amdgcn_readfirstlane(ok) != 0;
 }
 
-// combine units in chunk order, claimed per wavefront; chunk q's units wait
+// combine units of chunks [q0, q1) by worker w of n; chunk q's units wait
 // until every GEMM1 tile of chunk q is done
-__device__ __forceinline__ bool combine_loop(const FwdArgs& a, const Sched& S, Scratch& W) {
-  for (;;) {
-    const int u = wave_claim(&a.ctl[CTL_Q_COMB]);
-    if (u >= S.n_comb) return true;
-    int q = 0;
-    while (q + 1 < S.K && S.cstart[q + 1] <= u) ++q;
-    if (!wave_wait_geq(a, &a.ctl[CTL_G1DONE + q], S.g1need[q])) return false;
-    const int g0 = S.bnd[q] + (u - S.cstart[q]) * CT;
-    combine_tokens(a, W, g0, min(CT, S.bnd[q + 1] - g0));
+__device__ __forceinline__ bool combine_chunks(const FwdArgs& a, const Sched& S, Scratch& W, int q0, int q1, int w,
+                                               int n) {
+  for (int q = q0; q < q1; ++q) {
+    int u = S.cstart[q] + w * NWF + wave_id();
+    if (u >= S.cstart[q + 1]) continue;
+    const uint64_t t0 = a.trace ? now_ticks() : 0;
+    if (!wave_wait_geq(a, &a.ctl[CTL_G1DONE + q * CTL_PAD], S.g1need[q])) return false;
+    const uint64_t t1 = a.trace ? now_ticks() : 0;
+    for (; u < S.cstart[q + 1]; u += n * NWF) {
+      const int g0 = S.bnd[q] + (u - S.cstart[q]) * CT;
+      combine_tokens(a, W, g0, min(CT, S.bnd[q + 1] - g0));
+    }
+    if (a.trace && lane_id() == 0) trace_rec(a, 4, w, q | (wave_id() << 8), t0, t1, now_ticks());
   }
+  return true;
 }
 
 // ===========================================================================
@@ -534,6 +690,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
   const int tid = threadIdx.x;
+  const uint64_t t_entry = a.trace ? now_ticks() : 0;
 
   if (blockIdx.x == 0)
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
@@ -541,35 +698,44 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   prologue_plan(a, S, W);
   build_sched(a, S, W, S.K);
 
-  if (tid == 0) W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
+  if (tid == 0) {
+    W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
+    W.dexh = 0;
+  }
   __syncthreads();
-  const bool mover = W.bc[0] < S.c;
+  const int ticket = __builtin_amdgcn_readfirstlane(W.bc[0]);
+  const bool mover = ticket < S.c;
+  const int N = gridDim.x;
+  // chunks whose combine the movers do alone; the rest is the final combine
+  const int qa = S.final_all ? S.K - 1 : S.K;
+  const uint64_t t_sched = a.trace ? now_ticks() : 0;
   __syncthreads();
 
   bool ok = true;
   if (mover) {
-    // dispatch: every token row, in token (hence chunk) order, per wavefront
-    for (;;) {
-      const int u = wave_claim(&a.ctl[CTL_Q_DISP]);
-      if (u >= S.n_disp) break;
-      dispatch_unit(a, &S, W, u, true);
-    }
+    // dispatch: every token row, in token (hence chunk) order
+    dispatch_claimed(a, S, W);
     __syncthreads();
+    if (a.trace && tid == 0) trace_rec(a, 3, ticket, 0, t_sched, now_ticks(), 0);
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
     for (int i = 0; i < S.n_steal && ok; ++i) {
       const int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      ok = run_compute_tile(a, S, W, t, ring);
+      ok = run_compute_tile(a, S, W, t, ring, ticket);
     }
-    if (ok) combine_loop(a, S, W);
+    if (ok) ok = combine_chunks(a, S, W, 0, qa, ticket, S.c);
   } else {
     for (;;) {
       const int t = claim(W, &a.ctl[CTL_Q_COMP]);
       if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, ring)) { ok = false; break; }
+      if (!run_compute_tile(a, S, W, t, ring, ticket)) { ok = false; break; }
     }
-    // final combine on every worker (section 4)
-    if (ok && S.final_all) combine_loop(a, S, W);
+  }
+  // final combine of the last chunk on every worker (section 4)
+  if (ok && S.final_all) combine_chunks(a, S, W, S.K - 1, S.K, ticket, N);
+  if (a.trace) {
+    __syncthreads();
+    if (tid == 0) trace_rec(a, 1, ticket, mover ? 1 : 0, t_entry, t_sched, now_ticks());
   }
 }
 
@@ -581,12 +747,7 @@ __global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {
   const int tid = threadIdx.x;
   if (blockIdx.x == 0)
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
-  const int n = ceil_div(a.T, DT);
-  for (;;) {
-    const int u = wave_claim(&a.ctl[CTL_SQ + 0]);
-    if (u >= n) break;
-    dispatch_unit(a, nullptr, W, u, false);
-  }
+  dispatch_static(a, W, blockIdx.x * NWF + wave_id(), gridDim.x * NWF);
 }
 
 template <int PH>
@@ -600,7 +761,7 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
   for (int q = 0; q < S.K; ++q)
     count += S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
   for (;;) {
-    int t = claim(W, &a.ctl[CTL_SQ + 64 * qslot]);
+    int t = claim(W, &a.ctl[CTL_SQ + CTL_PAD * qslot]);
     if (t >= count) break;
     int q = 0;
     for (;; ++q) {
@@ -609,7 +770,7 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
       t -= n;
     }
     TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + t);
-    run_gemm(a, S, W, r, S.mb[r.q * S.nseg + r.seg] + r.mt, ring);
+    run_gemm(a, S, r, ring);
   }
 }
 
@@ -619,9 +780,7 @@ __global__ void __launch_bounds__(FNTH, 1) serial_gemm1_kernel(FwdArgs a) { seri
 __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   __shared__ Scratch W;
   const int n = ceil_div(a.T, CT);
-  for (;;) {
-    const int u = wave_claim(&a.ctl[CTL_SQ + 192]);
-    if (u >= n) break;
+  for (int u = blockIdx.x * NWF + wave_id(); u < n; u += gridDim.x * NWF) {
     const int g0 = u * CT;
     combine_tokens(a, W, g0, min(CT, a.T - g0));
   }

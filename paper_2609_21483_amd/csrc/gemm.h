@@ -267,56 +267,24 @@ __device__ __forceinline__ void store_bf16(const Acc& acc, uint16_t* out, int ld
     }
 }
 
-// split-K partial: fp32 tile in the lane-natural order (tile-contiguous,
-// 256 x 256 floats), read back by store_reduce with the same map
-__device__ __forceinline__ void store_partial(const Acc& acc, float* part) {
-  part = opaque(part);
+// GEMM1 split-K epilogue: this split's fp32 partial into a row-major buffer
+// (the combine adds the splits in a fixed order)
+__device__ __forceinline__ void store_f32(const Acc& acc, float* out, int ldo, int out_rows, int out_cols) {
+  ldo = opaque(ldo);
+  out = opaque(out);
   const OutMap m = out_map(TN);
+  const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m.row_l + out_dr(mb, r);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) part[row * TILE_N + m.col_l + nb * 32] = acc[mb][nb][r];
-    }
-}
-
-// split-K reduction in fixed order: P_0 + P_1 + ... + P_{S-1}, every partial
-// read back from memory (this split's own included, so the accumulators are
-// dead here), one 32-row block at a time; then bf16 into the tile
-template <int S>
-__device__ __forceinline__ void reduce_store(const float* parts, size_t part_stride, uint16_t* out, int ldo,
-                                             int out_rows, int out_cols) {
-  parts = opaque(parts);
-  part_stride = opaque(part_stride);
-  ldo = opaque(ldo);
-  const OutMap m = out_map(TN);
-  const uint32_t lbase = (uint32_t)(m.row_l * TILE_N + m.col_l);
-  const uint32_t obase = (uint32_t)(m.row_l * ldo + m.col_l);
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    float v[S][16][NB];
-#pragma unroll
-    for (int k = 0; k < S; ++k)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) v[k][r][nb] = parts[k * part_stride + lbase + out_dr(mb, r) * TILE_N + nb * 32];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int dr = out_dr(mb, r);
       if (m.row_l + dr < out_rows) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          float t = v[0][r][nb];
-#pragma unroll
-          for (int k = 1; k < S; ++k) t += v[k][r][nb];
-          if (m.col_l + nb * 32 < out_cols) out[obase + (uint32_t)(dr * ldo) + nb * 32] = (uint16_t)f32_to_bf16(t);
-        }
+        for (int nb = 0; nb < NB; ++nb)
+          if (m.col_l + nb * 32 < out_cols) out[base + (uint32_t)(dr * ldo) + nb * 32] = acc[mb][nb][r];
       }
     }
-  }
 }
 
 }  // namespace gemm

@@ -77,7 +77,10 @@ struct FwdArgs {
   uint16_t* A;
   uint16_t* Hb;
   uint16_t* O;
-  float* part;    // split-K partials (nsplit > 1)
+  float* part;    // split-K partials of GEMM1, fp32 [nsplit][prow][H] (nsplit > 1)
+  size_t prow;    // rows per split in part (the capacity of O)
+  long long* trace;  // timeline records (NULL: off); word 0 counts records
+  int trace_cap;     // records that fit
   // control
   int32_t* ctl;       // this launch's control set
   int32_t* ctl_next;  // cleared for the next launch

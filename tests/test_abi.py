@@ -32,7 +32,7 @@ def cfg_for(shape, **kw):
 @pytest.mark.parametrize("field,value", [
     ("hidden", 100), ("hidden", 0), ("ffn", 96), ("top_k", 0), ("top_k", 9), ("n_experts", 0),
     ("n_local_experts", 0), ("first_local_expert", 7), ("n_src_ranks", 0), ("tokens_per_rank", 0),
-    ("n_shared_experts", 9), ("n_workers", -1),
+    ("n_shared_experts", 9), ("n_workers", -1), ("gemm1_split", 3), ("gemm1_split", 8),
 ])
 def test_init_rejects_bad_config(field, value):
     c = cfg_for(W.TINY, **{field: value})
@@ -40,6 +40,15 @@ def test_init_rejects_bad_config(field, value):
         B.moe_init(c)
     assert ei.value.status in (B.MOE_ERR_INVALID_ARG, B.MOE_ERR_UNSUPPORTED)
     assert B.moe_last_error()
+
+
+def test_init_rejects_row_buffer_over_4gib():
+    # T * min(k, E_l) rows of H bf16 must stay under 4 GiB (32-bit offsets)
+    c = cfg_for(W.TINY, n_src_ranks=16, tokens_per_rank=65536, hidden=4096, n_experts=8, top_k=1,
+                n_local_experts=1)
+    with pytest.raises(B.MoeError) as ei:
+        B.moe_init(c)
+    assert ei.value.status == B.MOE_ERR_UNSUPPORTED
 
 
 def test_init_rejects_bad_calib():

@@ -48,10 +48,10 @@ def run_modes(B, layer, c, idx, w, modes=("dynamic", "static", "serial"), forced
     return outs
 
 
-def check_case(B, c, rows=None, forced=(), check_A=False):
+def check_case(B, c, rows=None, forced=(), check_A=False, gemm1_split=0):
     shape = c.shape
     idx, w = c.oracle_route()
-    layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+    layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2, gemm1_split=gemm1_split)
     try:
         outs = run_modes(B, layer, c, idx, w, forced=forced)
         rows = np.arange(shape.T) if rows is None else rows
@@ -93,6 +93,15 @@ def test_tiny_all_rows_all_plans(B):
 def test_edge_shapes(B, shape):
     c = make_case(shape.with_(w_std=0.05))
     check_case(B, c, forced=FORCED_SMALL, check_A=True)
+
+
+@pytest.mark.parametrize("split", [1, 2, 4])
+def test_gemm1_split_factors(B, split):
+    """GEMM1 split 1, 2 or 4 ways over F (the combine adds the fp32 partials
+    in split order); shared experts and a ragged row tail included."""
+    shape = W.MoeShape("split", 92, 3, 70, 128, 512, 8, 2, 4, n_shared_experts=1)
+    c = make_case(shape.with_(w_std=0.05))
+    check_case(B, c, forced=[(8, 2, 3, 1), (100, 4, 0, 0)], gemm1_split=split)
 
 
 def test_no_local_pairs(B):
