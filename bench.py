@@ -6,12 +6,17 @@ layer (moe_forward: dispatch, GEMM0 + SiLU*up, GEMM1, combine) in the
 dynamic-split megakernel.  Inputs are resident in HBM before timing starts.
 
 Prints one JSON line.  `value` is tokens/s of whole steps; `layer_us` is the
-MoE-layer time alone (the megakernel, from HIP events on the launch stream),
-next to the static-split and serial baselines measured the same way.
+MoE-layer time alone (the megakernel, from HIP events on its launch stream,
+the window the paper times: end of routing to end of combine), next to the
+static-split and serial baselines measured the same way.  `roofline` rates the
+megakernel (the dominant kernel) against the bf16 MFMA peak; `phases` comes
+from one extra traced launch after the timed region and gives the movement
+workers' HBM rate and the compute workers' MFMA utilisation.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -23,6 +28,11 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "MoE-layer µs + tokens/s at 1 GPU; HBM GB/s & MFMA util vs peak"
+# sources of the megakernel: a traffic figure measured on other sources is stale
+KERNEL_SOURCES = ("paper_2609_21483_amd/csrc/forward.hip", "paper_2609_21483_amd/csrc/gemm.h",
+                  "paper_2609_21483_amd/csrc/common.h", "paper_2609_21483_amd/csrc/kernels.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "megakernel_traffic.json")
 
 
 def parse():
@@ -35,7 +45,31 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128)
     ap.add_argument("--modes", default="static,serial", help="baselines timed next to the dynamic mode")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run a plain torch copy of this many MiB (the scale for PMC byte counters)")
     return ap.parse_args()
+
+
+def kernel_sources_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per megakernel launch from the committed PMC measurement, or
+    None when there is none for this workload or the kernel changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    rec = d.get(workload)
+    if not rec or rec.get("sources") != kernel_sources_hash():
+        return None
+    return float(rec["bytes_per_launch"])
 
 
 def time_forward(B, layer, x, idx, w, y, mode, steps, warmup, stream):
@@ -53,6 +87,49 @@ def time_forward(B, layer, x, idx, w, y, mode, steps, warmup, stream):
     if st != B.MOE_OK:
         raise RuntimeError(f"{mode}: {B.moe_last_error()}")
     return [a.elapsed_time(b) * 1e3 for a, b in ev]  # us
+
+
+def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
+    """One traced launch: movement bytes over the movers' dispatch window and
+    the compute workers' MFMA utilisation over their busy time."""
+    import numpy as np
+    import torch
+    buf = torch.zeros(64 + 32 * (1 << 17), dtype=torch.uint8, device="cuda")
+    B.moe_set_trace(layer.h, buf)
+    try:
+        layer.forward(x, idx, w, y, "dynamic", stream=stream)
+        torch.cuda.synchronize()
+    finally:
+        B.moe_set_trace(layer.h, None)
+    tr = B.read_trace(buf)
+    wgs, tiles, disp, comb = (tr[tr["kind"] == k] for k in (1, 2, 3, 4))
+    if len(wgs) == 0:
+        return None
+    t0 = wgs["t0"].min()
+    us = lambda t: (t - t0) / 100.0
+    H = shape.hidden
+    X, U = int(stats[0]), int(stats[3] + stats[4])
+    disp_bytes = (U + X) * 2.0 * H
+    comb_bytes = (X + shape.tokens_per_rank * shape.n_shared_experts) * 2.0 * H + shape.T * 2.0 * H
+    disp_end = float(us(disp["t1"]).max()) if len(disp) else float("nan")
+    busy = float(((tiles["t2"] - tiles["t1"]) / 100.0).sum())
+    n_comp = int((wgs["id"] == 0).sum())
+    span = float(us(wgs["t2"]).max())
+    comb_span = float((us(comb["t2"]).max() - us(comb["t1"]).min())) if len(comb) else float("nan")
+    per_cu_peak = PEAK_BF16_TFLOPS / 256.0
+    return {
+        "traced_layer_us": span,
+        "dispatch_us": disp_end,
+        "dispatch_hbm_gbs": disp_bytes / (disp_end * 1e-6) / 1e9,
+        "dispatch_frac_of_peak": disp_bytes / (disp_end * 1e-6) / 1e9 / PEAK_HBM_GBS,
+        "combine_us": comb_span,
+        "combine_hbm_gbs": comb_bytes / (comb_span * 1e-6) / 1e9,
+        "compute_workers": n_comp,
+        "compute_busy_frac": busy / (n_comp * span) if n_comp else None,
+        "mfma_util_while_busy": flops / (busy * 1e-6) / 1e12 / per_cu_peak,
+        "note": "one traced launch (tracing adds overhead); dispatch includes rows moved by compute workers "
+                "that steal movement while their tiles wait",
+    }
 
 
 def cpu_baseline(shape, c, rows_n):
@@ -115,14 +192,11 @@ def main():
     torch.cuda.synchronize()
     print("[bench] inputs resident; warmup", file=sys.stderr, flush=True)
 
-    def step():
+    for _ in range(args.warmup):
         layer.route(x, wg, bias, idx, w, stream=stream)
         layer.forward(x, idx, w, y, "dynamic", stream=stream)
-
-    for _ in range(args.warmup):
-        step()
     torch.cuda.synchronize()
-    # timed region: whole steps, with per-launch events around the megakernel
+    # timed region: whole steps, with events around each megakernel launch
     fwd_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -160,11 +234,20 @@ def main():
     baselines = {}
     for m in [m for m in args.modes.split(",") if m]:
         us = time_forward(B, layer, x, idx, w, y, m, args.steps, args.warmup, stream)
-        baselines[m] = {"layer_us_median": float(np.median(us)), "tokens_per_s": shape.T / (float(np.median(us)) * 1e-6)}
+        baselines[m] = {"layer_us_median": float(np.median(us)), "tokens_per_s": shape.T / (float(np.median(us)) * 1e-6),
+                        "dynamic_speedup": float(np.median(us)) / lat}
         print(f"[bench] {m} done", file=sys.stderr, flush=True)
+    phases = traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops)
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
 
     out = {
-        "metric": "MoE-layer tokens/s at 1 GPU (route + dynamic-split megakernel)",
+        "metric": METRIC,
         "value": shape.T / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -187,8 +270,10 @@ def main():
                  "t_pred_us": plan.t_pred_s * 1e6, "N": N, "calibrated": calib is not None},
         "baselines": baselines,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "kernel": "moe_megakernel", "flop_per_launch": flops},
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(shape.name),
+                     "kernel": "moe_megakernel", "flop_per_launch": flops,
+                     "flop_per_unit": "6*H*F per routed (token, local expert) row and per shared-expert row"},
+        "phases": phases,
         "context": "paper: 2.89x geomean MoE-layer speedup on 4xH100 SXM, EP=4, BF16 - different hardware and "
                    "baselines, not a target",
     }

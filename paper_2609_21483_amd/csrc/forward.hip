@@ -459,15 +459,13 @@ __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S,
   return r;
 }
 
-__device__ __forceinline__ void signal_done(int* p) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // Runs one GEMM0 tile or one split of a GEMM1 tile.  One mainloop instance
 // serves both GEMMs; only the operands and the epilogue differ.
-__device__ __forceinline__ void run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* ring) {
+// When claim_q is given, thread 0 claims the next queue entry between the
+// mainloop and the epilogue (returned on thread 0), so the claim's round trip
+// overlaps the epilogue stores.
+template <int CP>
+__device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* ring, int* claim_q) {
   const int qs = r.q * S.nseg + r.seg;
   const size_t orow = (size_t)S.row0[qs] + (size_t)r.mt * BM;
   const int n0 = r.nt * BN;
@@ -492,15 +490,16 @@ __device__ __forceinline__ void run_gemm(const FwdArgs& a, const Sched& S, const
   gemm::Acc acc;
   gemm::zero(acc);
   gemm::mainloop(acc, Aop, ld, r.rows, Bop, ld, b_rows, Kd, ring);
+  int nxt = 0;
+  if (claim_q && threadIdx.x == 0) nxt = fetch_add_relaxed(claim_q, 1);
   if (r.ph == 0) {
-    gemm::store_silu_mul(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
-    return;
-  }
-  if (a.nsplit == 1) {
-    gemm::store_bf16(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0);
+    gemm::store_silu_mul<CP>(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
+  } else if (a.nsplit == 1) {
+    gemm::store_bf16<CP>(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0);
   } else {
-    gemm::store_f32(acc, a.part + ((size_t)r.ks * a.prow + orow) * a.H + n0, a.H, r.rows, a.H - n0);
+    gemm::store_f32<CP>(acc, a.part + ((size_t)r.ks * a.prow + orow) * a.H + n0, a.H, r.rows, a.H - n0);
   }
+  return nxt;
 }
 
 // ===========================================================================
@@ -636,21 +635,37 @@ __device__ __forceinline__ int claim(Scratch& W, int* q) {
   return r;
 }
 
-// returns false when the launch was aborted
-__device__ __forceinline__ bool run_compute_tile(const FwdArgs& a, const Sched& S, Scratch& W, int t, char* ring,
-                                                 int ticket) {
-  const uint64_t t0 = a.trace ? now_ticks() : 0;
-  TileRef r = decode_tile(a, S, t);
-  const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
-  if (r.ph == 0) {
-    if (r.seg < a.El && !wait_rows(a, S, W, &a.ctl[CTL_READY + id * CTL_PAD], r.rows)) return false;
-  } else {
-    if (!wait_geq(a, W, &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD], a.nt0)) return false;
+// Runs up to max_tiles compute tiles from the shared queue (all of them for a
+// compute worker, n_steal for a movement worker).  A tile waits for its inputs
+// (GEMM0: its rows dispatched; GEMM1: every GEMM0 column tile of its row
+// tile), runs, and is published once every thread's agent-coherent output
+// stores have completed, with one relaxed increment.  The next tile is claimed
+// between mainloop and epilogue.  Returns false when the launch was aborted.
+__device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, Scratch& W, char* ring, int ticket,
+                                              int max_tiles) {
+  if (max_tiles <= 0) return true;
+  int t = claim(W, &a.ctl[CTL_Q_COMP]);
+  for (int done = 1; t < S.n_comp; ++done) {
+    const uint64_t t0 = a.trace ? now_ticks() : 0;
+    const TileRef r = decode_tile(a, S, t);
+    const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
+    if (r.ph == 0) {
+      if (r.seg < a.El && !wait_rows(a, S, W, &a.ctl[CTL_READY + id * CTL_PAD], r.rows)) return false;
+    } else {
+      if (!wait_geq(a, W, &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD], a.nt0)) return false;
+    }
+    const uint64_t t1 = a.trace ? now_ticks() : 0;
+    const bool more = done < max_tiles;
+    const int nxt = run_gemm<gemm::CP_SC1>(a, S, r, ring, more ? &a.ctl[CTL_Q_COMP] : nullptr);
+    __builtin_amdgcn_s_waitcnt(0);
+    if (threadIdx.x == 0) W.bc[1] = more ? nxt : S.n_comp;
+    __syncthreads();  // every thread's output stores have completed
+    if (threadIdx.x == 0) {
+      fetch_add_relaxed(r.ph == 0 ? &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD] : &a.ctl[CTL_G1DONE + r.q * CTL_PAD], 1);
+      if (a.trace) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
+    }
+    t = W.bc[1];  // rewritten only after the next mainloop's barriers
   }
-  const uint64_t t1 = a.trace ? now_ticks() : 0;
-  run_gemm(a, S, r, ring);
-  signal_done(r.ph == 0 ? &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD] : &a.ctl[CTL_G1DONE + r.q * CTL_PAD]);
-  if (a.trace && threadIdx.x == 0) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
   return true;
 }
 
@@ -718,18 +733,10 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
     __syncthreads();
     if (a.trace && tid == 0) trace_rec(a, 3, ticket, 0, t_sched, now_ticks(), 0);
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
-    for (int i = 0; i < S.n_steal && ok; ++i) {
-      const int t = claim(W, &a.ctl[CTL_Q_COMP]);
-      if (t >= S.n_comp) break;
-      ok = run_compute_tile(a, S, W, t, ring, ticket);
-    }
+    ok = compute_tiles(a, S, W, ring, ticket, S.n_steal);
     if (ok) ok = combine_chunks(a, S, W, 0, qa, ticket, S.c);
   } else {
-    for (;;) {
-      const int t = claim(W, &a.ctl[CTL_Q_COMP]);
-      if (t >= S.n_comp) break;
-      if (!run_compute_tile(a, S, W, t, ring, ticket)) { ok = false; break; }
-    }
+    ok = compute_tiles(a, S, W, ring, ticket, 1 << 30);
   }
   // final combine of the last chunk on every worker (section 4)
   if (ok && S.final_all) combine_chunks(a, S, W, S.K - 1, S.K, ticket, N);
@@ -760,17 +767,20 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
   int count = 0;
   for (int q = 0; q < S.K; ++q)
     count += S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
-  for (;;) {
-    int t = claim(W, &a.ctl[CTL_SQ + CTL_PAD * qslot]);
-    if (t >= count) break;
-    int q = 0;
+  int* qh = &a.ctl[CTL_SQ + CTL_PAD * qslot];
+  int t = claim(W, qh);
+  while (t < count) {
+    int q = 0, u = t;
     for (;; ++q) {
       const int n = S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
-      if (t < n) break;
-      t -= n;
+      if (u < n) break;
+      u -= n;
     }
-    TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + t);
-    run_gemm(a, S, r, ring);
+    const TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + u);
+    const int nxt = run_gemm<gemm::CP_PLAIN>(a, S, r, ring, qh);
+    if (threadIdx.x == 0) W.bc[1] = nxt;
+    __syncthreads();
+    t = W.bc[1];  // rewritten only after the next mainloop's barriers
   }
 }
 

@@ -229,10 +229,22 @@ __device__ __forceinline__ OutMap out_map(int cols_per_wave) {
 }
 __device__ __forceinline__ int out_dr(int mb, int r) { return mb * 32 + 8 * (r >> 2) + (r & 3); }
 
+// Epilogues write through 16- or 32-bit buffer stores.  With CP = SC1 the
+// stores are agent-coherent: once they have completed (vmcnt 0) every XCD can
+// read them, so the tile can be published without an L2 write-back.
+constexpr int CP_PLAIN = 0, CP_SC1 = 16;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(uniform_ptr(static_cast<const char*>(p))), 0, -1,
+                                           0x00020000);
+}
+
 // GEMM0 epilogue: gate/up 32-column pairs -> bf16(silu(gate) * up); the tile
 // writes TILE_N/2 output columns
+template <int CP>
 __device__ __forceinline__ void store_silu_mul(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
   ldo = opaque(ldo);
+  const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
   const OutMap m = out_map(TN / 2);
   const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
 #pragma unroll
@@ -243,14 +255,16 @@ __device__ __forceinline__ void store_silu_mul(const Acc& acc, uint16_t* out, in
       if (m.row_l + dr < out_rows && m.col_l < out_cols) {
         const float g = acc[mb][0][r], u = acc[mb][1][r];
         const float hv = (g / (1.0f + __expf(-g))) * u;
-        out[base + (uint32_t)(dr * ldo)] = (uint16_t)f32_to_bf16(hv);
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(hv), rs, (base + (uint32_t)(dr * ldo)) * 2u, 0, CP);
       }
     }
 }
 
 // GEMM1 epilogue: bf16(acc) into the tile
+template <int CP>
 __device__ __forceinline__ void store_bf16(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
   ldo = opaque(ldo);
+  const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
   const OutMap m = out_map(TN);
   const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
 #pragma unroll
@@ -262,16 +276,18 @@ __device__ __forceinline__ void store_bf16(const Acc& acc, uint16_t* out, int ld
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
           if (m.col_l + nb * 32 < out_cols)
-            out[base + (uint32_t)(dr * ldo) + nb * 32] = (uint16_t)f32_to_bf16(acc[mb][nb][r]);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(acc[mb][nb][r]), rs,
+                                                  (base + (uint32_t)(dr * ldo) + nb * 32) * 2u, 0, CP);
       }
     }
 }
 
 // GEMM1 split-K epilogue: this split's fp32 partial into a row-major buffer
 // (the combine adds the splits in a fixed order)
+template <int CP>
 __device__ __forceinline__ void store_f32(const Acc& acc, float* out, int ldo, int out_rows, int out_cols) {
   ldo = opaque(ldo);
-  out = opaque(out);
+  const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
   const OutMap m = out_map(TN);
   const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
 #pragma unroll
@@ -282,7 +298,9 @@ __device__ __forceinline__ void store_f32(const Acc& acc, float* out, int ldo, i
       if (m.row_l + dr < out_rows) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
-          if (m.col_l + nb * 32 < out_cols) out[base + (uint32_t)(dr * ldo) + nb * 32] = acc[mb][nb][r];
+          if (m.col_l + nb * 32 < out_cols)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][r]), rs,
+                                                  (base + (uint32_t)(dr * ldo) + nb * 32) * 4u, 0, CP);
       }
     }
 }

@@ -102,6 +102,11 @@ class Case:
     def bias_np(self):
         return None if self.bias is None else self.bias.numpy()
 
+    def with_tokens(self, other: "Case") -> "Case":
+        """other's tokens, gate and bias with this case's expert weights."""
+        return Case(self.shape, self.layer, other.x, other.wg, other.bias,
+                    self.w1, self.w3, self.w2, self.ws1, self.ws3, self.ws2)
+
     def oracle_route(self):
         lg = oracle_logits(self.xu, self.wgu, self.bias_np)
         return O.softmax_topk(lg, self.shape.top_k)

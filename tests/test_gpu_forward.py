@@ -187,6 +187,27 @@ def test_repeat_launches_deterministic(B):
         layer.close()
 
 
+def test_relaunch_with_new_inputs(B):
+    """The same workspace and control sets serve launches whose tokens and
+    routing change: each result matches the oracle for its own inputs (no
+    stale rows from the previous launch)."""
+    shape = W.FINE_ZIPF.with_(tokens_per_rank=384)
+    c1 = make_case(shape)
+    c2 = make_case(shape.with_(wid=shape.wid + 50))
+    layer = B.MoeLayer(shape, c1.w1, c1.w3, c1.w2)
+    try:
+        for c in (c1, c2, c1):
+            idx, w = c.oracle_route()
+            outs = run_modes(B, layer, c, idx, w, modes=("dynamic", "serial"))
+            rows = pick_rows(shape, idx, per_rank=24, seed=7)
+            # c2 shares c1's expert weights (the layer packs them once)
+            y_ref = oracle_rows(c1.with_tokens(c), idx, w, rows)
+            for y in outs.values():
+                assert rel_err(bf16_to_f64(y[torch.from_numpy(rows).cuda()]), y_ref) <= TOL
+    finally:
+        layer.close()
+
+
 def test_timeout_path_recovers(B):
     """Host-forced stall: every wait targets an unreachable value, so the
     launch times out on its own bounded waits, reports MOE_ERR_TIMEOUT, and the
