@@ -223,8 +223,12 @@ void orc_plan(const orc_plan_in* in, orc_plan_out* out) {
   out->c = in->c[bc];
   out->K = in->K[bk];
   out->t_total = best;
-  /* bubble stealing at (c*, K*) */
-  double t_comm = (in->w_dispatch + in->w_combine) / in->bw[bc];       /* Eq 11 */
+  /* bubble stealing at (c*, K*).  Eq 11's communication is what the movement
+   * workers still have to do while the GEMMs run: dispatch and the combine of
+   * chunks 0..K-2; the last chunk's combine runs on all N workers after the
+   * GEMMs (section 4), so it is not part of this window. */
+  double kd = (double)in->K[bk];
+  double t_comm = (in->w_dispatch + (in->w_combine * (kd - 1.0)) / kd) / in->bw[bc];  /* Eq 11 */
   double w_partial = t_comm * in->flops[bc];                           /* Eq 12 */
   double w_steal = in->w_comp - w_partial;                             /* Eq 13 */
   if (w_steal < 0.0) w_steal = 0.0;

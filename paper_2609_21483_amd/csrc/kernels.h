@@ -124,7 +124,11 @@ __host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_c
       double t = cm_t_total(cb, ci, ki, w_comp, w_disp, w_comb);
       if (t < best) { best = t; bc = ci; bk = ki; }
     }
-  double t_comm = (w_disp + w_comb) / cb.bw[bc];             // Eq 11
+  // Eq 11 over the window the movement workers have while the GEMMs run:
+  // dispatch and the combine of chunks 0..K-2 (the last chunk's combine runs
+  // on all N workers afterwards)
+  double kd = (double)cb.kk[bk];
+  double t_comm = (w_disp + (w_comb * (kd - 1.0)) / kd) / cb.bw[bc];  // Eq 11
   double w_partial = t_comm * cb.fl[bc];                     // Eq 12
   double w_steal = w_comp - w_partial;                       // Eq 13
   if (w_steal < 0.0) w_steal = 0.0;

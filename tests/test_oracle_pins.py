@@ -397,10 +397,16 @@ def test_cost_model_tie_break_first_minimum(orc):
 
 
 def test_n_steal_formula_by_hand(orc):
-    # t_comm = 2e9/1e12 = 2 ms; W_partial = 2e-3 * 5e14 = 1e12; W_steal = 4e12 - 1e12 = 3e12;
-    # W_tile = 4e12/4000 = 1e9; n_steal = floor(3e12 / (100 * 1e9)) = 30
+    # Eq 11 counts dispatch plus the combine of chunks 0..K-2 (the last chunk's
+    # combine runs on every worker after the GEMMs).
+    # K = 1: t_comm = 1e9/1e12 = 1 ms; W_partial = 1e-3 * 5e14 = 5e11; W_steal = 4e12 - 5e11 = 3.5e12;
+    # W_tile = 4e12/4000 = 1e9; n_steal = floor(3.5e12 / (100 * 1e9)) = 35
     p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
-    assert p.n_steal == 30
+    assert p.n_steal == 35
+    # K = 2: t_comm = (1e9 + 1e9/2)/1e12 = 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12;
+    # n_steal = floor(3.25e12 / (100 * 1e9)) = 32
+    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
+    assert p.n_steal == 32
 
 
 def test_tile_count_bruteforce(orc):
