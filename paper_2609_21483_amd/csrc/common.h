@@ -19,7 +19,7 @@ constexpr int BM = 256;
 constexpr int BN = 256;
 constexpr int MAX_SPLIT = 4;    // split-K factor limit of GEMM1
 
-constexpr int DT = 4;           // tokens per dispatch unit (one wavefront; DT * top_k <= 64)
+constexpr int DT = 8;           // tokens per dispatch unit (one wavefront; DT * top_k <= 64)
 constexpr int CT = 4;           // tokens per combine unit (one wavefront)
 
 constexpr int MAX_EL = 64;      // local experts
