@@ -44,6 +44,8 @@ struct moe_handle {
   DevCalib dcal{};
   moe_ws_layout lay{};
   size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_ctl[2] = {0, 0}, off_part = 0;
+  size_t off_gwt = 0, off_glt = 0, off_gxn = 0, off_gwn = 0;  // gate scratch
+  size_t off_chg = 0, off_che = 0, off_chl = 0, off_tb = 0, off_tn = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
   const int32_t* tables_from = nullptr;
@@ -83,9 +85,10 @@ moe_status validate_cfg(const moe_config* c) {
   long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
   if (xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM > (1LL << 31) / 2)
     return fail(MOE_ERR_UNSUPPORTED, "too many routed rows");
-  // dispatch addresses the row buffer A with 32-bit byte offsets
-  if ((xmax + BM) * (long long)c->hidden * 2 >= (1LL << 32))
-    return fail(MOE_ERR_UNSUPPORTED, "dispatched rows (T * min(k, E_l) x H bf16) exceed 4 GiB");
+  // dispatch addresses the row buffer A, the split reduction the output rows
+  // O, with 32-bit byte offsets
+  if ((xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM) * (long long)c->hidden * 2 >= (1LL << 32))
+    return fail(MOE_ERR_UNSUPPORTED, "routed rows (T * min(k, E_l) + S * T_r) x H bf16 exceed 4 GiB");
   return MOE_OK;
 }
 
@@ -165,6 +168,15 @@ void compute_layout(moe_handle* h) {
   L.plan = take(sizeof(moe_plan));
   L.err = take(sizeof(int32_t) * 4);
   h->off_calib = take(sizeof(DevCalib));
+  h->off_gwt = take(sizeof(uint16_t) * (size_t)c.n_experts * c.hidden);
+  h->off_glt = take(sizeof(float) * (size_t)T * c.n_experts);
+  h->off_gxn = take(sizeof(float) * (size_t)T);
+  h->off_gwn = take(sizeof(float) * (size_t)c.n_experts);
+  h->off_chg = take(sizeof(int32_t) * (size_t)T * c.n_experts);
+  h->off_che = take(sizeof(int32_t) * (size_t)T * c.n_experts);
+  h->off_chl = take(sizeof(float) * (size_t)T * c.n_experts);
+  h->off_tb = take(sizeof(int32_t) * (size_t)T);
+  h->off_tn = take(sizeof(int32_t) * (size_t)T);
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_ctl[0] = take(sizeof(int32_t) * (size_t)h->ctl_words);
@@ -303,7 +315,9 @@ moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** 
     h->nsplit = cfg->ffn >= 3 * cfg->hidden ? 4 : (2 * cfg->ffn >= 3 * cfg->hidden ? 2 : 1);
     while (h->nsplit > 1 && cfg->ffn % (32 * h->nsplit)) h->nsplit /= 2;
   }
-  h->ctl_words = CTL_READY + 2 * h->mt_max * CTL_PAD;
+  // readiness counters per row tile (dispatched rows, GEMM0 columns, GEMM1
+  // columns) and, when GEMM1 is split, split arrivals per (row, column) tile
+  h->ctl_words = CTL_READY + (3 * h->mt_max + (h->nsplit > 1 ? h->mt_max * h->nt1 : 0)) * CTL_PAD;
   if (calib) {
     st = validate_calib(calib, N);
     if (st != MOE_OK) { delete h; return st; }
@@ -419,7 +433,7 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
   if (!topk_idx) return fail(MOE_ERR_INVALID_ARG, "topk_idx is NULL");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   TableArgs a = table_args(h, topk_idx);
-  zero_i32_kernel<<<1, 64, 0, s>>>(a.stats, 16);
+  zero_i32_kernel<<<1, 64, 0, s>>>(a.stats, ST_CANDS);
   tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_scan_kernel<<<1, NTH, 0, s>>>(a);
   tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);
@@ -442,32 +456,35 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   g.bias = logit_bias;
   g.topk_idx = topk_idx;
   g.topk_w = topk_w;
+  g.wgt = at<uint16_t>(h, h->off_gwt);
+  g.lt = at<float>(h, h->off_glt);
+  g.xn = at<float>(h, h->off_gxn);
+  g.wn = at<float>(h, h->off_gwn);
+  g.ch_g = at<int32_t>(h, h->off_chg);
+  g.ch_e = at<int32_t>(h, h->off_che);
+  g.ch_l = at<float>(h, h->off_chl);
+  g.tok_base = at<int32_t>(h, h->off_tb);
+  g.tok_n = at<int32_t>(h, h->off_tn);
+  g.stats = at<int32_t>(h, h->lay.stats);
   g.T = h->T;
   g.H = h->cfg.hidden;
   g.E = h->cfg.n_experts;
   g.k = top_k;
-  // per-thread block of logits: the largest of 4x4, 2x2, 1x1 (tokens x
-  // experts) that still gives the grid enough workgroups
-  auto groups = [&](int tpt, int ept, int* tq) {
-    const int eq = (g.E + ept - 1) / ept;
-    if (eq > NTH) return -1;
-    int t = std::max(1, NTH / eq);
-    while (t * tpt > 256) --t;
-    *tq = t;
-    return (h->T + t * tpt - 1) / (t * tpt);
-  };
-  int tq44, tq22, tq11;
-  const int n44 = groups(4, 4, &tq44), n22 = groups(2, 2, &tq22), n11 = groups(1, 1, &tq11);
-  if (n44 >= 512 || (n22 < 0 && n11 < 0)) {
-    g.tq = tq44;
-    gate_topk_kernel<4, 4><<<n44, NTH, 0, s>>>(g);
-  } else if (n22 >= 256 || n11 < 0) {
-    g.tq = tq22;
-    gate_topk_kernel<2, 2><<<n22, NTH, 0, s>>>(g);
-  } else {
-    g.tq = tq11;
-    gate_topk_kernel<1, 1><<<n11, NTH, 0, s>>>(g);
+  // |L - L~| <= (gamma_{H-1}(2^-24) + gamma_H(2^-23)) * sum_h |x_h w_h|: the
+  // defined recursive fp32 sum and an fp32 accumulation of the MFMA products
+  // allowed twice the unit roundoff; sum |x w| <= ||x|| ||w||; 1% for the norms
+  {
+    const double H = (double)g.H, u = std::ldexp(1.0, -24), u2 = std::ldexp(1.0, -23);
+    const double g1 = (H - 1.0) * u / (1.0 - (H - 1.0) * u), g2 = H * u2 / (1.0 - H * u2);
+    g.bound = (float)(1.01 * (g1 + g2));
   }
+  zero_i32_kernel<<<1, 64, 0, s>>>(g.stats + ST_CANDS, 1);
+  gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
+  gate_mfma_kernel<<<(h->T + 31) / 32, 4 * WAVE, 0, s>>>(g);
+  const int tok_blocks = (h->T + (NTH / 16) - 1) / (NTH / 16);
+  gate_cand_kernel<<<tok_blocks, NTH, 0, s>>>(g);
+  gate_chain_kernel<<<std::min(4096, std::max(1, (h->T * g.k * 3 / 2 + NTH - 1) / NTH)), NTH, 0, s>>>(g);
+  gate_final_kernel<<<tok_blocks, NTH, 0, s>>>(g);
   HIP_TRY(hipGetLastError());
   return moe_build_tables(h, topk_idx, stream);
 }

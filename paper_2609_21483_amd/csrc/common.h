@@ -44,16 +44,19 @@ constexpr int CTL_Q_COMP = 0;     // compute-tile queue head
 constexpr int CTL_TICKET = 16;    // arrival ticket -> role
 constexpr int CTL_ABORT = 32;     // set once any wait times out
 constexpr int CTL_SQ = 48;        // queue heads of the serial GEMM kernels (CTL_PAD apart)
-constexpr int CTL_G1DONE = 128;   // [MAX_K] GEMM1 tiles finished per chunk (CTL_PAD apart)
+constexpr int CTL_QC = 128;       // [NSHARD] combine-unit queue heads (CTL_PAD apart)
 constexpr int NSHARD = 8;         // dispatch-unit queue shards
 constexpr int CTL_QD = 256;       // [NSHARD] dispatch-unit queue heads (CTL_PAD apart)
 constexpr int CTL_READY = 384;    // [mt_max] dispatched rows per row tile (CTL_PAD apart),
-// then [mt_max] GEMM0 column tiles finished per row tile (CTL_PAD apart)
-static_assert(CTL_G1DONE + MAX_K * CTL_PAD <= CTL_QD, "control block overlap");
+// then [mt_max] GEMM0 column tiles finished per row tile (CTL_PAD apart),
+// then [mt_max] GEMM1 (column tile, split) items finished per row tile (CTL_PAD apart)
+static_assert(CTL_QC + NSHARD * CTL_PAD <= CTL_QD, "control block overlap");
 static_assert(CTL_QD + NSHARD * CTL_PAD <= CTL_READY, "control block overlap");
 
 // stats words written by the table builder
 constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;
+// written by the gate: candidates whose defined logit was evaluated (all tokens)
+constexpr int ST_CANDS = 8;
 
 // device error word values
 constexpr int ERR_TIMEOUT = 1;

@@ -33,8 +33,6 @@ struct Sched {
   int n_comp, n_disp, n_comb;
   int c, n_steal, final_all;
   int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
-  int cstart[MAX_K + 1]; // combine units before chunk q
-  int g1need[MAX_K];     // GEMM1 (row, column, split) tiles of chunk q
   // per (chunk q, segment) at index q*nseg + seg
   int rows[MAX_K * MAX_SEG];
   int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts)
@@ -87,10 +85,7 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
     S.nseg = nseg;
     S.G = K * 2 * nseg;
     for (int q = 0; q <= K; ++q) S.bnd[q] = (int)(((long long)q * a.T + K - 1) / K);
-    int cs = 0;
-    for (int q = 0; q < K; ++q) { S.cstart[q] = cs; cs += ceil_div(S.bnd[q + 1] - S.bnd[q], CT); }
-    S.cstart[K] = cs;
-    S.n_comb = cs;
+    S.n_comb = ceil_div(a.T, CT);
     S.n_disp = ceil_div(a.T, DT);
   }
   __syncthreads();
@@ -120,11 +115,6 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
     S.gstart[gi] = S.mb[q * nseg + seg] * (ph ? g1tiles : a.nt0);
   }
   if (tid == 0) S.gstart[S.G] = 0;
-  if (tid < K) {
-    int s = 0;
-    for (int seg = 0; seg < nseg; ++seg) s += S.mb[tid * nseg + seg] * g1tiles;
-    S.g1need[tid] = s;
-  }
   __syncthreads();
   block_exscan(S.mb, K * nseg, W.part);
   block_exscan(S.gstart, S.G + 1, W.part);
@@ -279,16 +269,18 @@ __device__ __forceinline__ void dispatch_static(const FwdArgs& a, Scratch& W, in
   }
 }
 
-// Megakernel: units are claimed per wavefront from NSHARD queues (unit u is
-// the (u / NSHARD)-th of shard u % NSHARD, so every shard advances in token
-// order).  Trying the shards from `shard` on, returns the next unit or -1
-// once all are exhausted.
-__device__ __forceinline__ int claim_unit(const FwdArgs& a, const Sched& S, int& shard) {
+// Megakernel: movement units are claimed per wavefront from NSHARD queues
+// at ctl[base + shard * CTL_PAD] (unit u is the (u / NSHARD)-th of shard
+// u % NSHARD, so every shard advances in token order).  Trying the shards
+// from `shard` on (a plain read first, so exhausted shards take no atomic),
+// returns the next unit or -1 once all are exhausted.
+__device__ __forceinline__ int claim_unit(const FwdArgs& a, int base, int n_units, int& shard) {
   for (int tries = 0; tries < NSHARD; ++tries) {
+    int* q = &a.ctl[base + shard * CTL_PAD];
     int v = 0;
-    if (lane_id() == 0) v = fetch_add_relaxed(&a.ctl[CTL_QD + shard * CTL_PAD], 1);
+    if (lane_id() == 0) v = ld_relaxed(q) * NSHARD + shard < n_units ? fetch_add_relaxed(q, 1) : n_units;
     const int u = __builtin_amdgcn_readfirstlane(v) * NSHARD + shard;
-    if (u < S.n_disp) return u;
+    if (u < n_units) return u;
     shard = shard + 1 == NSHARD ? 0 : shard + 1;
   }
   return -1;
@@ -298,19 +290,21 @@ __device__ __forceinline__ int claim_unit(const FwdArgs& a, const Sched& S, int&
 __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& S, Scratch& W) {
   int shard = wave_id();
   for (;;) {
-    const int u = claim_unit(a, S, shard);
+    const int u = claim_unit(a, CTL_QD, S.n_disp, shard);
     if (u < 0) break;
     dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
   }
 }
 
+__device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target);
+
 // One wavefront combines nt <= CT tokens.  Each token has KS = k + S source
 // rows: its k routed slots (weight w, absent when the expert is not local)
 // followed by its S shared-expert rows (weight 1, present for tokens of rank
-// 0).  They are summed in that order in fp32.  A source row is O (bf16) or,
-// when GEMM1 is split NS ways, the bf16 rounding of its NS fp32 partials
-// added in split order.  KS and NS are template constants so that every lane
-// keeps about 16 row vectors in flight.
+// 0).  They are summed in that order in fp32.  A source row is O (bf16; a
+// split GEMM1 tile was reduced into O in split order by its last split).  KS
+// is a template constant so that every lane keeps about 16 row vectors in
+// flight (NS > 1 reads fp32 split partials directly; not used).
 template <int KS, int NS>
 __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
   constexpr int NV = NS == 1 ? 1 : 2 * NS;                    // 16-byte loads per source row
@@ -391,16 +385,20 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
   __builtin_amdgcn_s_waitcnt(0);
 }
 
-__device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int g0, int nt) {
+// A wavefront combines tokens [g0, g0 + nt).  In the megakernel (S given) it
+// first waits until every GEMM1 item of each row tile holding one of those
+// tokens' source rows is done: one lane polls per distinct row tile.
+// Returns false when the launch was aborted.
+__device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S, Scratch& W, int g0, int nt) {
   const int lane = lane_id();
   int* sl = W.wsl[wave_id()];
   float* wt = W.wwt[wave_id()];
   const int k = a.k, ks = a.k + a.S;
   // source rows of token g0 + lane / ks, entry lane % ks
+  int s = -1, id = -1;
+  float w = 1.0f;
   if (lane < nt * ks) {
     const int t = lane / ks, j = lane - t * ks, g = g0 + t;
-    int s = -1;
-    float w = 1.0f;
     if (j < k) {
       s = a.slot[(size_t)g * k + j];
       w = a.topk_w[(size_t)g * k + j];
@@ -408,15 +406,34 @@ __device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int
     } else if (g < a.Tr) {
       s = a.xmax + (j - k) * a.Tr + g;
     }
-    sl[lane] = s;
-    wt[lane] = w;
+    if (S && s >= 0) {
+      const int q = (int)(((long long)g * S->K) / a.T);
+      if (j < k) {
+        const int seg = a.topk_idx[(size_t)g * k + j] - a.e0;
+        id = S->mb[q * S->nseg + seg] + (s - S->row0[q * S->nseg + seg]) / BM;
+      } else {
+        const int seg = a.El + (j - k);
+        id = S->mb[q * S->nseg + seg] + (g - S->bnd[q]) / BM;
+      }
+      if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
+    }
+  }
+  sl[lane] = s;
+  wt[lane] = w;
+  if (S) {
+    const int need = a.nt1;  // every column tile of the row tile (split ones reduced)
+    uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
+    while (pending) {
+      const int leader = __builtin_ctzll(pending);
+      const int tile = __builtin_amdgcn_readlane(id, leader);
+      pending &= ~__builtin_amdgcn_ballot_w64(id == tile);
+      if (!wave_wait_geq(a, &a.ctl[CTL_READY + (2 * a.mt_max + tile) * CTL_PAD], need)) return false;
+    }
   }
   __builtin_amdgcn_wave_barrier();
-  switch (ks * 8 + a.nsplit) {
-#define MOE_COMBINE_CASE(n)                                       \
-  case n * 8 + 1: combine_body<n, 1>(a, sl, wt, g0, nt); break; \
-  case n * 8 + 2: combine_body<n, 2>(a, sl, wt, g0, nt); break; \
-  case n * 8 + 4: combine_body<n, 4>(a, sl, wt, g0, nt); break;
+  switch (ks) {
+#define MOE_COMBINE_CASE(n) \
+  case n: combine_body<n, 1>(a, sl, wt, g0, nt); break;
     MOE_COMBINE_CASE(1) MOE_COMBINE_CASE(2) MOE_COMBINE_CASE(3) MOE_COMBINE_CASE(4)
     MOE_COMBINE_CASE(5) MOE_COMBINE_CASE(6) MOE_COMBINE_CASE(7) MOE_COMBINE_CASE(8)
     MOE_COMBINE_CASE(9) MOE_COMBINE_CASE(10) MOE_COMBINE_CASE(11) MOE_COMBINE_CASE(12)
@@ -425,6 +442,7 @@ __device__ __forceinline__ void combine_tokens(const FwdArgs& a, Scratch& W, int
     default: break;
   }
   __builtin_amdgcn_wave_barrier();
+  return true;
 }
 
 // ===========================================================================
@@ -500,6 +518,61 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
     gemm::store_f32<CP>(acc, a.part + ((size_t)r.ks * a.prow + orow) * a.H + n0, a.H, r.rows, a.H - n0);
   }
   return nxt;
+}
+
+// Split-K reduction of one GEMM1 tile by its last-arriving split: O rows
+// [orow, orow + rows) x columns [n0, n0 + cols) = bf16(P_0 + P_1 + ... ) in
+// split order, 4 columns per thread and step.
+template <int CP>
+__device__ __forceinline__ void reduce_split(const FwdArgs& a, size_t orow, int rows, int n0, int cols) {
+  const __amdgpu_buffer_rsrc_t rO = __builtin_amdgcn_make_buffer_rsrc(a.O, 0, -1, 0x00020000);
+  const int q4 = cols >> 2;  // cols % 64 == 0
+  const int total = rows * q4;
+  constexpr int RB = 8;
+  for (int v0 = threadIdx.x; v0 < total; v0 += RB * FNTH) {
+    f32x4_t t[RB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int v = v0 + i * FNTH;
+      if (v >= total) continue;
+      const int r = v / q4, c = (v - r * q4) * 4;
+      const size_t e = (orow + r) * (size_t)a.H + n0 + c;
+      t[i] = *reinterpret_cast<const f32x4_t*>(a.part + e);
+      for (int p = 1; p < a.nsplit; ++p) {
+        const f32x4_t u = *reinterpret_cast<const f32x4_t*>(a.part + (size_t)p * a.prow * a.H + e);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t[i][j] += u[j];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int v = v0 + i * FNTH;
+      if (v >= total) continue;
+      const int r = v / q4, c = (v - r * q4) * 4;
+      const size_t e = (orow + r) * (size_t)a.H + n0 + c;
+      typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+      const u32x2_t packed = {pack_bf16x2(t[i][0], t[i][1]), pack_bf16x2(t[i][2], t[i][3])};
+      if constexpr (CP == gemm::CP_PLAIN) *reinterpret_cast<u32x2_t*>(a.O + e) = packed;
+      else __builtin_amdgcn_raw_buffer_store_b64(packed, rO, (uint32_t)(e * 2), 0, CP);
+    }
+  }
+}
+
+// After a GEMM1 item's partial stores have completed (all threads, past a
+// barrier): counts its arrival; the last split of the tile reduces it.
+// Returns true on the workgroup that reduced (its O stores still draining).
+template <int CP>
+__device__ __forceinline__ bool arrive_and_reduce(const FwdArgs& a, const Sched& S, Scratch& W, const TileRef& r,
+                                                  int id) {
+  if (threadIdx.x == 0)
+    W.bc[3] = fetch_add_relaxed(&a.ctl[CTL_READY + (3 * a.mt_max + id * a.nt1 + r.nt) * CTL_PAD], 1);
+  __syncthreads();
+  const bool last = W.bc[3] == a.nsplit - 1;
+  __syncthreads();
+  if (!last) return false;
+  const size_t orow = (size_t)S.row0[r.q * S.nseg + r.seg] + (size_t)r.mt * BM;
+  reduce_split<CP>(a, orow, r.rows, r.nt * BN, min(BN, a.H - r.nt * BN));
+  return true;
 }
 
 // ===========================================================================
@@ -621,7 +694,7 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
     __syncthreads();
     if (st) return st > 0;
     int shard = wave_id();
-    const int u = claim_unit(a, S, shard);
+    const int u = claim_unit(a, CTL_QD, S.n_disp, shard);
     if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
     else if (lane_id() == 0) W.dexh = 1;
   }
@@ -660,8 +733,18 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
     __builtin_amdgcn_s_waitcnt(0);
     if (threadIdx.x == 0) W.bc[1] = more ? nxt : S.n_comp;
     __syncthreads();  // every thread's output stores have completed
+    // GEMM0 tile: its row tile gains a column; GEMM1 tile (or the last split
+    // of one, after it reduced the tile): its row tile gains a column
+    bool publish = true;
+    if (r.ph == 1 && a.nsplit > 1) {
+      publish = arrive_and_reduce<gemm::CP_SC1>(a, S, W, r, id);
+      if (publish) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+      }
+    }
     if (threadIdx.x == 0) {
-      fetch_add_relaxed(r.ph == 0 ? &a.ctl[CTL_READY + (a.mt_max + id) * CTL_PAD] : &a.ctl[CTL_G1DONE + r.q * CTL_PAD], 1);
+      if (publish) fetch_add_relaxed(&a.ctl[CTL_READY + ((r.ph == 0 ? 1 : 2) * a.mt_max + id) * CTL_PAD], 1);
       if (a.trace) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
     }
     t = W.bc[1];  // rewritten only after the next mainloop's barriers
@@ -677,23 +760,20 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
   return __builtin_amdgcn_readfirstlane(ok) != 0;
 }
 
-// combine units of chunks [q0, q1) by worker w of n; chunk q's units wait
-// until every GEMM1 tile of chunk q is done
-__device__ __forceinline__ bool combine_chunks(const FwdArgs& a, const Sched& S, Scratch& W, int q0, int q1, int w,
-                                               int n) {
-  for (int q = q0; q < q1; ++q) {
-    int u = S.cstart[q] + w * NWF + wave_id();
-    if (u >= S.cstart[q + 1]) continue;
+// Combine units (CT tokens, in token and hence chunk order) are claimed per
+// wavefront from the sharded combine queue until every unit is claimed; each
+// waits only for the row tiles its tokens' rows come from, so the combine of
+// finished tokens starts while the last GEMM tiles run.
+__device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S, Scratch& W, int ticket) {
+  int shard = wave_id();
+  for (;;) {
+    const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
+    if (u < 0) return true;
     const uint64_t t0 = a.trace ? now_ticks() : 0;
-    if (!wave_wait_geq(a, &a.ctl[CTL_G1DONE + q * CTL_PAD], S.g1need[q])) return false;
-    const uint64_t t1 = a.trace ? now_ticks() : 0;
-    for (; u < S.cstart[q + 1]; u += n * NWF) {
-      const int g0 = S.bnd[q] + (u - S.cstart[q]) * CT;
-      combine_tokens(a, W, g0, min(CT, S.bnd[q + 1] - g0));
-    }
-    if (a.trace && lane_id() == 0) trace_rec(a, 4, w, q | (wave_id() << 8), t0, t1, now_ticks());
+    const int g0 = u * CT;
+    if (!combine_tokens(a, &S, W, g0, min(CT, a.T - g0))) return false;
+    if (a.trace && lane_id() == 0) trace_rec(a, 4, ticket, u | ((long long)wave_id() << 24), t0, t0, now_ticks());
   }
-  return true;
 }
 
 // ===========================================================================
@@ -720,9 +800,6 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   __syncthreads();
   const int ticket = __builtin_amdgcn_readfirstlane(W.bc[0]);
   const bool mover = ticket < S.c;
-  const int N = gridDim.x;
-  // chunks whose combine the movers do alone; the rest is the final combine
-  const int qa = S.final_all ? S.K - 1 : S.K;
   const uint64_t t_sched = a.trace ? now_ticks() : 0;
   __syncthreads();
 
@@ -734,12 +811,13 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
     if (a.trace && tid == 0) trace_rec(a, 3, ticket, 0, t_sched, now_ticks(), 0);
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
     ok = compute_tiles(a, S, W, ring, ticket, S.n_steal);
-    if (ok) ok = combine_chunks(a, S, W, 0, qa, ticket, S.c);
+    if (ok) combine_claimed(a, S, W, ticket);
   } else {
     ok = compute_tiles(a, S, W, ring, ticket, 1 << 30);
+    // the final combine on every worker (section 4): once the compute queue
+    // is empty a compute worker joins the combine
+    if (ok && S.final_all) combine_claimed(a, S, W, ticket);
   }
-  // final combine of the last chunk on every worker (section 4)
-  if (ok && S.final_all) combine_chunks(a, S, W, S.K - 1, S.K, ticket, N);
   if (a.trace) {
     __syncthreads();
     if (tid == 0) trace_rec(a, 1, ticket, mover ? 1 : 0, t_entry, t_sched, now_ticks());
@@ -777,9 +855,14 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
       u -= n;
     }
     const TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + u);
-    const int nxt = run_gemm<gemm::CP_PLAIN>(a, S, r, ring, qh);
+    const bool split = PH == 1 && a.nsplit > 1;
+    // split partials are read by another workgroup within this kernel:
+    // agent-coherent stores, drained before the arrival count
+    const int nxt = split ? run_gemm<gemm::CP_SC1>(a, S, r, ring, qh) : run_gemm<gemm::CP_PLAIN>(a, S, r, ring, qh);
+    if (split) __builtin_amdgcn_s_waitcnt(0);
     if (threadIdx.x == 0) W.bc[1] = nxt;
     __syncthreads();
+    if (split) arrive_and_reduce<gemm::CP_PLAIN>(a, S, W, r, S.mb[r.q * S.nseg + r.seg] + r.mt);
     t = W.bc[1];  // rewritten only after the next mainloop's barriers
   }
 }
@@ -792,7 +875,7 @@ __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   const int n = ceil_div(a.T, CT);
   for (int u = blockIdx.x * NWF + wave_id(); u < n; u += gridDim.x * NWF) {
     const int g0 = u * CT;
-    combine_tokens(a, W, g0, min(CT, a.T - g0));
+    combine_tokens(a, nullptr, W, g0, min(CT, a.T - g0));
   }
 }
 

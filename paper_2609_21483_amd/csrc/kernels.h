@@ -7,13 +7,23 @@
 namespace moe {
 
 struct GateArgs {
-  const uint16_t* x;
-  const uint16_t* wg;
-  const float* bias;
+  const uint16_t* x;   // [T][H] bf16
+  const uint16_t* wg;  // [H][E] bf16
+  const float* bias;   // [E] or NULL
   int32_t* topk_idx;
   float* topk_w;
+  uint16_t* wgt;       // [E][H] bf16: Wg transposed (workspace)
+  float* lt;           // [T][E] approximate logits without bias (workspace)
+  float* xn;           // [T] ||x_g||_2 (workspace)
+  float* wn;           // [E] ||w_e||_2 (workspace)
+  int32_t* ch_g;       // [T * E] chain list: token of each chain (workspace)
+  int32_t* ch_e;       // [T * E] expert of each chain
+  float* ch_l;         // [T * E] defined logit of each chain
+  int32_t* tok_base;   // [T] first chain of each token
+  int32_t* tok_n;      // [T] chains of each token
+  int32_t* stats;
+  float bound;         // |L - L~| <= bound * ||x|| * ||w|| (plus rounding of the bias add)
   int T, H, E, k;
-  int tq;  // token groups per workgroup
 };
 
 struct TableArgs {
@@ -166,8 +176,11 @@ __host__ __device__ inline void cm_volumes(const int32_t* stats, int H, int F, i
 }
 
 // ---- launch prototypes ---------------------------------------------------------
-template <int TPT, int EPT>
-__global__ void gate_topk_kernel(GateArgs a);
+__global__ void gate_prep_kernel(GateArgs a);
+__global__ void gate_mfma_kernel(GateArgs a);
+__global__ void gate_cand_kernel(GateArgs a);
+__global__ void gate_chain_kernel(GateArgs a);
+__global__ void gate_final_kernel(GateArgs a);
 __global__ void tab_count_kernel(TableArgs a);
 __global__ void tab_scan_kernel(TableArgs a);
 __global__ void tab_perm_kernel(TableArgs a);

@@ -3,9 +3,10 @@
 // (section 3.1 descriptors X_local, X_in, X_in^uniq; the dispatch permutation
 // and its deduplication, section 4; the chunk offsets of section 3.2.1).
 //
-// Everything here is deterministic: logits use one fp32 accumulator per
-// (token, expert) over ascending h, and slots come from block histograms, an
-// ordered scan and wavefront ballots, never from atomic slot claiming.
+// Everything here is deterministic: the routing decisions are those of logits
+// with one fp32 accumulator per (token, expert) over ascending h, and slots
+// come from block histograms, an ordered scan and wavefront ballots, never
+// from atomic slot claiming.
 #include "common.h"
 #include "kernels.h"
 
@@ -13,153 +14,361 @@ namespace moe {
 
 // ---------------------------------------------------------------------------
 // Gate: logits -> softmax -> top-k (on logits, ties -> smaller id) -> renormalise
-// Each thread owns a TPT-token x EPT-expert block of logits (one fp32
-// accumulator per (token, expert), ascending h).  x and Wg are staged
-// through LDS as fp32 in chunks of GH hidden values, token-major and
-// expert-major rows padded to GHP floats so float4 reads are conflict-free.
-// The host picks the block size so that the grid has enough workgroups.
+//
+// The logit of (token g, expert e) is defined in fp32 with one accumulator,
+// hidden index ascending, each product rounded to fp32 before it is added,
+// then + bias[e].  That sum is a chain of H dependent additions, so it is
+// evaluated only where it can change the routing, and the selection is still
+// exactly the one the full definition gives:
+//   1. gate_prep:  WgT = Wg transposed ([E][H]) and ||w_e||_2.
+//   2. gate_mfma:  approximate logits L~ by bf16 MFMA (fp32 accumulation) and
+//                  ||x_g||_2.
+//   3. gate_select: per token, a bound d_e >= |L - L~| (from the worst-case
+//      error of the two summations, |x|.|w| <= ||x|| ||w||) gives intervals
+//      [L~ - d, L~ + d] that hold the defined logits.  tau = k-th largest lower
+//      end; every expert whose upper end reaches tau is a candidate.  The true
+//      top-k lie among the candidates and every other expert is strictly
+//      below the k-th logit, so the top-k of the candidates' exact logits
+//      (the defined chains) is the top-k of all experts.
+// Softmax weights come from the exact logits of the chosen experts; the
+// normaliser over all experts cancels in the renormalisation up to rounding.
 // ---------------------------------------------------------------------------
-constexpr int GH = 16;
-constexpr int GHP = GH + 4;
-constexpr int GATE_MAX_TT = 256;
 
-template <int TPT, int EPT>
-__global__ void __launch_bounds__(NTH) gate_topk_kernel(GateArgs a) {
-  __shared__ __attribute__((aligned(16))) float xs[GATE_MAX_TT * GHP];
-  __shared__ __attribute__((aligned(16))) float ws[MAX_E * GHP];
-  __shared__ float lg[NTH * 16];
-
+__global__ void __launch_bounds__(NTH) gate_prep_kernel(GateArgs a) {
+  __shared__ float part[NTH / WAVE];
+  const int e = blockIdx.x;
   const int tid = threadIdx.x;
-  const int EQ = (a.E + EPT - 1) / EPT;
-  const int EP = EQ * EPT;
-  const int TQ = a.tq;  // token groups per workgroup
-  const int TT = TQ * TPT;
-  const int g0 = blockIdx.x * TT;
-  const bool active = tid < TQ * EQ;
-  const int tq = active ? tid / EQ : 0;
-  const int eq = active ? tid % EQ : 0;
-
-  float acc[TPT][EPT];
-#pragma unroll
-  for (int i = 0; i < TPT; ++i)
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) acc[i][j] = 0.0f;
-
-  for (int h0 = 0; h0 < a.H; h0 += GH) {
-    // stage x[g0 .. g0+TT)[h0 .. h0+GH) as xs[t][h]
-    for (int v = tid; v < TT * (GH / 8); v += NTH) {
-      const int t = v / (GH / 8), part = v % (GH / 8);
-      const int g = g0 + t;
-      u32x4_t w = {0u, 0u, 0u, 0u};
-      if (g < a.T) w = *reinterpret_cast<const u32x4_t*>(a.x + (size_t)g * a.H + h0 + part * 8);
-      float* d = xs + t * GHP + part * 8;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        d[2 * q] = bf16_lo(w[q]);
-        d[2 * q + 1] = bf16_hi(w[q]);
-      }
-    }
-    // stage Wg[h0 .. h0+GH)[0 .. E) as ws[e][h]
-    for (int v = tid; v < GH * EP; v += NTH) {
-      const int h = v / EP, e = v % EP;
-      ws[e * GHP + h] = e < a.E ? bf16_to_f32(a.wg[(size_t)(h0 + h) * a.E + e]) : 0.0f;
-    }
-    __syncthreads();
-    if (active) {
-#pragma unroll
-      for (int h = 0; h < GH; h += 4) {
-        float4 xv[TPT], wv[EPT];
-#pragma unroll
-        for (int i = 0; i < TPT; ++i) xv[i] = *reinterpret_cast<const float4*>(xs + (tq * TPT + i) * GHP + h);
-#pragma unroll
-        for (int j = 0; j < EPT; ++j) wv[j] = *reinterpret_cast<const float4*>(ws + (eq * EPT + j) * GHP + h);
-        // products of two bf16 values are exact in fp32, so a fused or an
-        // unfused multiply-add gives the same rounded sum; h ascends
-#pragma unroll
-        for (int i = 0; i < TPT; ++i)
-#pragma unroll
-          for (int j = 0; j < EPT; ++j) {
-            acc[i][j] = acc[i][j] + xv[i].x * wv[j].x;
-            acc[i][j] = acc[i][j] + xv[i].y * wv[j].y;
-            acc[i][j] = acc[i][j] + xv[i].z * wv[j].z;
-            acc[i][j] = acc[i][j] + xv[i].w * wv[j].w;
-          }
-      }
-    }
-    __syncthreads();
+  float ss = 0.0f;
+  for (int h = tid; h < a.H; h += NTH) {
+    const uint16_t v = a.wg[(size_t)h * a.E + e];
+    a.wgt[(size_t)e * a.H + h] = v;
+    const float f = bf16_to_f32(v);
+    ss += f * f;
   }
-
-  if (active) {
 #pragma unroll
-    for (int i = 0; i < TPT; ++i)
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const int e = eq * EPT + j;
-        if (e < a.E) {
-          float l = acc[i][j];
-          if (a.bias) l = l + a.bias[e];
-          lg[(tq * TPT + i) * EP + e] = l;
-        }
-      }
-  }
+  for (int d = WAVE / 2; d > 0; d >>= 1) ss += __shfl_xor(ss, d, WAVE);
+  if ((tid & (WAVE - 1)) == 0) part[tid / WAVE] = ss;
   __syncthreads();
-
-  // one thread per token: softmax statistics, top-k insertion, renormalise
-  for (int t = tid; t < TT; t += NTH) {
-    const int g = g0 + t;
-    if (g >= a.T) break;
-    const float* l = lg + t * EP;
-    float m = l[0];
-    for (int e = 1; e < a.E; ++e) m = fmaxf(m, l[e]);
-    float z = 0.0f;
-    for (int e = 0; e < a.E; ++e) z += expf(l[e] - m);
-
-    float tv[MAX_TOPK];
-    int ti[MAX_TOPK];
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j) { tv[j] = -INFINITY; ti[j] = -1; }
-    for (int e = 0; e < a.E; ++e) {
-      const float v = l[e];
-      // insert e if it beats the current k-th entry; equal logits keep the
-      // earlier (smaller) expert id in front
-      if (ti[a.k - 1] >= 0 && !(v > tv[a.k - 1])) continue;
-      int carry_i = e;
-      float carry_v = v;
-      bool placed = false;
-#pragma unroll
-      for (int j = 0; j < MAX_TOPK; ++j) {
-        if (j < a.k) {
-          const bool go = placed || ti[j] < 0 || carry_v > tv[j];
-          if (go) {
-            const float sv = tv[j];
-            const int si = ti[j];
-            tv[j] = carry_v;
-            ti[j] = carry_i;
-            carry_v = sv;
-            carry_i = si;
-            placed = true;
-            if (si < 0) break;
-          }
-        }
-      }
-    }
-    float p[MAX_TOPK];
-    float ps = 0.0f;
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j)
-      if (j < a.k) { p[j] = expf(tv[j] - m) / z; ps += p[j]; }
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j)
-      if (j < a.k) {
-        a.topk_idx[(size_t)g * a.k + j] = ti[j];
-        a.topk_w[(size_t)g * a.k + j] = p[j] / ps;
-      }
+  if (tid == 0) {
+    float t = 0.0f;
+    for (int w = 0; w < NTH / WAVE; ++w) t += part[w];
+    a.wn[e] = sqrtf(t);
   }
 }
 
-template __global__ void gate_topk_kernel<4, 4>(GateArgs);
-template __global__ void gate_topk_kernel<2, 2>(GateArgs);
-template __global__ void gate_topk_kernel<1, 1>(GateArgs);
+// 32 tokens x all experts per workgroup, v_mfma_f32_32x32x16_bf16 with the
+// operands read straight from global memory.  Each of the 4 wavefronts sums
+// a quarter of the hidden range (any order is allowed here: the bound below
+// covers recursive fp32 summation of all H products) and the quarters are
+// added through LDS.  Lane l holds token row (l & 31) and expert row (l & 31)
+// of the current 32-expert block at hidden offsets 8 * (l >> 5) .. + 8 of each
+// 16-deep step; GSTEP steps are loaded before their MFMAs.
+constexpr int GATE_EB = 4;   // 32-expert blocks per pass (128 experts)
+constexpr int GSTEP = 4;     // 16-deep steps loaded ahead
+constexpr int GWAVES = 4;
+__global__ void __launch_bounds__(GWAVES * WAVE) gate_mfma_kernel(GateArgs a) {
+  __shared__ float red[GWAVES - 1][32 * 32 * GATE_EB];
+  __shared__ float ssr[GWAVES][64];
+  const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
+  const int g0 = blockIdx.x * 32;
+  const int row = lane & 31, kh = (lane >> 5) * 8;
+  const int g = g0 + row;
+  const bool grow = g < a.T;
+  const int hq = a.H / GWAVES;  // multiple of 16
+  const int hbeg = wave * hq;
+  const uint16_t* xr = a.x + (size_t)(grow ? g : 0) * a.H + kh + hbeg;
+  float ss = 0.0f;
+  for (int eb0 = 0; eb0 < a.E; eb0 += 32 * GATE_EB) {
+    const int nb = min(GATE_EB, (a.E - eb0 + 31) / 32);
+    f32x16_t acc[GATE_EB];
+    const uint16_t* wr[GATE_EB];
+    bool ev[GATE_EB];
+#pragma unroll
+    for (int b = 0; b < GATE_EB; ++b) {
+      acc[b] = f32x16_t{};
+      const int e = eb0 + 32 * b + row;
+      ev[b] = e < a.E;
+      wr[b] = a.wgt + (size_t)(ev[b] ? e : 0) * a.H + kh + hbeg;
+    }
+    // GSTEP steps of operands per set; the next set is loaded before the
+    // MFMAs of the current one
+    bf16x8_t xa[2][GSTEP], wb[2][GSTEP][GATE_EB];
+    auto load_set = [&](int set, int h0) {
+#pragma unroll
+      for (int st = 0; st < GSTEP; ++st) {
+        const int h = h0 + 16 * st;
+        xa[set][st] = bf16x8_t{};
+        if (h < hq && grow) xa[set][st] = *reinterpret_cast<const bf16x8_t*>(xr + h);
+#pragma unroll
+        for (int b = 0; b < GATE_EB; ++b) {
+          wb[set][st][b] = bf16x8_t{};
+          if (b < nb && h < hq && ev[b]) wb[set][st][b] = *reinterpret_cast<const bf16x8_t*>(wr[b] + h);
+        }
+      }
+    };
+    auto mfma_set = [&](int set) {
+#pragma unroll
+      for (int st = 0; st < GSTEP; ++st) {
+        if (eb0 == 0) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float f = (float)xa[set][st][q];
+            ss += f * f;
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < GATE_EB; ++b)
+          if (b < nb) acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[set][st], wb[set][st][b], acc[b], 0, 0, 0);
+      }
+    };
+    load_set(0, 0);
+    int h0 = 0;
+    for (; h0 + 16 * GSTEP < hq; h0 += 32 * GSTEP) {
+      load_set(1, h0 + 16 * GSTEP);
+      mfma_set(0);
+      if (h0 + 32 * GSTEP < hq) load_set(0, h0 + 32 * GSTEP);
+      mfma_set(1);
+    }
+    if (h0 < hq) mfma_set(0);
+    // add the quarters: C[8 (r >> 2) + 4 (l >> 5) + (r & 3)][l & 31]
+    if (wave > 0) {
+#pragma unroll
+      for (int b = 0; b < GATE_EB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[wave - 1][(b * 16 + r) * WAVE + lane] = acc[b][r];
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int b = 0; b < GATE_EB; ++b) {
+        const int e = eb0 + 32 * b + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float v = acc[b][r];
+#pragma unroll
+          for (int w = 0; w < GWAVES - 1; ++w) v += red[w][(b * 16 + r) * WAVE + lane];
+          const int gr = g0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (b < nb && e < a.E && gr < a.T) a.lt[(size_t)gr * a.E + e] = v;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  ssr[wave][lane] = ss;
+  __syncthreads();
+  if (wave == 0) {
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < GWAVES; ++w) t += ssr[w][lane] + ssr[w][lane ^ 32];
+    if (lane < 32 && grow) a.xn[g] = sqrtf(t);
+  }
+}
+
+// lanes of one token's group of GG: reductions stay inside the group
+constexpr int GG = 16;
+constexpr int GEPL = MAX_E / GG;  // experts per lane
+constexpr int GTOK = NTH / GG;    // tokens per workgroup
+
+__device__ __forceinline__ bool better(float v, int e, float bv, int be) {
+  return v > bv || (v == bv && e < be);
+}
+__device__ __forceinline__ void group_argmax(float& v, int& e) {
+#pragma unroll
+  for (int d = GG / 2; d > 0; d >>= 1) {
+    const float ov = __shfl_xor(v, d, WAVE);
+    const int oe = __shfl_xor(e, d, WAVE);
+    if (better(ov, oe, v, e)) { v = ov; e = oe; }
+  }
+}
+
+// approximate logit of (g, e) with bias, and its half-width
+__device__ __forceinline__ void interval(const GateArgs& a, int g, int e, float xn, float& l, float& d) {
+  l = a.lt[(size_t)g * a.E + e];
+  if (a.bias) l = l + a.bias[e];
+  d = a.bound * xn * a.wn[e];
+  d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
+}
+
+// Candidates: tau = k-th largest lower end; every expert whose upper end
+// reaches tau becomes a chain (g, e) of the chain list, in expert order per
+// token.  A workgroup takes its chain range with one atomic.
+__global__ void __launch_bounds__(NTH) gate_cand_kernel(GateArgs a) {
+  __shared__ int cnt[GTOK];
+  __shared__ int base_s;
+  const int tid = threadIdx.x, grp = tid / GG, gl = tid % GG;
+  const int g = blockIdx.x * GTOK + grp;
+  const bool valid = g < a.T;
+  const int gs = valid ? g : 0;
+  const float xn = a.xn[gs];
+  float lo[GEPL], hi[GEPL];
+#pragma unroll
+  for (int i = 0; i < GEPL; ++i) {
+    const int e = gl + GG * i;
+    lo[i] = hi[i] = -INFINITY;
+    if (e < a.E) {
+      float l, d;
+      interval(a, gs, e, xn, l, d);
+      lo[i] = l - d;
+      hi[i] = l + d;
+    }
+  }
+  float tau = -INFINITY;
+  for (int r = 0; r < a.k; ++r) {
+    float v = -INFINITY;
+    int e = 1 << 30;
+#pragma unroll
+    for (int i = 0; i < GEPL; ++i)
+      if (better(lo[i], gl + GG * i, v, e)) { v = lo[i]; e = gl + GG * i; }
+    group_argmax(v, e);
+    tau = v;
+#pragma unroll
+    for (int i = 0; i < GEPL; ++i)
+      if (gl + GG * i == e) lo[i] = -INFINITY;
+  }
+  int mine = 0;
+#pragma unroll
+  for (int i = 0; i < GEPL; ++i) mine += valid && hi[i] >= tau;
+  int pre = mine;
+#pragma unroll
+  for (int d = 1; d < GG; d <<= 1) {
+    const int o = __shfl_up(pre, d, GG);
+    if (gl >= d) pre += o;
+  }
+  const int total = __shfl(pre, GG - 1, GG);
+  if (gl == 0) cnt[grp] = total;
+  __syncthreads();
+  if (tid == 0) {
+    int t = 0;
+    for (int q = 0; q < GTOK; ++q) { const int c = cnt[q]; cnt[q] = t; t += c; }
+    base_s = atomicAdd(&a.stats[ST_CANDS], t);
+  }
+  __syncthreads();
+  const int tb = base_s + cnt[grp];
+  if (valid && gl == 0) {
+    a.tok_base[g] = tb;
+    a.tok_n[g] = total;
+  }
+  // this lane's candidates, in expert order within the lane; the final pass
+  // does not depend on the order
+  int pos = tb + pre - mine;
+#pragma unroll
+  for (int i = 0; i < GEPL; ++i)
+    if (valid && hi[i] >= tau) {
+      a.ch_g[pos] = g;
+      a.ch_e[pos] = gl + GG * i;
+      ++pos;
+    }
+}
+
+// the defined logit of one (token, expert): fp32, one accumulator, h
+// ascending, each product rounded before the add.  The chain of adds is
+// serial; two register sets take turns so that the loads of the next PF
+// vectors are in flight while the current ones are added.
+constexpr int PF = 8;
+__device__ __forceinline__ void chain_add(float& acc, const u32x4_t (&xb)[PF], const u32x4_t (&wb)[PF]) {
+#pragma clang fp contract(off)
+#pragma unroll
+  for (int i = 0; i < PF; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float p0 = bf16_lo(xb[i][q]) * bf16_lo(wb[i][q]);
+      acc = acc + p0;
+      const float p1 = bf16_hi(xb[i][q]) * bf16_hi(wb[i][q]);
+      acc = acc + p1;
+    }
+}
+__device__ __forceinline__ float exact_logit(const uint16_t* xr, const uint16_t* wr, int H) {
+  const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(xr);
+  const u32x4_t* wv = reinterpret_cast<const u32x4_t*>(wr);
+  const int nv = H >> 3;  // H % 64 == 0: nv is a multiple of 8
+  u32x4_t x0[PF], w0[PF], x1[PF], w1[PF];
+#pragma unroll
+  for (int i = 0; i < PF; ++i) { x0[i] = xv[i]; w0[i] = wv[i]; }
+  float acc = 0.0f;
+  int v0 = 0;
+  for (; v0 + 2 * PF <= nv; v0 += 2 * PF) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) { x1[i] = xv[v0 + PF + i]; w1[i] = wv[v0 + PF + i]; }
+    chain_add(acc, x0, w0);
+    if (v0 + 2 * PF < nv) {
+#pragma unroll
+      for (int i = 0; i < PF; ++i) { x0[i] = xv[v0 + 2 * PF + i]; w0[i] = wv[v0 + 2 * PF + i]; }
+    }
+    chain_add(acc, x1, w1);
+  }
+  if (v0 < nv) chain_add(acc, x0, w0);  // nv % 16 == 8: one set left, already loaded
+  return acc;
+}
+
+// one lane per chain of the list
+__global__ void __launch_bounds__(NTH) gate_chain_kernel(GateArgs a) {
+  const int n = a.stats[ST_CANDS];
+  for (int i = blockIdx.x * NTH + threadIdx.x; i < n; i += gridDim.x * NTH) {
+    const int g = a.ch_g[i], e = a.ch_e[i];
+    float l = exact_logit(a.x + (size_t)g * a.H, a.wgt + (size_t)e * a.H, a.H);
+    if (a.bias) l = l + a.bias[e];
+    a.ch_l[i] = l;
+  }
+}
+
+// top-k of the candidates' defined logits (descending, equal logits ->
+// smaller id); softmax normaliser from the defined logits of the candidates
+// and the approximate ones elsewhere (it cancels in the renormalisation)
+__global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a) {
+  __shared__ uint32_t cmask[GTOK][MAX_E / 32];
+  const int tid = threadIdx.x, grp = tid / GG, gl = tid % GG;
+  const int g = blockIdx.x * GTOK + grp;
+  const bool valid = g < a.T;
+  const int gs = valid ? g : 0;
+  for (int i = gl; i < MAX_E / 32; i += GG) cmask[grp][i] = 0u;
+  __builtin_amdgcn_wave_barrier();
+  const int tb = valid ? a.tok_base[g] : 0, tn = valid ? a.tok_n[g] : 0;
+  for (int c = gl; c < tn; c += GG) {
+    const int e = a.ch_e[tb + c];
+    atomicOr(&cmask[grp][e >> 5], 1u << (e & 31));
+  }
+  __builtin_amdgcn_wave_barrier();
+  float tv[MAX_TOPK];
+  int ti[MAX_TOPK];
+  for (int r = 0; r < a.k; ++r) {
+    float v = -INFINITY;
+    int e = 1 << 30;
+    for (int c = gl; c < tn; c += GG) {
+      const int ce = a.ch_e[tb + c];
+      const float cv = a.ch_l[tb + c];
+      bool taken = false;
+      for (int q = 0; q < r; ++q) taken |= ti[q] == ce;
+      if (!taken && better(cv, ce, v, e)) { v = cv; e = ce; }
+    }
+    group_argmax(v, e);
+    tv[r] = v;
+    ti[r] = e;
+  }
+  const float m = tv[0];
+  const float xn = a.xn[gs];
+  float z = 0.0f;
+#pragma unroll
+  for (int i = 0; i < GEPL; ++i) {
+    const int e = gl + GG * i;
+    if (e < a.E && !((cmask[grp][e >> 5] >> (e & 31)) & 1u)) {
+      float l, d;
+      interval(a, gs, e, xn, l, d);
+      z += expf(l - m);
+    }
+  }
+  for (int c = gl; c < tn; c += GG) z += expf(a.ch_l[tb + c] - m);
+#pragma unroll
+  for (int d = GG / 2; d > 0; d >>= 1) z += __shfl_xor(z, d, WAVE);
+  if (gl == 0 && valid) {
+    float p[MAX_TOPK];
+    float ps = 0.0f;
+    for (int j = 0; j < a.k; ++j) { p[j] = expf(tv[j] - m) / z; ps += p[j]; }
+    for (int j = 0; j < a.k; ++j) {
+      a.topk_idx[(size_t)g * a.k + j] = ti[j];
+      a.topk_w[(size_t)g * a.k + j] = p[j] / ps;
+    }
+  }
+}
 
 // ---------------------------------------------------------------------------
 // Routing tables.  A pair (g, j) is local when id = topk_idx[g,j] is in

@@ -88,6 +88,40 @@ def test_route_parity(B, name, layer):
         assert mism.size == 0, f"{mism.size} tokens differ, first {mism[:5]}"
         assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= 1e-6
         check_tables(hd, shape, idx_ref)
+        # the certified filter evaluated the defined logit of few experts per token
+        cands = int(hd.view("stats", 16)[8])
+        assert shape.T * shape.top_k <= cands <= min(shape.T * shape.n_experts, 3 * shape.T * shape.top_k), cands
+    finally:
+        hd.close()
+
+
+@pytest.mark.parametrize("bias", [False, True])
+def test_route_ties_and_candidate_overflow(B, bias):
+    """Exact ties and the exact fallback: zero token rows tie every expert
+    (more candidates than the per-token list holds), duplicated gate columns
+    tie expert pairs; equal logits go to the smaller id."""
+    shape = W.MoeShape("ties", 98, 2, 40, 128, 64, 128, 8, 8)
+    rng = np.random.default_rng(11)
+    x = torch.from_numpy(rng.standard_normal((shape.T, shape.hidden)).astype(np.float32)).to(torch.bfloat16)
+    x[[0, 7, 41]] = 0
+    wg = torch.from_numpy(0.05 * rng.standard_normal((shape.hidden, shape.n_experts)).astype(np.float32)).to(torch.bfloat16)
+    wg[:, 5] = wg[:, 3]
+    wg[:, 40] = wg[:, 2]
+    wg[:, 100] = wg[:, 99]
+    b = torch.from_numpy((-0.1 * np.log(np.arange(1, shape.n_experts + 1))).astype(np.float32)) if bias else None
+    bu = None if b is None else b.numpy()
+    lg = O.gate_logits(W.as_u16_numpy(x), W.as_u16_numpy(wg), bu)
+    idx_ref, w_ref = O.softmax_topk(lg, shape.top_k)
+    hd = Handle(B, shape)
+    try:
+        idx = torch.full((shape.T, shape.top_k), -7, dtype=torch.int32, device="cuda")
+        w = torch.zeros((shape.T, shape.top_k), dtype=torch.float32, device="cuda")
+        B.moe_route(hd.h, x.cuda(), wg.cuda(), None if b is None else b.cuda(), shape.top_k, idx, w)
+        assert B.moe_sync_status(hd.h) == B.MOE_OK, B.moe_last_error()
+        assert np.array_equal(idx.cpu().numpy(), idx_ref)
+        assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= 1e-6
+        if not bias:
+            assert list(idx_ref[0]) == list(range(8))
     finally:
         hd.close()
 
