@@ -87,7 +87,10 @@ typedef struct {
  * ratio at k_chunks[j] chunks; alpha is the tile-level overlap ratio (Eq 6).
  * literal_volumes = 1 uses the printed remote-only volumes of Eq 2-3;
  * 0 (default) counts every moved row, since on one GPU rank 0's rows also go
- * through the movement workers. */
+ * through the movement workers.  bw_all_bytes_per_s is the rate of all N
+ * workers moving together: the last chunk's combine runs on every worker
+ * (section 4), so the exposed tail of Eq 6/10 moves at that rate; 0 takes the
+ * printed BW(c) instead. */
 typedef struct {
   int32_t n_c;
   int32_t c[MOE_CALIB_MAX_C];            /* ascending, 1 <= c < N */
@@ -99,6 +102,7 @@ typedef struct {
   double alpha;                          /* in [0, 1] */
   int32_t literal_volumes;
   int32_t static_c;                      /* split used by MOE_MODE_STATIC */
+  double bw_all_bytes_per_s;             /* >= 0; 0: tail at BW(c) */
 } moe_calib;
 
 /* Execution plan (section 3.3): the split, the chunk count and the steal count. */

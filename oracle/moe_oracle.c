@@ -205,7 +205,8 @@ double orc_t_total(const orc_plan_in* in, int ci, int ki) {
   double K = (double)in->K[ki];
   double t_comp = in->w_comp / (fl * eff);                              /* Eq 9 */
   double t_comm = (in->w_dispatch + in->w_combine) / bw;                /* Eq 5 */
-  double t_tail = ((1.0 - in->alpha) * in->w_combine) / (bw * K);       /* Eq 10 */
+  double bw_tail = in->bw_all > 0.0 ? in->bw_all : bw;
+  double t_tail = ((1.0 - in->alpha) * in->w_combine) / (bw_tail * K);  /* Eq 10 */
   double a = t_comp + t_tail;
   return a > t_comm ? a : t_comm;                                       /* Eq 15 */
 }

@@ -116,6 +116,10 @@ typedef struct {
   double w_dispatch;     /* Eq 2, bytes */
   double w_combine;      /* Eq 3, bytes */
   const int64_t* n_tiles; /* GEMM tiles for each K[j] (W_tile = w_comp / n_tiles) */
+  /* rate of all N workers moving together (bytes/s); the last chunk's combine
+   * runs on every worker (section 4), so when bw_all > 0 the exposed tail of
+   * Eq 6/10 moves at bw_all, else at BW(c) as printed */
+  double bw_all;
 } orc_plan_in;
 
 typedef struct {

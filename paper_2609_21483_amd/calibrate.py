@@ -10,6 +10,8 @@ For a workload share (layer 0, its own routing):
                   uses, Eq 2-3 as counted on one GPU);
   TFLOPS(N - c) = W_comp / time of GEMM0 + GEMM1 on N - c workgroups (Eq 1);
   eff_chunk(K)  = GEMM time at K = 1 / GEMM time with the tiling of K chunks;
+  BW(N)         = the same movement on all N workgroups (the final combine
+                  runs on every worker, section 4);
   alpha         = least-squares fit of Eq 15 to the megakernel's time over a
                   (c, K) grid of forced plans.
 The table is written to calib/<workload>.json and loaded by bench.py.
@@ -44,7 +46,8 @@ def load_calib(workload: str, N: int):
     d = json.load(open(p))
     if int(d.get("N", -1)) != N:
         return None
-    return B.make_calib(d["c"], d["bw"], d["flops"], d["K"], d["eff"], d["alpha"], d["static_c"], d.get("literal", 0))
+    return B.make_calib(d["c"], d["bw"], d["flops"], d["K"], d["eff"], d["alpha"], d["static_c"], d.get("literal", 0),
+                        d.get("bw_all", 0.0))
 
 
 def _time(fn, reps: int) -> float:
@@ -94,6 +97,9 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
             bw.append(w_move / t_m)
             fl.append(w_comp / t_c)
             log(f"[calib] c={c:3d}: BW {bw[-1] / 1e9:8.1f} GB/s  TFLOPS(N-c) {fl[-1] / 1e12:7.1f}")
+        # the rate of all N workers moving together (the final combine)
+        bw_all = w_move / _time(lambda: run(1 | 8, N), reps)
+        log(f"[calib] all {N} workers: BW {bw_all / 1e9:8.1f} GB/s")
         Ks = [1, 2, 4, 8]
         t_k = [_time(lambda: run(2 | 4, N, K), reps) for K in Ks]
         eff = [min(1.0, t_k[0] / t) for t in t_k]
@@ -111,7 +117,7 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
         def predict(alpha, ci, ki):
             t_comp = w_comp / (fl[ci] * eff[ki])
             t_comm = w_move / bw[ci]
-            t_tail = (1 - alpha) * (X * 2.0 * H) / (bw[ci] * Ks[ki])
+            t_tail = (1 - alpha) * (X * 2.0 * H) / (bw_all * Ks[ki])
             return max(t_comp + t_tail, t_comm)
 
         alphas = np.linspace(0.0, 1.0, 101)
@@ -123,7 +129,7 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
         static_c = max(1, min(N - 1, int(round(N * 20 / 132 / 8)) * 8))
         return {
             "workload": workload, "N": N, "c": c_grid, "bw": bw, "flops": fl, "K": Ks, "eff": eff,
-            "alpha": alpha, "static_c": static_c, "literal": 0,
+            "alpha": alpha, "static_c": static_c, "literal": 0, "bw_all": bw_all,
             "sweep": [[c_grid[ci], Ks[ki], t] for ci, ki, t in sweep],
             "device": torch.cuda.get_device_name(0), "date": time.strftime("%Y-%m-%d"),
         }

@@ -110,6 +110,8 @@ moe_status validate_calib(const moe_calib* k, int N) {
   }
   if (!(k->alpha >= 0 && k->alpha <= 1)) return fail(MOE_ERR_INVALID_ARG, "alpha must be in [0, 1]");
   if (k->static_c < 1 || k->static_c >= N) return fail(MOE_ERR_INVALID_ARG, "static_c must be in [1, N-1]");
+  if (!(k->bw_all_bytes_per_s >= 0) || !std::isfinite(k->bw_all_bytes_per_s))
+    return fail(MOE_ERR_INVALID_ARG, "bw_all must be >= 0 and finite");
   return MOE_OK;
 }
 
@@ -138,6 +140,7 @@ void default_calib(int N, moe_calib* k) {
   k->literal_volumes = 0;
   int sc = (int)std::lround(N * 20.0 / 132.0 / 8.0) * 8;  // 20 of 132 SMs, rounded to XCD multiples
   k->static_c = std::min(std::max(sc, 1), N - 1);
+  k->bw_all_bytes_per_s = 4.0e12;  // all workers copying together
 }
 
 void to_dev(const moe_calib& k, DevCalib* d) {
@@ -149,6 +152,7 @@ void to_dev(const moe_calib& k, DevCalib* d) {
   d->alpha = k.alpha;
   d->literal = k.literal_volumes;
   d->static_c = k.static_c;
+  d->bw_all = k.bw_all_bytes_per_s;
 }
 
 void compute_layout(moe_handle* h) {

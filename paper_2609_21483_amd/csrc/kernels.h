@@ -62,6 +62,7 @@ struct DevCalib {
   double alpha;
   int32_t literal;
   int32_t static_c;
+  double bw_all;  // > 0: the exposed tail moves at this rate (all N workers)
 };
 
 struct FwdArgs {
@@ -118,7 +119,10 @@ __host__ __device__ inline double cm_t_total(const DevCalib& cb, int ci, int ki,
   double K = (double)cb.kk[ki];
   double t_comp = w_comp / (fl * cb.eff[ki]);                // Eq 9 (Eq 4 at K = 1)
   double t_comm = (w_disp + w_comb) / bw;                    // Eq 5
-  double t_tail = ((1.0 - cb.alpha) * w_comb) / (bw * K);    // Eq 10 (Eq 6 at K = 1)
+  // Eq 10 (Eq 6 at K = 1); the last chunk's combine runs on all N workers
+  // (section 4), at the calibrated all-worker rate when one is given
+  double bw_tail = cb.bw_all > 0.0 ? cb.bw_all : bw;
+  double t_tail = ((1.0 - cb.alpha) * w_comb) / (bw_tail * K);
   double s = t_comp + t_tail;
   return s > t_comm ? s : t_comm;                            // Eq 15 (Eq 7 at K = 1)
 }

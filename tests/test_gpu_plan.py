@@ -39,7 +39,7 @@ def oracle_plan(B, h, shape, idx):
     n = cal.n_c
     return O.plan([cal.c[i] for i in range(n)], [cal.bw_bytes_per_s[i] for i in range(n)],
                   [cal.comp_flop_per_s[i] for i in range(n)], Ks, [cal.eff_chunk[j] for j in range(cal.n_k)],
-                  cal.alpha, n_workers(), wc, wd, wb, n_tiles)
+                  cal.alpha, n_workers(), wc, wd, wb, n_tiles, bw_all=cal.bw_all_bytes_per_s)
 
 
 def n_workers():

@@ -347,6 +347,30 @@ def test_cost_model_hand_example(orc):
         assert p.n_steal == n_steal
 
 
+def test_cost_model_hand_example_all_worker_tail(orc):
+    """The same hand example with the last chunk's combine moving at the rate
+    of all N = 64 workers, bw_all = 2^30 * 64 = 2^36 (section 4 runs the final
+    combine on every worker): Eq 10 becomes 0.5 * 2^34 / (2^36 K) = 1/(8K) s.
+    c=16: K=1 max(4 + 1/8, 1.5) = 4.125; K=2 4/0.75 + 1/16 = 259/48; K=4 8 + 1/32.
+    c=32: 6.125; 8.0625; 12.03125.  c=8, K=1: 192/56 + 1/8 = 199/56 (minimum).
+    n_steal (Eq 11-14) does not use the tail: 0 and 544 as before."""
+    d = json.load(open(os.path.join(GOLDEN, "cost_model_hand_example.json")))
+    args = dict(c=d["c"], bw=d["bw"], flops=d["flops"], K=d["K"], eff=d["eff"], alpha=d["alpha"],
+                N=d["N"], w_comp=d["w_comp"], w_dispatch=d["w_dispatch"], w_combine=d["w_combine"],
+                bw_all=float(2 ** 36))
+    assert orc.t_total(1, 0, n_tiles=[1, 1, 1], **args) == 4.125
+    assert math.isclose(orc.t_total(1, 1, n_tiles=[1, 1, 1], **args), 259 / 48, rel_tol=4e-16)
+    assert orc.t_total(1, 2, n_tiles=[1, 1, 1], **args) == 8.03125
+    assert orc.t_total(2, 0, n_tiles=[1, 1, 1], **args) == 6.125
+    assert orc.t_total(2, 1, n_tiles=[1, 1, 1], **args) == 8.0625
+    assert orc.t_total(2, 2, n_tiles=[1, 1, 1], **args) == 12.03125
+    for n_tiles, n_steal in d["cases_n_tiles"]:
+        p = orc.plan(n_tiles=n_tiles, **args)
+        assert (p.c, p.K) == (8, 1)
+        assert math.isclose(p.t_total, 199 / 56, rel_tol=5e-16)
+        assert p.n_steal == n_steal
+
+
 def test_cost_model_balance_point(orc):
     """BW(c) = beta*c, TFLOPS(N-c) = phi*(N-c), eff = 1, alpha = 1: T_total is
     max(Wc/(phi(N-c)), Wm/(beta c)); the continuous optimum is the balance
@@ -388,6 +412,11 @@ def test_cost_model_special_cases(orc):
     # movement-dominated: nothing to steal
     p = orc.plan(cs, bw, fl, Ks, eff_dec, 0.5, N, 1e9, 5e10, 5e10, nt)
     assert p.t_total == pytest.approx(1e11 / bw[-1]) and p.n_steal == 0
+    # a tail moved by all workers at a high rate is worth less than any
+    # chunking loss: K* = 1 where the printed BW(c) tail would chunk
+    p_lit = orc.plan(cs, bw, fl, Ks, [1.0, 0.9, 0.8, 0.7], 0.0, N, 1e12, 2e8, 2e8, nt)
+    p_all = orc.plan(cs, bw, fl, Ks, [1.0, 0.9, 0.8, 0.7], 0.0, N, 1e12, 2e8, 2e8, nt, bw_all=5e12)
+    assert p_lit.K > 1 and p_all.K == 1
 
 
 def test_cost_model_tie_break_first_minimum(orc):
