@@ -74,7 +74,7 @@ typedef struct {
   int32_t first_local_expert; /* e0, 0 <= e0 <= E - E_l */
   int32_t n_shared_experts;   /* S, 0..8, always-on experts applied to rank-0 tokens */
   int32_t n_workers;          /* persistent workgroups N; 0 = one per CU */
-  int32_t gemm1_split;        /* split-K factor of GEMM1 (K = F): 1, 2 or 4; 0 = chosen from F/H */
+  int32_t gemm1_split;        /* split-K factor of GEMM1 (K = F): 1, 2, 4 or 8; 0 = chosen from F/H */
 } moe_config;
 
 #define MOE_CALIB_MAX_C 32

@@ -40,6 +40,7 @@ struct moe_handle {
   moe_config cfg;
   int N = 0;
   int T = 0, xmax = 0, mt_max = 0, ctl_words = 0, nblk = 0, nseg = 0, nt0 = 0, nt1 = 0, nsplit = 1;
+  int qx = 0, qxs = 0;
   moe_calib calib{};
   DevCalib dcal{};
   moe_ws_layout lay{};
@@ -78,8 +79,9 @@ moe_status validate_cfg(const moe_config* c) {
   if (c->n_shared_experts < 0 || c->n_shared_experts > MAX_S)
     return fail(MOE_ERR_INVALID_ARG, "n_shared_experts must be in [0, %d]", MAX_S);
   if (c->n_workers < 0) return fail(MOE_ERR_INVALID_ARG, "n_workers must be >= 0");
-  if (c->gemm1_split != 0 && c->gemm1_split != 1 && c->gemm1_split != 2 && c->gemm1_split != 4)
-    return fail(MOE_ERR_INVALID_ARG, "gemm1_split must be 0, 1, 2 or 4");
+  if (c->gemm1_split != 0 && c->gemm1_split != 1 && c->gemm1_split != 2 && c->gemm1_split != 4 &&
+      c->gemm1_split != 8)
+    return fail(MOE_ERR_INVALID_ARG, "gemm1_split must be 0, 1, 2, 4 or 8");
   if (c->gemm1_split > 1 && c->ffn % (32 * c->gemm1_split))
     return fail(MOE_ERR_INVALID_ARG, "ffn must be a multiple of 32 * gemm1_split");
   long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
@@ -253,6 +255,8 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.xmax = h->xmax;
   a.mt_max = h->mt_max;
   a.ctl_words = h->ctl_words;
+  a.qx = h->qx;
+  a.qxs = h->qxs;
   a.x = x;
   a.topk_idx = topk_idx;
   a.topk_w = topk_w;
@@ -322,6 +326,11 @@ moe_status moe_init(const moe_config* cfg, const moe_calib* calib, moe_handle** 
   // readiness counters per row tile (dispatched rows, GEMM0 columns, GEMM1
   // columns) and, when GEMM1 is split, split arrivals per (row, column) tile
   h->ctl_words = CTL_READY + (3 * h->mt_max + (h->nsplit > 1 ? h->mt_max * h->nt1 : 0)) * CTL_PAD;
+  // per (stage, slab class) tile queue heads of the megakernel, then of the
+  // serial GEMM kernels
+  h->qx = h->ctl_words;
+  h->qxs = h->qx + 2 * MAX_K * NXCD * CTL_PAD;
+  h->ctl_words = h->qxs + 2 * MAX_K * NXCD * CTL_PAD;
   if (calib) {
     st = validate_calib(calib, N);
     if (st != MOE_OK) { delete h; return st; }

@@ -40,12 +40,11 @@ __host__ __device__ inline int kopt_value(int i) { return 1 << i; }
 // Every counter has a 64-byte line of its own (CTL_PAD words), so pollers of
 // one counter do not share a line with updates of another.
 constexpr int CTL_PAD = 16;
-constexpr int CTL_Q_COMP = 0;     // compute-tile queue head
 constexpr int CTL_TICKET = 16;    // arrival ticket -> role
 constexpr int CTL_ABORT = 32;     // set once any wait times out
-constexpr int CTL_SQ = 48;        // queue heads of the serial GEMM kernels (CTL_PAD apart)
 constexpr int CTL_QC = 128;       // [NSHARD] combine-unit queue heads (CTL_PAD apart)
 constexpr int NSHARD = 8;         // dispatch-unit queue shards
+constexpr int NXCD = 8;           // XCDs of gfx950 (slab classes of the tile queues)
 constexpr int CTL_QD = 256;       // [NSHARD] dispatch-unit queue heads (CTL_PAD apart)
 constexpr int CTL_READY = 384;    // [mt_max] dispatched rows per row tile (CTL_PAD apart),
 // then [mt_max] GEMM0 column tiles finished per row tile (CTL_PAD apart),

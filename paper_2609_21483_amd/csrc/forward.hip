@@ -39,6 +39,7 @@ struct Sched {
   int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A slot or token)
   int mb[MAX_K * MAX_SEG];     // first row-tile id (counter index)
   int gstart[MAX_K * 2 * MAX_SEG + 1];
+  int ncls[2 * MAX_K][NXCD];   // tiles of stage (chunk, phase) in slab class x
 };
 
 struct Scratch {
@@ -74,6 +75,14 @@ __device__ __forceinline__ void block_exscan(int* v, int n, int* part) {
   for (int i = b; i < e; ++i) { int t = v[i]; v[i] = run; run += t; }
   __syncthreads();
 }
+
+// XCD-aware tile queues.  A tile's weight slab is its GEMM0 column tile, or
+// its GEMM1 (column tile, split) pair; the tiles of one slab share the slab's
+// weights, so they are queued for one XCD (slab class = slab mod NXCD) and
+// read them from that XCD's L2.  Stage = (chunk, phase) in DAG order; each
+// stage has one queue per class, the row tile fastest within a slab.
+__device__ __forceinline__ int phase_slabs(const FwdArgs& a, int ph) { return ph == 0 ? a.nt0 : a.nt1 * a.nsplit; }
+__device__ __forceinline__ int class_slabs(int ns, int x) { return ns > x ? (ns - x + NXCD - 1) / NXCD : 0; }
 
 __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
   const int tid = threadIdx.x;
@@ -116,6 +125,13 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
   }
   if (tid == 0) S.gstart[S.G] = 0;
   __syncthreads();
+  for (int v = tid; v < 2 * K * NXCD; v += FNTH) {
+    const int stage = v / NXCD, x = v % NXCD, q = stage >> 1;
+    const int nsx = class_slabs(phase_slabs(a, stage & 1), x);
+    int n = 0;
+    for (int seg = 0; seg < nseg; ++seg) n += nsx * ceil_div(S.rows[q * nseg + seg], BM);
+    S.ncls[stage][x] = n;
+  }
   block_exscan(S.mb, K * nseg, W.part);
   block_exscan(S.gstart, S.G + 1, W.part);
   if (tid == 0) S.n_comp = S.gstart[S.G];
@@ -175,19 +191,35 @@ __device__ __forceinline__ int unit_slot(const FwdArgs& a, int u) {
   return (g < a.T && lane < min(DT, a.T - g) * a.k) ? a.slot[(size_t)g * a.k + lane] : -1;
 }
 
+// The lane id and the launch constants of a movement unit are defined by
+// opaque statements (see gemm::opaque), so that where a unit runs inside the
+// GEMM tile loop (movement stealing) the optimiser cannot hoist the unit's
+// per-lane index and address arithmetic out of that loop and keep it live
+// across the GEMM mainloop.
+__device__ __forceinline__ int lane_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 template <bool SIG>
 __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, Scratch& W, int u, int cur) {
+  using gemm::opaque;
   constexpr int VB = 32;  // 16-byte vectors per lane in flight
-  const int lane = lane_id();
-  int* sl = W.wsl[wave_id()];
-  int* act = W.wact[wave_id()];
-  const int k = a.k;
-  const int VPR = a.H >> 3;
+  const int lane = lane_here();
+  const int wv = opaque(wave_id());
+  int* sl = W.wsl[wv];
+  int* act = W.wact[wv];
+  const int k = opaque(a.k);
+  const int H = opaque(a.H);
+  const int VPR = H >> 3;
+  const int T = opaque(a.T);
+  const int xmax = opaque(a.xmax);
   const int g0 = u * DT;
-  const int nt = min(DT, a.T - g0);
+  const int nt = min(DT, T - g0);
   sl[lane] = cur;
   // tokens with at least one local slot, compacted in token order
-  const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)a.xmax);
+  const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)xmax);
   const bool tact = lane < nt && ((vm >> min(lane * k, 56)) & ((1ull << k) - 1)) != 0;
   const uint64_t am = __builtin_amdgcn_ballot_w64(tact);
   const int na = __builtin_popcountll(am);
@@ -206,7 +238,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
 #pragma unroll
         for (int m = 1; m < DT; ++m) t += v >= m * VPR;
         const int c = v - t * VPR;
-        val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + act[t]) * a.H) + c);
+        val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + act[t]) * H) + c);
       }
     }
 #pragma unroll
@@ -220,12 +252,12 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
       const int tok = act[t];
       for (int j = 0; j < k; ++j) {
         const int s = sl[tok * k + j];
-        if ((unsigned)s >= (unsigned)a.xmax) continue;
+        if ((unsigned)s >= (unsigned)xmax) continue;
         if constexpr (SIG) {
-          const uint32_t off = ((uint32_t)s * (uint32_t)a.H + (uint32_t)c * 8u) * 2u;
+          const uint32_t off = ((uint32_t)s * (uint32_t)H + (uint32_t)c * 8u) * 2u;
           __builtin_amdgcn_raw_buffer_store_b128(val[i], rA, off, 0, 16 /* sc1 */);
         } else {
-          reinterpret_cast<u32x4_t*>(a.A + (size_t)s * a.H)[c] = val[i];
+          reinterpret_cast<u32x4_t*>(a.A + (size_t)s * H)[c] = val[i];
         }
       }
     }
@@ -235,11 +267,11 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
     // this wavefront's rows have reached the coherence point: count them in
     // the readiness counters of their row tiles
     int id = -1;
-    if ((unsigned)cur < (unsigned)a.xmax) {
+    if ((unsigned)cur < (unsigned)xmax) {
       const int g = g0 + lane / k;
       const int le = a.topk_idx[(size_t)g * k + (lane % k)] - a.e0;
       if ((unsigned)le < (unsigned)a.El) {
-        const int q = (int)(((long long)g * S->K) / a.T);
+        const int q = (int)(((long long)g * S->K) / T);
         id = S->mb[q * S->nseg + le] + (cur - S->row0[q * S->nseg + le]) / BM;
         if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
       }
@@ -301,15 +333,12 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
 // One wavefront combines nt <= CT tokens.  Each token has KS = k + S source
 // rows: its k routed slots (weight w, absent when the expert is not local)
 // followed by its S shared-expert rows (weight 1, present for tokens of rank
-// 0).  They are summed in that order in fp32.  A source row is O (bf16; a
-// split GEMM1 tile was reduced into O in split order by its last split).  KS
+// 0).  They are summed in that order in fp32.  A source row is O (bf16).  KS
 // is a template constant so that every lane keeps about 16 row vectors in
-// flight (NS > 1 reads fp32 split partials directly; not used).
-template <int KS, int NS>
+// flight.
+template <int KS>
 __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
-  constexpr int NV = NS == 1 ? 1 : 2 * NS;                    // 16-byte loads per source row
-  constexpr int P = KS * NV >= 16 ? 1 : 16 / (KS * NV);       // positions per lane per pass
-  constexpr int JB = KS * NV <= 32 ? KS : (32 / NV);          // source rows per load batch
+  constexpr int P = KS >= 16 ? 1 : 16 / KS;  // positions per lane per pass
   const int lane = lane_id();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
@@ -324,55 +353,26 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[i][e] = 0.0f;
     }
+    u32x4_t o[P][KS];
 #pragma unroll
-    for (int j0 = 0; j0 < KS; j0 += JB) {
-      u32x4_t o[P][JB][NV];
+    for (int i = 0; i < P; ++i)
 #pragma unroll
-      for (int i = 0; i < P; ++i)
+      for (int j = 0; j < KS; ++j) {
+        const int s = tt[i] >= 0 ? sl[tt[i] * KS + j] : -1;
+        if (s >= 0) o[i][j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
+      }
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj) {
-          const int j = j0 + jj;
-          const int s = (j < KS && tt[i] >= 0) ? sl[tt[i] * KS + j] : -1;
-          if (s < 0) continue;
-          if constexpr (NS == 1) {
-            o[i][jj][0] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
-          } else {
+    for (int i = 0; i < P; ++i)
 #pragma unroll
-            for (int p = 0; p < NS; ++p) {
-              const u32x4_t* src =
-                  reinterpret_cast<const u32x4_t*>(a.part + ((size_t)p * a.prow + s) * a.H + cc[i] * 8);
-              o[i][jj][2 * p] = src[0];
-              o[i][jj][2 * p + 1] = src[1];
-            }
-          }
+      for (int j = 0; j < KS; ++j) {
+        if (tt[i] < 0 || sl[tt[i] * KS + j] < 0) continue;
+        const float w = wt[tt[i] * KS + j];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[i][2 * q] += w * bf16_lo(o[i][j][q]);
+          acc[i][2 * q + 1] += w * bf16_hi(o[i][j][q]);
         }
-#pragma unroll
-      for (int i = 0; i < P; ++i)
-#pragma unroll
-        for (int jj = 0; jj < JB; ++jj) {
-          const int j = j0 + jj;
-          if (j >= KS || tt[i] < 0 || sl[tt[i] * KS + j] < 0) continue;
-          const float w = wt[tt[i] * KS + j];
-          float ov[8];
-          if constexpr (NS == 1) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              ov[2 * q] = bf16_lo(o[i][jj][0][q]);
-              ov[2 * q + 1] = bf16_hi(o[i][jj][0][q]);
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              float t = __uint_as_float(o[i][jj][e >> 2][e & 3]);
-#pragma unroll
-              for (int p = 1; p < NS; ++p) t += __uint_as_float(o[i][jj][2 * p + (e >> 2)][e & 3]);
-              ov[e] = bf16_to_f32(f32_to_bf16(t));
-            }
-          }
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[i][e] += w * ov[e];
-        }
-    }
+      }
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       if (tt[i] < 0) continue;
@@ -386,8 +386,8 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
 }
 
 // A wavefront combines tokens [g0, g0 + nt).  In the megakernel (S given) it
-// first waits until every GEMM1 item of each row tile holding one of those
-// tokens' source rows is done: one lane polls per distinct row tile.
+// first waits until every GEMM1 column tile of each row tile holding one of
+// those tokens' source rows is done: one lane polls per distinct row tile.
 // Returns false when the launch was aborted.
 __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S, Scratch& W, int g0, int nt) {
   const int lane = lane_id();
@@ -433,7 +433,7 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
   __builtin_amdgcn_wave_barrier();
   switch (ks) {
 #define MOE_COMBINE_CASE(n) \
-  case n: combine_body<n, 1>(a, sl, wt, g0, nt); break;
+  case n: combine_body<n>(a, sl, wt, g0, nt); break;
     MOE_COMBINE_CASE(1) MOE_COMBINE_CASE(2) MOE_COMBINE_CASE(3) MOE_COMBINE_CASE(4)
     MOE_COMBINE_CASE(5) MOE_COMBINE_CASE(6) MOE_COMBINE_CASE(7) MOE_COMBINE_CASE(8)
     MOE_COMBINE_CASE(9) MOE_COMBINE_CASE(10) MOE_COMBINE_CASE(11) MOE_COMBINE_CASE(12)
@@ -452,38 +452,69 @@ struct TileRef {
   int q, ph, seg, mt, nt, ks, rows;
 };
 
-__device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S, int t) {
-  int lo = 0, hi = S.G;  // the group gi with gstart[gi] <= t < gstart[gi+1]
-  while (hi - lo > 1) {
-    int mid = (lo + hi) >> 1;
-    if (S.gstart[mid] <= t) lo = mid; else hi = mid;
-  }
+// tile code: stage << 24 | class << 21 | index in the class queue
+__device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S, int code) {
+  const int stage = code >> 24, x = (code >> 21) & (NXCD - 1);
+  int i = code & ((1 << 21) - 1);
   TileRef r;
-  r.q = lo / (2 * S.nseg);
-  r.ph = (lo / S.nseg) & 1;
-  r.seg = lo % S.nseg;
-  int local = t - S.gstart[lo];
-  const int rows = S.rows[r.q * S.nseg + r.seg];
-  const int nmt = ceil_div(rows, BM);
+  r.q = stage >> 1;
+  r.ph = stage & 1;
+  const int nsx = class_slabs(phase_slabs(a, r.ph), x);
+  int seg = 0, nmt = 1, rows = 0;
+  for (; seg < S.nseg; ++seg) {
+    rows = S.rows[r.q * S.nseg + seg];
+    nmt = ceil_div(rows, BM);
+    const int c = nsx * nmt;
+    if (i < c) break;
+    i -= c;
+  }
+  r.seg = seg;
+  r.mt = i % nmt;
+  const int slab = x + NXCD * (i / nmt);
   if (r.ph == 0) {
+    r.nt = slab;
     r.ks = 0;
   } else {
-    r.ks = local % a.nsplit;
-    local /= a.nsplit;
+    r.nt = slab / a.nsplit;
+    r.ks = slab % a.nsplit;
   }
-  r.mt = local % nmt;
-  r.nt = local / nmt;
   r.rows = min(BM, rows - r.mt * BM);
   return r;
 }
 
+// Claims the next tile for a workgroup on XCD `home` (thread 0): its own
+// class of the current stage first, then the other classes of that stage;
+// the next stage only once every class of this one is exhausted, so a GEMM1
+// tile is taken only when every GEMM0 tile of its chunk has been claimed by a
+// running workgroup.  ph_only >= 0 restricts to one phase.  Returns the tile
+// code or -1.
+__device__ __forceinline__ int claim_tile(const FwdArgs& a, const Sched& S, int base, int ph_only, int home,
+                                          int& stage, uint32_t& exhausted) {
+  for (; stage < 2 * S.K; ++stage, exhausted = 0u) {
+    if (ph_only >= 0 && (stage & 1) != ph_only) continue;
+    for (int j = 0; j < NXCD; ++j) {
+      const int x = (home + j) & (NXCD - 1);
+      const int n = S.ncls[stage][x];
+      if (n == 0 || ((exhausted >> x) & 1u)) continue;
+      int* q = &a.ctl[base + (stage * NXCD + x) * CTL_PAD];
+      // other classes are read first so that exhausted queues take no atomic
+      if (j > 0 && ld_relaxed(q) >= n) { exhausted |= 1u << x; continue; }
+      const int i = fetch_add_relaxed(q, 1);
+      if (i < n) return (stage << 24) | (x << 21) | i;
+      exhausted |= 1u << x;
+    }
+  }
+  return -1;
+}
+
 // Runs one GEMM0 tile or one split of a GEMM1 tile.  One mainloop instance
 // serves both GEMMs; only the operands and the epilogue differ.
-// When claim_q is given, thread 0 claims the next queue entry between the
-// mainloop and the epilogue (returned on thread 0), so the claim's round trip
-// overlaps the epilogue stores.
-template <int CP>
-__device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* ring, int* claim_q) {
+// Thread 0 claims the next tile (claim_next) between the mainloop and the
+// epilogue (returned on thread 0), so the claim's round trip overlaps the
+// epilogue stores.
+template <int CP, typename ClaimFn>
+__device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const TileRef& r, char* ring,
+                                        ClaimFn&& claim_next) {
   const int qs = r.q * S.nseg + r.seg;
   const size_t orow = (size_t)S.row0[qs] + (size_t)r.mt * BM;
   const int n0 = r.nt * BN;
@@ -508,8 +539,8 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
   gemm::Acc acc;
   gemm::zero(acc);
   gemm::mainloop(acc, Aop, ld, r.rows, Bop, ld, b_rows, Kd, ring);
-  int nxt = 0;
-  if (claim_q && threadIdx.x == 0) nxt = fetch_add_relaxed(claim_q, 1);
+  int nxt = -1;
+  if (threadIdx.x == 0) nxt = claim_next();
   if (r.ph == 0) {
     gemm::store_silu_mul<CP>(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
   } else if (a.nsplit == 1) {
@@ -522,39 +553,53 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
 
 // Split-K reduction of one GEMM1 tile by its last-arriving split: O rows
 // [orow, orow + rows) x columns [n0, n0 + cols) = bf16(P_0 + P_1 + ... ) in
-// split order, 4 columns per thread and step.
-template <int CP>
-__device__ __forceinline__ void reduce_split(const FwdArgs& a, size_t orow, int rows, int n0, int cols) {
+// split order, 4 columns per thread and step.  NS (the split count) is a
+// template constant so that the loads of every split of a batch are issued
+// before the first add: one memory round trip per batch.
+template <int CP, int NS>
+__device__ __forceinline__ void reduce_split_n(const FwdArgs& a, size_t orow, int rows, int n0, int cols) {
   const __amdgpu_buffer_rsrc_t rO = __builtin_amdgcn_make_buffer_rsrc(a.O, 0, -1, 0x00020000);
   const int q4 = cols >> 2;  // cols % 64 == 0
   const int total = rows * q4;
-  constexpr int RB = 8;
+  const size_t pstride = (size_t)a.prow * a.H;
+  constexpr int RB = NS >= 8 ? 4 : 32 / NS;  // 32 vectors in flight per thread
   for (int v0 = threadIdx.x; v0 < total; v0 += RB * FNTH) {
-    f32x4_t t[RB];
+    f32x4_t u[RB][NS];
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int v = v0 + i * FNTH;
       if (v >= total) continue;
       const int r = v / q4, c = (v - r * q4) * 4;
-      const size_t e = (orow + r) * (size_t)a.H + n0 + c;
-      t[i] = *reinterpret_cast<const f32x4_t*>(a.part + e);
-      for (int p = 1; p < a.nsplit; ++p) {
-        const f32x4_t u = *reinterpret_cast<const f32x4_t*>(a.part + (size_t)p * a.prow * a.H + e);
+      const float* src = a.part + (orow + r) * (size_t)a.H + n0 + c;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) t[i][j] += u[j];
-      }
+      for (int p = 0; p < NS; ++p) u[i][p] = *reinterpret_cast<const f32x4_t*>(src + p * pstride);
     }
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int v = v0 + i * FNTH;
       if (v >= total) continue;
       const int r = v / q4, c = (v - r * q4) * 4;
+      f32x4_t t = u[i][0];
+#pragma unroll
+      for (int p = 1; p < NS; ++p)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t[j] += u[i][p][j];
       const size_t e = (orow + r) * (size_t)a.H + n0 + c;
       typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-      const u32x2_t packed = {pack_bf16x2(t[i][0], t[i][1]), pack_bf16x2(t[i][2], t[i][3])};
+      const u32x2_t packed = {pack_bf16x2(t[0], t[1]), pack_bf16x2(t[2], t[3])};
       if constexpr (CP == gemm::CP_PLAIN) *reinterpret_cast<u32x2_t*>(a.O + e) = packed;
       else __builtin_amdgcn_raw_buffer_store_b64(packed, rO, (uint32_t)(e * 2), 0, CP);
     }
+  }
+}
+
+template <int CP>
+__device__ __forceinline__ void reduce_split(const FwdArgs& a, size_t orow, int rows, int n0, int cols) {
+  switch (a.nsplit) {
+    case 2: reduce_split_n<CP, 2>(a, orow, rows, n0, cols); break;
+    case 4: reduce_split_n<CP, 4>(a, orow, rows, n0, cols); break;
+    case 8: reduce_split_n<CP, 8>(a, orow, rows, n0, cols); break;
+    default: break;
   }
 }
 
@@ -700,14 +745,6 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
   }
 }
 
-__device__ __forceinline__ int claim(Scratch& W, int* q) {
-  if (threadIdx.x == 0) W.bc[1] = fetch_add_relaxed(q, 1);
-  __syncthreads();
-  const int r = W.bc[1];
-  __syncthreads();
-  return r;
-}
-
 // Runs up to max_tiles compute tiles from the shared queue (all of them for a
 // compute worker, n_steal for a movement worker).  A tile waits for its inputs
 // (GEMM0: its rows dispatched; GEMM1: every GEMM0 column tile of its row
@@ -717,8 +754,14 @@ __device__ __forceinline__ int claim(Scratch& W, int* q) {
 __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, Scratch& W, char* ring, int ticket,
                                               int max_tiles) {
   if (max_tiles <= 0) return true;
-  int t = claim(W, &a.ctl[CTL_Q_COMP]);
-  for (int done = 1; t < S.n_comp; ++done) {
+  const int home = xcd_id() & (NXCD - 1);
+  int stage = 0;           // thread 0's claim position
+  uint32_t exhausted = 0;  // classes of that stage found empty
+  if (threadIdx.x == 0) W.bc[1] = claim_tile(a, S, a.qx, -1, home, stage, exhausted);
+  __syncthreads();
+  int t = __builtin_amdgcn_readfirstlane(W.bc[1]);
+  __syncthreads();
+  for (int done = 1; t >= 0; ++done) {
     const uint64_t t0 = a.trace ? now_ticks() : 0;
     const TileRef r = decode_tile(a, S, t);
     const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
@@ -729,9 +772,9 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
     }
     const uint64_t t1 = a.trace ? now_ticks() : 0;
     const bool more = done < max_tiles;
-    const int nxt = run_gemm<gemm::CP_SC1>(a, S, r, ring, more ? &a.ctl[CTL_Q_COMP] : nullptr);
+    const int nxt = run_gemm<gemm::CP_SC1>(a, S, r, ring, [&] { return more ? claim_tile(a, S, a.qx, -1, home, stage, exhausted) : -1; });
     __builtin_amdgcn_s_waitcnt(0);
-    if (threadIdx.x == 0) W.bc[1] = more ? nxt : S.n_comp;
+    if (threadIdx.x == 0) W.bc[1] = nxt;
     __syncthreads();  // every thread's output stores have completed
     // GEMM0 tile: its row tile gains a column; GEMM1 tile (or the last split
     // of one, after it reduced the tile): its row tile gains a column
@@ -747,7 +790,7 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
       if (publish) fetch_add_relaxed(&a.ctl[CTL_READY + ((r.ph == 0 ? 1 : 2) * a.mt_max + id) * CTL_PAD], 1);
       if (a.trace) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
     }
-    t = W.bc[1];  // rewritten only after the next mainloop's barriers
+    t = __builtin_amdgcn_readfirstlane(W.bc[1]);  // rewritten only after the next mainloop's barriers
   }
   return true;
 }
@@ -836,39 +879,35 @@ __global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {
 }
 
 template <int PH>
-__device__ __forceinline__ void serial_gemm(const FwdArgs& a, int qslot) {
+__device__ __forceinline__ void serial_gemm(const FwdArgs& a) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
   build_sched(a, S, W, a.serial_K);
-  // the tiles of phase PH in every chunk, in queue order
-  int count = 0;
-  for (int q = 0; q < S.K; ++q)
-    count += S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
-  int* qh = &a.ctl[CTL_SQ + CTL_PAD * qslot];
-  int t = claim(W, qh);
-  while (t < count) {
-    int q = 0, u = t;
-    for (;; ++q) {
-      const int n = S.gstart[(2 * q + PH + 1) * S.nseg] - S.gstart[(2 * q + PH) * S.nseg];
-      if (u < n) break;
-      u -= n;
-    }
-    const TileRef r = decode_tile(a, S, S.gstart[(2 * q + PH) * S.nseg] + u);
+  const int home = xcd_id() & (NXCD - 1);
+  int stage = 0;
+  uint32_t exhausted = 0;
+  if (threadIdx.x == 0) W.bc[1] = claim_tile(a, S, a.qxs, PH, home, stage, exhausted);
+  __syncthreads();
+  int t = __builtin_amdgcn_readfirstlane(W.bc[1]);
+  __syncthreads();
+  while (t >= 0) {
+    const TileRef r = decode_tile(a, S, t);
     const bool split = PH == 1 && a.nsplit > 1;
+    auto next = [&] { return claim_tile(a, S, a.qxs, PH, home, stage, exhausted); };
     // split partials are read by another workgroup within this kernel:
     // agent-coherent stores, drained before the arrival count
-    const int nxt = split ? run_gemm<gemm::CP_SC1>(a, S, r, ring, qh) : run_gemm<gemm::CP_PLAIN>(a, S, r, ring, qh);
+    const int nxt = split ? run_gemm<gemm::CP_SC1>(a, S, r, ring, next) : run_gemm<gemm::CP_PLAIN>(a, S, r, ring, next);
     if (split) __builtin_amdgcn_s_waitcnt(0);
     if (threadIdx.x == 0) W.bc[1] = nxt;
     __syncthreads();
     if (split) arrive_and_reduce<gemm::CP_PLAIN>(a, S, W, r, S.mb[r.q * S.nseg + r.seg] + r.mt);
-    t = W.bc[1];  // rewritten only after the next mainloop's barriers
+    t = __builtin_amdgcn_readfirstlane(W.bc[1]);  // rewritten only after the next mainloop's barriers
   }
 }
 
-__global__ void __launch_bounds__(FNTH, 1) serial_gemm0_kernel(FwdArgs a) { serial_gemm<0>(a, 1); }
-__global__ void __launch_bounds__(FNTH, 1) serial_gemm1_kernel(FwdArgs a) { serial_gemm<1>(a, 2); }
+__global__ void __launch_bounds__(FNTH, 1) serial_gemm0_kernel(FwdArgs a) { serial_gemm<0>(a); }
+__global__ void __launch_bounds__(FNTH, 1) serial_gemm1_kernel(FwdArgs a) { serial_gemm<1>(a); }
 
 __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   __shared__ Scratch W;

@@ -114,15 +114,17 @@ __device__ __forceinline__ void dma_offsets(DmaOff& o, int lda, int a_rows, int 
   }
 }
 
-__device__ __forceinline__ void issue_stage(char* stage, const char* A, const char* B, const DmaOff& o, int k0) {
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const char* Ak = uniform_ptr(A + (size_t)k0 * 2);
-  const char* Bk = uniform_ptr(B + (size_t)k0 * 2);
-  const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds_u32(stage));
+// One k-step of A and B into a ring stage.  Every operand is a scalar
+// computed once per tile (see mainloop), so the loop holds no vector
+// register that was loaded from memory before it: a reload in front of the
+// loop would otherwise make the compiler wait for every outstanding DMA at
+// each iteration.
+__device__ __forceinline__ void issue_stage(uint32_t lds_a, uint32_t lds_b, const char* Ak, const char* Bk,
+                                            const DmaOff& o) {
 #pragma unroll
-  for (int i = 0; i < A_INSTR; ++i) dma16(Ak, o.a[i], l0 + (wave * A_INSTR + i) * 1024);
+  for (int i = 0; i < A_INSTR; ++i) dma16(Ak, o.a[i], lds_a + i * 1024);
 #pragma unroll
-  for (int i = 0; i < B_INSTR; ++i) dma16(Bk, o.b[i], l0 + A_BYTES + (wave * B_INSTR + i) * 1024);
+  for (int i = 0; i < B_INSTR; ++i) dma16(Bk, o.b[i], lds_b + i * 1024);
 }
 
 struct FragOff {
@@ -170,12 +172,22 @@ __device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, i
   const int nk = Kd / KSTEP;
   DmaOff o;
   dma_offsets(o, lda, a_rows, ldb, b_rows);
-  const char* Ab = reinterpret_cast<const char*>(A);
-  const char* Bb = reinterpret_cast<const char*>(B);
+  // scalars of the DMA issue: this wave's destinations in stage 0 and the
+  // operand bases, pinned in scalar registers
+  const int wave = opaque((int)(threadIdx.x >> 6));
+  const uint32_t ring0 = (uint32_t)opaque((int)lds_u32(ring));
+  const uint32_t la0 = ring0 + (uint32_t)(wave * A_INSTR * 1024);
+  const uint32_t lb0 = ring0 + (uint32_t)(A_BYTES + wave * B_INSTR * 1024);
+  const char* Ab = opaque(reinterpret_cast<const char*>(A));
+  const char* Bb = opaque(reinterpret_cast<const char*>(B));
   auto st = [&](int s) { return ring + (s & (NSTAGE - 1)) * STAGE_BYTES; };
-  issue_stage(st(0), Ab, Bb, o, 0);
-  if (nk > 1) issue_stage(st(1), Ab, Bb, o, KSTEP);
-  if (nk > 2) issue_stage(st(2), Ab, Bb, o, 2 * KSTEP);
+  auto issue = [&](int s) {
+    const uint32_t so = (uint32_t)((s & (NSTAGE - 1)) * STAGE_BYTES);
+    issue_stage(la0 + so, lb0 + so, Ab + (size_t)s * (KSTEP * 2), Bb + (size_t)s * (KSTEP * 2), o);
+  };
+  issue(0);
+  if (nk > 1) issue(1);
+  if (nk > 2) issue(2);
   if (nk > 2) wait_vm<2 * INSTR>(); else if (nk > 1) wait_vm<INSTR>(); else wait_vm<0>();
   __builtin_amdgcn_s_barrier();
   compiler_fence();
@@ -189,7 +201,7 @@ __device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, i
     wait_vm<INSTR>();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    issue_stage(st(s + 3), Ab, Bb, o, (s + 3) * KSTEP);
+    issue(s + 3);
     load_frags(st(s + 1), 0, fo, fa0, fb0);
     mfma_block(acc, fa1, fb1);
   }

@@ -69,10 +69,11 @@ struct FwdArgs {
   // shape
   int T, Tr, R, H, F, k, El, S, e0, N;
   int nt0, nt1;   // column tiles of GEMM0 (over 2F) and GEMM1 (over H)
-  int nsplit;     // split-K factor of GEMM1 (1, 2 or 4)
+  int nsplit;     // split-K factor of GEMM1 (1, 2, 4 or 8)
   int xmax;       // rows reserved for routed pairs in A / Hbuf / O
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
+  int qx, qxs;    // word offsets of the [2 MAX_K][NXCD] tile queue heads (megakernel, serial GEMMs)
   // inputs / output
   const uint16_t* x;
   const int32_t* topk_idx;

@@ -32,7 +32,7 @@ def cfg_for(shape, **kw):
 @pytest.mark.parametrize("field,value", [
     ("hidden", 100), ("hidden", 0), ("ffn", 96), ("top_k", 0), ("top_k", 9), ("n_experts", 0),
     ("n_local_experts", 0), ("first_local_expert", 7), ("n_src_ranks", 0), ("tokens_per_rank", 0),
-    ("n_shared_experts", 9), ("n_workers", -1), ("gemm1_split", 3), ("gemm1_split", 8),
+    ("n_shared_experts", 9), ("n_workers", -1), ("gemm1_split", 3), ("gemm1_split", 16),
 ])
 def test_init_rejects_bad_config(field, value):
     c = cfg_for(W.TINY, **{field: value})
@@ -84,7 +84,7 @@ def test_workspace_layout_covers_buffers(shape):
             shape.hidden * shape.ffn * 2
         bm, nt0, nt1 = B.moe_tile_geometry(h)
         assert nt0 == math.ceil(2 * shape.ffn / 256) and bm > 0
-        # GEMM1 tiles per row tile: column tiles over H times a split-K factor of 1, 2 or 4
+        # GEMM1 tiles per row tile: column tiles over H times a split-K factor of 1, 2, 4 or 8
         assert nt1 // math.ceil(shape.hidden / 256) in (1, 2, 4) and nt1 % math.ceil(shape.hidden / 256) == 0
     finally:
         B.moe_destroy(h)

@@ -95,10 +95,11 @@ def test_edge_shapes(B, shape):
     check_case(B, c, forced=FORCED_SMALL, check_A=True)
 
 
-@pytest.mark.parametrize("split", [1, 2, 4])
+@pytest.mark.parametrize("split", [1, 2, 4, 8])
 def test_gemm1_split_factors(B, split):
-    """GEMM1 split 1, 2 or 4 ways over F (the combine adds the fp32 partials
-    in split order); shared experts and a ragged row tail included."""
+    """GEMM1 split 1, 2, 4 or 8 ways over F (the last split of a tile adds
+    the fp32 partials in split order); shared experts and a ragged row tail
+    included."""
     shape = W.MoeShape("split", 92, 3, 70, 128, 512, 8, 2, 4, n_shared_experts=1)
     c = make_case(shape.with_(w_std=0.05))
     check_case(B, c, forced=[(8, 2, 3, 1), (100, 4, 0, 0)], gemm1_split=split)
