@@ -167,10 +167,13 @@ moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
  *   int64 word 0: kind | ticket << 8 | xcd << 20 | id << 32
  *   int64 words 1-3: times t0, t1, t2 from the 100 MHz device clock
  * kind 1 workgroup (id 1 = movement worker): entry, plan + schedule built, exit
- * kind 2 compute tile (id = queue index): claimed, inputs ready, finished
+ * kind 2 compute tile (id = tile code: stage << 24 | XCD class << 21 |
+ *        index): claimed, inputs ready, finished
  * kind 3 dispatch by one movement worker: start, end
- * kind 4 combine of one chunk by one wavefront (id = chunk | wave << 8):
- *        start, inputs ready, end
+ * kind 4 combine unit of one wavefront (id = unit | wave << 24): claimed,
+ *        claimed, end
+ * kind 5 dispatch unit of one wavefront (id = unit | wave << 24): start,
+ *        rows stored and drained, readiness counted
  * Word 0 of buf holds the number of records written (at most
  * (bytes - 64) / 32 are stored); records start at byte 64.  The layout of a
  * trace follows the handle's current plan; it changes nothing else.

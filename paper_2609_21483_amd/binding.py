@@ -170,7 +170,7 @@ def moe_set_trace(h: int, buf, nbytes: int = 0) -> None:
     _check("moe_set_trace", _lib.moe_set_trace(h, ptr, n))
 
 
-TRACE_KINDS = {1: "workgroup", 2: "tile", 3: "dispatch", 4: "combine"}
+TRACE_KINDS = {1: "workgroup", 2: "tile", 3: "dispatch", 4: "combine", 5: "dispatch unit"}
 
 
 def read_trace(buf) -> "np.ndarray":

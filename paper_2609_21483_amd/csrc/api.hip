@@ -252,6 +252,14 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.nt0 = h->nt0;
   a.nt1 = h->nt1;
   a.nsplit = h->nsplit;
+  // movement units: as many as there are wavefronts on the workers (a whole
+  // unit per wavefront while every worker still moves rows), at most DT / CT
+  // tokens each
+  {
+    const int per = h->T / (h->N * (FNTH / WAVE));
+    a.dt = per < 1 ? 1 : (per > DT ? DT : per);
+    a.ct = per < 1 ? 1 : (per > CT ? CT : per);
+  }
   a.xmax = h->xmax;
   a.mt_max = h->mt_max;
   a.ctl_words = h->ctl_words;

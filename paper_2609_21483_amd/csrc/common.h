@@ -17,15 +17,16 @@ constexpr int WAVE = 64;
 // grouped-GEMM tile: BM rows x BN columns (bf16 MFMA 32x32x16, see gemm.h)
 constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int MAX_SPLIT = 4;    // split-K factor limit of GEMM1
+constexpr int MAX_SPLIT = 8;    // split-K factor limit of GEMM1
 
-constexpr int DT = 8;           // tokens per dispatch unit (one wavefront; DT * top_k <= 64)
-constexpr int CT = 4;           // tokens per combine unit (one wavefront)
+constexpr int DT = 8;           // most tokens per dispatch unit (one wavefront; DT * top_k <= 64)
+constexpr int CT = 4;           // most tokens per combine unit (one wavefront)
 
 constexpr int MAX_EL = 64;      // local experts
 constexpr int MAX_S = 8;        // shared experts
 constexpr int MAX_SEG = MAX_EL + MAX_S;
 constexpr int MAX_K = 8;        // chunk count limit
+constexpr int NLVL = 16;       // readiness levels of the row tiles of a stage
 constexpr int MAX_TOPK = 8;
 constexpr int MAX_E = 512;
 constexpr int KOPT = 4;         // chunk options with stored offsets: K = 1, 2, 4, 8

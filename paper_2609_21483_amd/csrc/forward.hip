@@ -38,6 +38,7 @@ struct Sched {
   int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts)
   int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A slot or token)
   int mb[MAX_K * MAX_SEG];     // first row-tile id (counter index)
+  int lvl[MAX_K][NLVL + 1];    // row tiles of chunk q at readiness level <= L
   int gstart[MAX_K * 2 * MAX_SEG + 1];
   int ncls[2 * MAX_K][NXCD];   // tiles of stage (chunk, phase) in slab class x
 };
@@ -84,6 +85,26 @@ __device__ __forceinline__ void block_exscan(int* v, int n, int* part) {
 __device__ __forceinline__ int phase_slabs(const FwdArgs& a, int ph) { return ph == 0 ? a.nt0 : a.nt1 * a.nsplit; }
 __device__ __forceinline__ int class_slabs(int ns, int x) { return ns > x ? (ns - x + NXCD - 1) / NXCD : 0; }
 
+// Readiness levels order the row tiles of a stage by when their inputs can be
+// complete.  Dispatch writes a local expert's rows in token order, so row
+// tile mt of a segment of `rows` rows is complete once the fraction
+// min((mt + 1) * BM, rows) / rows of the segment is written; its level is
+// that fraction rounded up to a multiple of 1/NLVL (1..NLVL).  Shared-expert
+// rows are read straight from x: level 0, ready at launch.
+__device__ __forceinline__ int tiles_upto(int rows, int L) {  // routed tiles at level <= L
+  const int nmt = (rows + BM - 1) / BM;
+  if (L <= 0) return 0;
+  if (L >= NLVL) return nmt;
+  return min(nmt, (int)(((long long)L * rows) / ((long long)NLVL * BM)));
+}
+__device__ __forceinline__ int level_lo(int rows, bool shared, int L) {  // first row tile of level L
+  return shared ? 0 : tiles_upto(rows, L - 1);
+}
+__device__ __forceinline__ int level_tiles(int rows, bool shared, int L) {
+  if (shared) return L == 0 ? (rows + BM - 1) / BM : 0;
+  return tiles_upto(rows, L) - tiles_upto(rows, L - 1);
+}
+
 __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
   const int tid = threadIdx.x;
   const int ki = kopt_index(K);
@@ -94,8 +115,8 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
     S.nseg = nseg;
     S.G = K * 2 * nseg;
     for (int q = 0; q <= K; ++q) S.bnd[q] = (int)(((long long)q * a.T + K - 1) / K);
-    S.n_comb = ceil_div(a.T, CT);
-    S.n_disp = ceil_div(a.T, DT);
+    S.n_comb = ceil_div(a.T, a.ct);
+    S.n_disp = ceil_div(a.T, a.dt);
   }
   __syncthreads();
   for (int v = tid; v < K * nseg; v += FNTH) {
@@ -132,6 +153,15 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
     for (int seg = 0; seg < nseg; ++seg) n += nsx * ceil_div(S.rows[q * nseg + seg], BM);
     S.ncls[stage][x] = n;
   }
+  for (int v = tid; v < K * (NLVL + 1); v += FNTH) {
+    const int q = v / (NLVL + 1), L = v % (NLVL + 1);
+    int n = 0;
+    for (int seg = 0; seg < nseg; ++seg) n += level_tiles(S.rows[q * nseg + seg], seg >= a.El, L);
+    S.lvl[q][L] = n;
+  }
+  __syncthreads();
+  if (tid < K)
+    for (int L = 1; L <= NLVL; ++L) S.lvl[tid][L] += S.lvl[tid][L - 1];
   block_exscan(S.mb, K * nseg, W.part);
   block_exscan(S.gstart, S.G + 1, W.part);
   if (tid == 0) S.n_comp = S.gstart[S.G];
@@ -141,9 +171,9 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
 // ===========================================================================
 // Movement work, one wavefront per unit (no workgroup barriers, so the eight
 // wavefronts of a movement worker overlap their latency chains):
-// dispatch copies the rows of DT tokens into their expert-contiguous A slots
+// dispatch copies the rows of dt tokens into their expert-contiguous A slots
 // (each row read once, written to every local slot); combine writes the
-// weighted sum of the expert outputs of CT tokens into the output staging
+// weighted sum of the expert outputs of ct tokens into the output staging
 // region.
 // ===========================================================================
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
@@ -175,7 +205,7 @@ __device__ __forceinline__ void trace_rec(const FwdArgs& a, int kind, int ticket
 // queue counter is contended.
 
 // Dispatch (section 4, with dedup): a wavefront copies the rows of tokens
-// [u*DT, u*DT + DT) of unit u; each token row is read once and written to
+// [u*dt, u*dt + dt) of unit u; each token row is read once and written to
 // every local slot it has.  Only tokens with a local slot are read.
 // In the megakernel (SIG) the rows are written with agent-coherent (sc1)
 // 16-byte buffer stores, so once they have completed (vmcnt 0) they are
@@ -186,9 +216,9 @@ __device__ __forceinline__ void trace_rec(const FwdArgs& a, int kind, int ticket
 
 // this lane's slot entry of unit u (lane = token * k + j), or -1
 __device__ __forceinline__ int unit_slot(const FwdArgs& a, int u) {
-  const int g = u * DT;
+  const int g = u * a.dt;
   const int lane = lane_id();
-  return (g < a.T && lane < min(DT, a.T - g) * a.k) ? a.slot[(size_t)g * a.k + lane] : -1;
+  return (g < a.T && lane < min(a.dt, a.T - g) * a.k) ? a.slot[(size_t)g * a.k + lane] : -1;
 }
 
 // The lane id and the launch constants of a movement unit are defined by
@@ -215,8 +245,10 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
   const int VPR = H >> 3;
   const int T = opaque(a.T);
   const int xmax = opaque(a.xmax);
-  const int g0 = u * DT;
-  const int nt = min(DT, T - g0);
+  const int dt = opaque(a.dt);
+  const int g0 = u * dt;
+  const int nt = min(dt, T - g0);
+  const uint64_t tr0 = (SIG && a.trace) ? now_ticks() : 0;
   sl[lane] = cur;
   // tokens with at least one local slot, compacted in token order
   const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)xmax);
@@ -263,6 +295,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
     }
   }
   __builtin_amdgcn_s_waitcnt(0);
+  const uint64_t tr1 = (SIG && a.trace) ? now_ticks() : 0;
   if constexpr (SIG) {
     // this wavefront's rows have reached the coherence point: count them in
     // the readiness counters of their row tiles
@@ -285,6 +318,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
       if (lane == leader) fetch_add_relaxed(&a.ctl[CTL_READY + tile * CTL_PAD], (int)__builtin_popcountll(same));
       pending &= ~same;
     }
+    if (a.trace && lane == 0) trace_rec(a, 5, 0, u | ((long long)wv << 24), tr0, tr1, now_ticks());
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -292,7 +326,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
 // serial kernel: units u0, u0 + ustride, ..., the next unit's slot entries
 // fetched while the current one is copied
 __device__ __forceinline__ void dispatch_static(const FwdArgs& a, Scratch& W, int u, int ustride) {
-  const int nu = ceil_div(a.T, DT);
+  const int nu = ceil_div(a.T, a.dt);
   int next = unit_slot(a, u);
   for (; u < nu; u += ustride) {
     const int cur = next;
@@ -330,7 +364,7 @@ __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& 
 
 __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target);
 
-// One wavefront combines nt <= CT tokens.  Each token has KS = k + S source
+// One wavefront combines nt <= ct tokens.  Each token has KS = k + S source
 // rows: its k routed slots (weight w, absent when the expert is not local)
 // followed by its S shared-expert rows (weight 1, present for tokens of rank
 // 0).  They are summed in that order in fp32.  A source row is O (bf16).  KS
@@ -452,7 +486,10 @@ struct TileRef {
   int q, ph, seg, mt, nt, ks, rows;
 };
 
-// tile code: stage << 24 | class << 21 | index in the class queue
+// tile code: stage << 24 | class << 21 | index in the class queue.  A class
+// queue holds its stage's tiles by readiness level, then segment, then slab,
+// then row tile: the first claims go to the row tiles whose inputs are
+// complete first, and the tiles of one level share their weight slabs.
 __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S, int code) {
   const int stage = code >> 24, x = (code >> 21) & (NXCD - 1);
   int i = code & ((1 << 21) - 1);
@@ -460,17 +497,24 @@ __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S,
   r.q = stage >> 1;
   r.ph = stage & 1;
   const int nsx = class_slabs(phase_slabs(a, r.ph), x);
-  int seg = 0, nmt = 1, rows = 0;
+  const int* cum = S.lvl[r.q];
+  int L = 0;
+  while (L < NLVL && i >= nsx * cum[L]) ++L;
+  if (L > 0) i -= nsx * cum[L - 1];
+  int seg = 0, rows = 0, c = 1, lo = 0;
   for (; seg < S.nseg; ++seg) {
     rows = S.rows[r.q * S.nseg + seg];
-    nmt = ceil_div(rows, BM);
-    const int c = nsx * nmt;
-    if (i < c) break;
-    i -= c;
+    const bool sh = seg >= a.El;
+    c = level_tiles(rows, sh, L);
+    if (i < nsx * c) {
+      lo = level_lo(rows, sh, L);
+      break;
+    }
+    i -= nsx * c;
   }
   r.seg = seg;
-  r.mt = i % nmt;
-  const int slab = x + NXCD * (i / nmt);
+  r.mt = lo + i % c;
+  const int slab = x + NXCD * (i / c);
   if (r.ph == 0) {
     r.nt = slab;
     r.ks = 0;
@@ -803,7 +847,7 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
   return __builtin_amdgcn_readfirstlane(ok) != 0;
 }
 
-// Combine units (CT tokens, in token and hence chunk order) are claimed per
+// Combine units (ct tokens, in token and hence chunk order) are claimed per
 // wavefront from the sharded combine queue until every unit is claimed; each
 // waits only for the row tiles its tokens' rows come from, so the combine of
 // finished tokens starts while the last GEMM tiles run.
@@ -813,8 +857,8 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
     const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
     if (u < 0) return true;
     const uint64_t t0 = a.trace ? now_ticks() : 0;
-    const int g0 = u * CT;
-    if (!combine_tokens(a, &S, W, g0, min(CT, a.T - g0))) return false;
+    const int g0 = u * a.ct;
+    if (!combine_tokens(a, &S, W, g0, min(a.ct, a.T - g0))) return false;
     if (a.trace && lane_id() == 0) trace_rec(a, 4, ticket, u | ((long long)wave_id() << 24), t0, t0, now_ticks());
   }
 }
@@ -911,10 +955,10 @@ __global__ void __launch_bounds__(FNTH, 1) serial_gemm1_kernel(FwdArgs a) { seri
 
 __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   __shared__ Scratch W;
-  const int n = ceil_div(a.T, CT);
+  const int n = ceil_div(a.T, a.ct);
   for (int u = blockIdx.x * NWF + wave_id(); u < n; u += gridDim.x * NWF) {
-    const int g0 = u * CT;
-    combine_tokens(a, nullptr, W, g0, min(CT, a.T - g0));
+    const int g0 = u * a.ct;
+    combine_tokens(a, nullptr, W, g0, min(a.ct, a.T - g0));
   }
 }
 

@@ -70,6 +70,7 @@ struct FwdArgs {
   int T, Tr, R, H, F, k, El, S, e0, N;
   int nt0, nt1;   // column tiles of GEMM0 (over 2F) and GEMM1 (over H)
   int nsplit;     // split-K factor of GEMM1 (1, 2, 4 or 8)
+  int dt, ct;     // tokens per dispatch unit (<= DT) and per combine unit (<= CT)
   int xmax;       // rows reserved for routed pairs in A / Hbuf / O
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
