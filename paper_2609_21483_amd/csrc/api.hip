@@ -285,6 +285,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.plan_out = at<moe_plan>(h, h->lay.plan);
   a.calib = at<DevCalib>(h, h->off_calib);
   a.mode = mode;
+  a.move_steal = mode == MOE_MODE_DYNAMIC ? 1 : 0;
   a.forced = forced ? 1 : 0;
   if (forced) a.fplan = *forced;
   a.timeout_ticks = h->timeout_ticks;

@@ -105,6 +105,19 @@ __device__ __forceinline__ int level_tiles(int rows, bool shared, int L) {
   return tiles_upto(rows, L) - tiles_upto(rows, L - 1);
 }
 
+// Queue order of the stages (chunk, phase) of a K-chunk schedule, skewed by
+// one chunk: (0,G0), (1,G0), (0,G1), (2,G0), (1,G1), ..., (K-1,G0), (K-2,G1),
+// (K-1,G1).  Workers reach chunk q's GEMM1 tiles only after claiming chunk
+// q+1's GEMM0 tiles, which depend on dispatch alone, so chunk q's last GEMM0
+// tiles finish while those run instead of holding up a worker at every chunk
+// boundary.  Returns chunk << 1 | phase.
+__device__ __forceinline__ int stage_qph(int s, int K) {
+  if (s == 0) return 0;
+  if (s >= 2 * K - 1) return ((K - 1) << 1) | 1;
+  const int j = (s + 1) >> 1;
+  return (s & 1) ? (j << 1) : (((j - 1) << 1) | 1);
+}
+
 __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
   const int tid = threadIdx.x;
   const int ki = kopt_index(K);
@@ -147,8 +160,8 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
   if (tid == 0) S.gstart[S.G] = 0;
   __syncthreads();
   for (int v = tid; v < 2 * K * NXCD; v += FNTH) {
-    const int stage = v / NXCD, x = v % NXCD, q = stage >> 1;
-    const int nsx = class_slabs(phase_slabs(a, stage & 1), x);
+    const int stage = v / NXCD, x = v % NXCD, qp = stage_qph(stage, K), q = qp >> 1;
+    const int nsx = class_slabs(phase_slabs(a, qp & 1), x);
     int n = 0;
     for (int seg = 0; seg < nseg; ++seg) n += nsx * ceil_div(S.rows[q * nseg + seg], BM);
     S.ncls[stage][x] = n;
@@ -233,7 +246,7 @@ __device__ __forceinline__ int lane_here() {
 }
 
 template <bool SIG>
-__device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, Scratch& W, int u, int cur) {
+__device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int u, int cur) {
   using gemm::opaque;
   constexpr int VB = 32;  // 16-byte vectors per lane in flight
   const int lane = lane_here();
@@ -248,7 +261,6 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
   const int dt = opaque(a.dt);
   const int g0 = u * dt;
   const int nt = min(dt, T - g0);
-  const uint64_t tr0 = (SIG && a.trace) ? now_ticks() : 0;
   sl[lane] = cur;
   // tokens with at least one local slot, compacted in token order
   const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)xmax);
@@ -295,30 +307,48 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
     }
   }
   __builtin_amdgcn_s_waitcnt(0);
-  const uint64_t tr1 = (SIG && a.trace) ? now_ticks() : 0;
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Readiness accounting of a copied unit whose rows have reached the coherence
+// point (needs the schedule): each row tile the unit wrote rows of gains
+// that many rows, one counter update per distinct row tile.
+__device__ __forceinline__ void dispatch_count(const FwdArgs& a, const Sched* S, int u, int cur) {
+  using gemm::opaque;
+  const int lane = lane_here();
+  const int k = opaque(a.k);
+  const int T = opaque(a.T);
+  const int xmax = opaque(a.xmax);
+  const int g0 = u * opaque(a.dt);
+  int id = -1;
+  if ((unsigned)cur < (unsigned)xmax) {
+    const int g = g0 + lane / k;
+    const int le = a.topk_idx[(size_t)g * k + (lane % k)] - a.e0;
+    if ((unsigned)le < (unsigned)a.El) {
+      const int q = (int)(((long long)g * S->K) / T);
+      id = S->mb[q * S->nseg + le] + (cur - S->row0[q * S->nseg + le]) / BM;
+      if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
+    }
+  }
+  uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
+  while (pending) {
+    const int leader = __builtin_ctzll(pending);
+    const int tile = __builtin_amdgcn_readlane(id, leader);
+    const uint64_t same = __builtin_amdgcn_ballot_w64(id == tile);
+    if (lane == leader) fetch_add_relaxed(&a.ctl[CTL_READY + tile * CTL_PAD], (int)__builtin_popcountll(same));
+    pending &= ~same;
+  }
+}
+
+// A whole unit: copy, then (megakernel) count.
+template <bool SIG>
+__device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, Scratch& W, int u, int cur) {
+  const uint64_t tr0 = (SIG && a.trace) ? now_ticks() : 0;
+  dispatch_copy<SIG>(a, W, u, cur);
   if constexpr (SIG) {
-    // this wavefront's rows have reached the coherence point: count them in
-    // the readiness counters of their row tiles
-    int id = -1;
-    if ((unsigned)cur < (unsigned)xmax) {
-      const int g = g0 + lane / k;
-      const int le = a.topk_idx[(size_t)g * k + (lane % k)] - a.e0;
-      if ((unsigned)le < (unsigned)a.El) {
-        const int q = (int)(((long long)g * S->K) / T);
-        id = S->mb[q * S->nseg + le] + (cur - S->row0[q * S->nseg + le]) / BM;
-        if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
-      }
-    }
-    // one counter update per distinct row tile of this unit
-    uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
-    while (pending) {
-      const int leader = __builtin_ctzll(pending);
-      const int tile = __builtin_amdgcn_readlane(id, leader);
-      const uint64_t same = __builtin_amdgcn_ballot_w64(id == tile);
-      if (lane == leader) fetch_add_relaxed(&a.ctl[CTL_READY + tile * CTL_PAD], (int)__builtin_popcountll(same));
-      pending &= ~same;
-    }
-    if (a.trace && lane == 0) trace_rec(a, 5, 0, u | ((long long)wv << 24), tr0, tr1, now_ticks());
+    const uint64_t tr1 = a.trace ? now_ticks() : 0;
+    dispatch_count(a, S, u, cur);
+    if (a.trace && lane_id() == 0) trace_rec(a, 5, 0, u | ((long long)wave_id() << 24), tr0, tr1, now_ticks());
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -494,8 +524,9 @@ __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S,
   const int stage = code >> 24, x = (code >> 21) & (NXCD - 1);
   int i = code & ((1 << 21) - 1);
   TileRef r;
-  r.q = stage >> 1;
-  r.ph = stage & 1;
+  const int qp = stage_qph(stage, S.K);
+  r.q = qp >> 1;
+  r.ph = qp & 1;
   const int nsx = class_slabs(phase_slabs(a, r.ph), x);
   const int* cum = S.lvl[r.q];
   int L = 0;
@@ -535,7 +566,7 @@ __device__ __forceinline__ TileRef decode_tile(const FwdArgs& a, const Sched& S,
 __device__ __forceinline__ int claim_tile(const FwdArgs& a, const Sched& S, int base, int ph_only, int home,
                                           int& stage, uint32_t& exhausted) {
   for (; stage < 2 * S.K; ++stage, exhausted = 0u) {
-    if (ph_only >= 0 && (stage & 1) != ph_only) continue;
+    if (ph_only >= 0 && (stage_qph(stage, S.K) & 1) != ph_only) continue;
     for (int j = 0; j < NXCD; ++j) {
       const int x = (home + j) & (NXCD - 1);
       const int n = S.ncls[stage][x];
@@ -770,7 +801,7 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
   for (;;) {
     if (threadIdx.x == 0) {
       int st = ld_relaxed(p) >= target ? 1 : 0;
-      if (!st && W.dexh) st = poll_geq(a, p, target) ? 1 : -1;
+      if (!st && (W.dexh || !a.move_steal)) st = poll_geq(a, p, target) ? 1 : -1;
       else if (!st && (ld_relaxed(&a.ctl[CTL_ABORT]) || now_ticks() > deadline)) {
         st_relaxed(&a.ctl[CTL_ABORT], 1);
         atomicOr(a.err, ERR_TIMEOUT);

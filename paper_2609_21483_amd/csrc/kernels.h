@@ -71,6 +71,8 @@ struct FwdArgs {
   int nt0, nt1;   // column tiles of GEMM0 (over 2F) and GEMM1 (over H)
   int nsplit;     // split-K factor of GEMM1 (1, 2, 4 or 8)
   int dt, ct;     // tokens per dispatch unit (<= DT) and per combine unit (<= CT)
+  int move_steal; // compute workers copy dispatch units while their rows are not
+                  // ready (dynamic mode; the static split keeps its roles fixed)
   int xmax;       // rows reserved for routed pairs in A / Hbuf / O
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
