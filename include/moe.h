@@ -90,7 +90,13 @@ typedef struct {
  * through the movement workers.  bw_all_bytes_per_s is the rate of all N
  * workers moving together: the last chunk's combine runs on every worker
  * (section 4), so the exposed tail of Eq 6/10 moves at that rate; 0 takes the
- * printed BW(c) instead. */
+ * printed BW(c) instead.  head_on_all = 1 (the default) is the window of
+ * Eq 11 under movement stealing: compute workers whose GEMM0 rows are not
+ * dispatched yet copy rows themselves, so the first chunk's dispatch runs on
+ * all N workers before any GEMM tile starts, and the movement workers' own
+ * work while the GEMMs run is the dispatch of chunks 1..K-1 and the combine
+ * of chunks 0..K-2, (W_dispatch + W_combine)(K-1)/K; 0 keeps the whole
+ * dispatch in that window, W_dispatch + W_combine (K-1)/K. */
 typedef struct {
   int32_t n_c;
   int32_t c[MOE_CALIB_MAX_C];            /* ascending, 1 <= c < N */
@@ -103,6 +109,7 @@ typedef struct {
   int32_t literal_volumes;
   int32_t static_c;                      /* split used by MOE_MODE_STATIC */
   double bw_all_bytes_per_s;             /* >= 0; 0: tail at BW(c) */
+  int32_t head_on_all;                   /* 0 or 1 */
 } moe_calib;
 
 /* Execution plan (section 3.3): the split, the chunk count and the steal count. */

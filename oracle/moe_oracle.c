@@ -225,11 +225,14 @@ void orc_plan(const orc_plan_in* in, orc_plan_out* out) {
   out->K = in->K[bk];
   out->t_total = best;
   /* bubble stealing at (c*, K*).  Eq 11's communication is what the movement
-   * workers still have to do while the GEMMs run: dispatch and the combine of
-   * chunks 0..K-2; the last chunk's combine runs on all N workers after the
-   * GEMMs (section 4), so it is not part of this window. */
+   * workers still have to do while the GEMMs run: the combine of chunks
+   * 0..K-2 (the last chunk's combine runs on all N workers after the GEMMs,
+   * section 4) and the dispatch, without the first chunk's when every worker
+   * dispatches it before any GEMM tile can start. */
   double kd = (double)in->K[bk];
-  double t_comm = (in->w_dispatch + (in->w_combine * (kd - 1.0)) / kd) / in->bw[bc];  /* Eq 11 */
+  double w_win = in->head_on_all ? ((in->w_dispatch + in->w_combine) * (kd - 1.0)) / kd
+                                 : in->w_dispatch + (in->w_combine * (kd - 1.0)) / kd;
+  double t_comm = w_win / in->bw[bc];                                  /* Eq 11 */
   double w_partial = t_comm * in->flops[bc];                           /* Eq 12 */
   double w_steal = in->w_comp - w_partial;                             /* Eq 13 */
   if (w_steal < 0.0) w_steal = 0.0;
@@ -237,7 +240,9 @@ void orc_plan(const orc_plan_in* in, orc_plan_out* out) {
   int n_steal = 0;
   if (nt > 0 && in->w_comp > 0.0) {
     double w_tile = in->w_comp / (double)nt;
-    n_steal = (int)floor(w_steal / ((double)in->N * w_tile));          /* Eq 14 */
+    /* Eq 14 gives a share, not a count: a movement worker claims up to the
+     * share rounded up (claims stop anyway once the queue is empty) */
+    n_steal = (int)ceil(w_steal / ((double)in->N * w_tile));           /* Eq 14 */
   }
   out->n_steal = n_steal;
 }

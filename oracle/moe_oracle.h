@@ -120,6 +120,11 @@ typedef struct {
    * runs on every worker (section 4), so when bw_all > 0 the exposed tail of
    * Eq 6/10 moves at bw_all, else at BW(c) as printed */
   double bw_all;
+  /* nonzero: the first chunk's dispatch runs on all N workers before any GEMM
+   * tile starts (compute workers copy rows they are waiting for), so the
+   * window of Eq 11 holds (W_dispatch + W_combine)(K-1)/K; zero: the whole
+   * dispatch plus the combine of chunks 0..K-2 */
+  int head_on_all;
 } orc_plan_in;
 
 typedef struct {

@@ -39,7 +39,8 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
+        srcs = [os.path.join(HERE, f) for f in ("moe_oracle.c", "moe_oracle.h")]
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < max(os.path.getmtime(f) for f in srcs):
             build()
         L = C.CDLL(LIB)
         P = C.c_void_p
@@ -184,7 +185,7 @@ class PlanIn(C.Structure):
         ("n_k", C.c_int), ("K", C.c_void_p), ("eff", C.c_void_p), ("alpha", C.c_double),
         ("N", C.c_int),
         ("w_comp", C.c_double), ("w_dispatch", C.c_double), ("w_combine", C.c_double),
-        ("n_tiles", C.c_void_p), ("bw_all", C.c_double),
+        ("n_tiles", C.c_void_p), ("bw_all", C.c_double), ("head_on_all", C.c_int),
     ]
 
 
@@ -204,7 +205,8 @@ class Plan:
 
 
 class _PlanArgs:
-    def __init__(self, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0):
+    def __init__(self, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0,
+                 head_on_all=0):
         self.c = _c(c, np.int32)
         self.bw = _c(bw, np.float64)
         self.flops = _c(flops, np.float64)
@@ -215,18 +217,19 @@ class _PlanArgs:
         assert self.K.shape == self.eff.shape == self.n_tiles.shape
         self.s = PlanIn(len(self.c), _p(self.c), _p(self.bw), _p(self.flops), len(self.K), _p(self.K),
                         _p(self.eff), float(alpha), int(N), float(w_comp), float(w_dispatch),
-                        float(w_combine), _p(self.n_tiles), float(bw_all))
+                        float(w_combine), _p(self.n_tiles), float(bw_all), int(head_on_all))
 
 
-def plan(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0) -> Plan:
-    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all)
+def plan(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0, head_on_all=0) -> Plan:
+    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all, head_on_all)
     o = PlanOut()
     lib().orc_plan(C.byref(a.s), C.byref(o))
     return Plan(o.c, o.K, o.n_steal, o.ci, o.ki, o.t_total)
 
 
-def t_total(ci, ki, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0) -> float:
-    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all)
+def t_total(ci, ki, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0,
+            head_on_all=0) -> float:
+    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all, head_on_all)
     return lib().orc_t_total(C.byref(a.s), int(ci), int(ki))
 
 

@@ -49,7 +49,7 @@ class moe_calib(C.Structure):
         ("bw_bytes_per_s", C.c_double * CALIB_MAX_C), ("comp_flop_per_s", C.c_double * CALIB_MAX_C),
         ("n_k", C.c_int32), ("k_chunks", C.c_int32 * CALIB_MAX_K), ("eff_chunk", C.c_double * CALIB_MAX_K),
         ("alpha", C.c_double), ("literal_volumes", C.c_int32), ("static_c", C.c_int32),
-        ("bw_all_bytes_per_s", C.c_double),
+        ("bw_all_bytes_per_s", C.c_double), ("head_on_all", C.c_int32),
     ]
 
 
@@ -277,7 +277,8 @@ def make_config(shape, n_workers: int = 0, first_local_expert: int = 0, gemm1_sp
                       gemm1_split)
 
 
-def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int = 0, bw_all: float = 0.0) -> moe_calib:
+def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int = 0, bw_all: float = 0.0,
+               head_on_all: int = 1) -> moe_calib:
     k = moe_calib()
     k.n_c = len(c)
     for i, (cv, b, f) in enumerate(zip(c, bw, flops)):
@@ -289,6 +290,7 @@ def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int =
     k.literal_volumes = int(literal)
     k.static_c = int(static_c)
     k.bw_all_bytes_per_s = float(bw_all)
+    k.head_on_all = int(head_on_all)
     return k
 
 

@@ -9,11 +9,16 @@ For a workload share (layer 0, its own routing):
                   separate kernels on c workgroups (the volumes the cost model
                   uses, Eq 2-3 as counted on one GPU);
   TFLOPS(N - c) = W_comp / time of GEMM0 + GEMM1 on N - c workgroups (Eq 1);
-  eff_chunk(K)  = GEMM time at K = 1 / GEMM time with the tiling of K chunks;
   BW(N)         = the same movement on all N workgroups (the final combine
                   runs on every worker, section 4);
-  alpha         = least-squares fit of Eq 15 to the megakernel's time over a
-                  (c, K) grid of forced plans.
+  eff_chunk(K)  = the megakernel's best time over c at K = 1 / its best time
+                  over c at K, on a (c, K) grid of forced plans whose movement
+                  workers steal GEMM tiles freely: the throughput the chunk
+                  pipeline keeps in the megakernel itself, where chunk
+                  boundaries add dependency waits and ragged row tiles that
+                  GEMM-only runs do not show (their ratio, GEMM time at K = 1 /
+                  GEMM time with the tiling of K chunks, is kept as eff_gemm);
+  alpha         = least-squares fit of Eq 15 to the same grid.
 The table is written to calib/<workload>.json and loaded by bench.py.
 """
 from __future__ import annotations
@@ -47,7 +52,7 @@ def load_calib(workload: str, N: int):
     if int(d.get("N", -1)) != N:
         return None
     return B.make_calib(d["c"], d["bw"], d["flops"], d["K"], d["eff"], d["alpha"], d["static_c"], d.get("literal", 0),
-                        d.get("bw_all", 0.0))
+                        d.get("bw_all", 0.0), d.get("head_on_all", 1))
 
 
 def _time(fn, reps: int) -> float:
@@ -102,17 +107,22 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
         log(f"[calib] all {N} workers: BW {bw_all / 1e9:8.1f} GB/s")
         Ks = [1, 2, 4, 8]
         t_k = [_time(lambda: run(2 | 4, N, K), reps) for K in Ks]
-        eff = [min(1.0, t_k[0] / t) for t in t_k]
-        log(f"[calib] eff_chunk {dict(zip(Ks, [round(e, 3) for e in eff]))}")
+        eff_gemm = [min(1.0, t_k[0] / t) for t in t_k]
+        log(f"[calib] GEMM-only chunk efficiency {dict(zip(Ks, [round(e, 3) for e in eff_gemm]))}")
 
-        # alpha: Eq 15 against the megakernel over a (c, K) grid
+        # the megakernel over a (c, K) grid of forced plans, movement workers
+        # stealing GEMM tiles freely after dispatch
+        steal_all = 1 << 20
         sweep = []
         for c in c_grid[:: max(1, len(c_grid) // 6)]:
             for K in Ks:
-                p = B.moe_plan(c, K, 0, 1, 0.0)
+                p = B.moe_plan(c, K, steal_all, 1, 0.0)
                 t = _time(lambda: layer.forward(xd, idx, w, y, "dynamic", forced=p), reps)
                 sweep.append((c_grid.index(c), Ks.index(K), t))
         assert B.moe_sync_status(layer.h) == B.MOE_OK, B.moe_last_error()
+        best_k = [min(t for _, ki, t in sweep if ki == j) for j in range(len(Ks))]
+        eff = [min(1.0, best_k[0] / t) for t in best_k]
+        log(f"[calib] eff_chunk {dict(zip(Ks, [round(e, 3) for e in eff]))}")
 
         def predict(alpha, ci, ki):
             t_comp = w_comp / (fl[ci] * eff[ki])
@@ -129,7 +139,8 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
         static_c = max(1, min(N - 1, int(round(N * 20 / 132 / 8)) * 8))
         return {
             "workload": workload, "N": N, "c": c_grid, "bw": bw, "flops": fl, "K": Ks, "eff": eff,
-            "alpha": alpha, "static_c": static_c, "literal": 0, "bw_all": bw_all,
+            "alpha": alpha, "static_c": static_c, "literal": 0, "bw_all": bw_all, "head_on_all": 1,
+            "eff_gemm": eff_gemm,
             "sweep": [[c_grid[ci], Ks[ki], t] for ci, ki, t in sweep],
             "device": torch.cuda.get_device_name(0), "date": time.strftime("%Y-%m-%d"),
         }

@@ -63,6 +63,7 @@ struct DevCalib {
   int32_t literal;
   int32_t static_c;
   double bw_all;  // > 0: the exposed tail moves at this rate (all N workers)
+  int32_t head_on_all;  // the first chunk's dispatch is outside the Eq 11 window
 };
 
 struct FwdArgs {
@@ -143,10 +144,12 @@ __host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_c
       if (t < best) { best = t; bc = ci; bk = ki; }
     }
   // Eq 11 over the window the movement workers have while the GEMMs run:
-  // dispatch and the combine of chunks 0..K-2 (the last chunk's combine runs
-  // on all N workers afterwards)
+  // the combine of chunks 0..K-2 (the last chunk's combine runs on all N
+  // workers afterwards) and the dispatch, less the first chunk's when all
+  // workers dispatch it before any GEMM tile starts (movement stealing)
   double kd = (double)cb.kk[bk];
-  double t_comm = (w_disp + (w_comb * (kd - 1.0)) / kd) / cb.bw[bc];  // Eq 11
+  double w_win = cb.head_on_all ? ((w_disp + w_comb) * (kd - 1.0)) / kd : w_disp + (w_comb * (kd - 1.0)) / kd;
+  double t_comm = w_win / cb.bw[bc];                         // Eq 11
   double w_partial = t_comm * cb.fl[bc];                     // Eq 12
   double w_steal = w_comp - w_partial;                       // Eq 13
   if (w_steal < 0.0) w_steal = 0.0;
@@ -154,7 +157,9 @@ __host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_c
   int n_steal = 0;
   if (nt > 0 && w_comp > 0.0) {
     double w_tile = w_comp / (double)nt;
-    n_steal = (int)floor(w_steal / ((double)N * w_tile));   // Eq 14
+    // Eq 14 gives a share, not a count: a movement worker claims up to the
+    // share rounded up (claims stop anyway once the queue is empty)
+    n_steal = (int)ceil(w_steal / ((double)N * w_tile));    // Eq 14
   }
   out->c = cb.c[bc];
   out->K = cb.kk[bk];

@@ -57,7 +57,8 @@ def test_init_rejects_bad_calib():
     h = B.moe_init(c, B.make_calib(**good))
     B.moe_destroy(h)
     for bad in [dict(c=[16, 8]), dict(c=[8, 256]), dict(bw=[0.0, 1.0]), dict(K=[1, 3]), dict(eff=[1.0, 1.5]),
-                dict(alpha=2.0), dict(static_c=0), dict(bw_all=-1.0), dict(bw_all=float("inf"))]:
+                dict(alpha=2.0), dict(static_c=0), dict(bw_all=-1.0), dict(bw_all=float("inf")),
+                dict(head_on_all=2), dict(head_on_all=-1)]:
         kw = {**good, **bad}
         with pytest.raises(B.MoeError):
             B.moe_init(c, B.make_calib(**kw))
@@ -129,9 +130,11 @@ def test_host_cost_model_matches_oracle(orc):
             wc, wd, wb = float(rng.uniform(0, 1e13)), float(rng.uniform(0, 2e9)), float(rng.uniform(0, 2e9))
             nt = rng.integers(0, 5000, len(Ks))
             bw_all = 0.0 if trial % 3 == 0 else float(rng.uniform(1e11, 8e12))
-            B.moe_set_calib(h, B.make_calib(cs, bw, fl, Ks, eff, alpha, static_c=int(cs[0]), bw_all=bw_all))
+            head = trial % 2
+            B.moe_set_calib(h, B.make_calib(cs, bw, fl, Ks, eff, alpha, static_c=int(cs[0]), bw_all=bw_all,
+                                            head_on_all=head))
             p = B.moe_plan_host(h, wc, wd, wb, list(nt) + [0] * (4 - len(Ks)))
-            o = orc.plan(cs, bw, fl, Ks, eff, alpha, 256, wc, wd, wb, nt, bw_all=bw_all)
+            o = orc.plan(cs, bw, fl, Ks, eff, alpha, 256, wc, wd, wb, nt, bw_all=bw_all, head_on_all=head)
             assert (p.c, p.K, p.n_steal) == (o.c, o.K, o.n_steal), trial
             assert p.t_pred_s == o.t_total, trial
     finally:

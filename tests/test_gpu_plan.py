@@ -39,7 +39,8 @@ def oracle_plan(B, h, shape, idx):
     n = cal.n_c
     return O.plan([cal.c[i] for i in range(n)], [cal.bw_bytes_per_s[i] for i in range(n)],
                   [cal.comp_flop_per_s[i] for i in range(n)], Ks, [cal.eff_chunk[j] for j in range(cal.n_k)],
-                  cal.alpha, n_workers(), wc, wd, wb, n_tiles, bw_all=cal.bw_all_bytes_per_s)
+                  cal.alpha, n_workers(), wc, wd, wb, n_tiles, bw_all=cal.bw_all_bytes_per_s,
+                  head_on_all=cal.head_on_all)
 
 
 def n_workers():
@@ -47,17 +48,18 @@ def n_workers():
     return torch.cuda.get_device_properties(0).multi_processor_count
 
 
-@pytest.mark.parametrize("name,literal", [("tiny", 0), ("fine_zipf", 0), ("fine_zipf", 1), ("shared_routed", 0)])
-def test_prologue_plan_matches_oracle(B, name, literal):
+@pytest.mark.parametrize("name,literal,head", [("tiny", 0, 1), ("fine_zipf", 0, 1), ("fine_zipf", 1, 1),
+                                               ("fine_zipf", 0, 0), ("shared_routed", 0, 1)])
+def test_prologue_plan_matches_oracle(B, name, literal, head):
     shape = W.WORKLOADS[name]
     c = make_case(shape)
     idx, w = c.oracle_route()
     layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
     try:
-        if literal:
-            cal = B.moe_get_calib(layer.h)
-            cal.literal_volumes = 1
-            B.moe_set_calib(layer.h, cal)
+        cal = B.moe_get_calib(layer.h)
+        cal.literal_volumes = literal
+        cal.head_on_all = head
+        B.moe_set_calib(layer.h, cal)
         x = c.x.cuda()
         idx_d = torch.from_numpy(idx).cuda()
         w_d = torch.from_numpy(w.astype(np.float32)).cuda()

@@ -353,7 +353,7 @@ def test_cost_model_hand_example_all_worker_tail(orc):
     combine on every worker): Eq 10 becomes 0.5 * 2^34 / (2^36 K) = 1/(8K) s.
     c=16: K=1 max(4 + 1/8, 1.5) = 4.125; K=2 4/0.75 + 1/16 = 259/48; K=4 8 + 1/32.
     c=32: 6.125; 8.0625; 12.03125.  c=8, K=1: 192/56 + 1/8 = 199/56 (minimum).
-    n_steal (Eq 11-14) does not use the tail: 0 and 544 as before."""
+    n_steal (Eq 11-14) does not use the tail: 1 and 544 as before."""
     d = json.load(open(os.path.join(GOLDEN, "cost_model_hand_example.json")))
     args = dict(c=d["c"], bw=d["bw"], flops=d["flops"], K=d["K"], eff=d["eff"], alpha=d["alpha"],
                 N=d["N"], w_comp=d["w_comp"], w_dispatch=d["w_dispatch"], w_combine=d["w_combine"],
@@ -429,13 +429,32 @@ def test_n_steal_formula_by_hand(orc):
     # Eq 11 counts dispatch plus the combine of chunks 0..K-2 (the last chunk's
     # combine runs on every worker after the GEMMs).
     # K = 1: t_comm = 1e9/1e12 = 1 ms; W_partial = 1e-3 * 5e14 = 5e11; W_steal = 4e12 - 5e11 = 3.5e12;
-    # W_tile = 4e12/4000 = 1e9; n_steal = floor(3.5e12 / (100 * 1e9)) = 35
+    # W_tile = 4e12/4000 = 1e9; n_steal = ceil(3.5e12 / (100 * 1e9)) = 35
     p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
     assert p.n_steal == 35
     # K = 2: t_comm = (1e9 + 1e9/2)/1e12 = 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12;
-    # n_steal = floor(3.25e12 / (100 * 1e9)) = 32
+    # n_steal = ceil(3.25e12 / (100 * 1e9)) = ceil(32.5) = 33
     p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
-    assert p.n_steal == 32
+    assert p.n_steal == 33
+
+
+def test_n_steal_formula_by_hand_head_on_all(orc):
+    # With every worker dispatching the first chunk before any GEMM tile can
+    # start, Eq 11's window is (W_dispatch + W_combine)(K-1)/K.
+    # K = 1: empty window; W_steal = W_comp = 4e12; n_steal = ceil(4e12 / (100 * 1e9)) = 40
+    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    assert p.n_steal == 40
+    # K = 2: window 2e9 / 2 = 1e9 bytes -> 1 ms; W_partial = 5e11; W_steal = 3.5e12; n_steal = 35
+    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    assert p.n_steal == 35
+    # K = 4: window 2e9 * 3/4 = 1.5e9 bytes -> 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12; n_steal = 33
+    p = orc.plan([20], [1e12], [5e14], [4], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    assert p.n_steal == 33
+    # the window does not enter T_total (Eq 15): same plan and prediction either way
+    a = orc.plan([8, 16], [1e11, 2e11], [1e15, 9e14], [1, 2], [1.0, 0.9], 0.5, 64, 1e12, 2e8, 2e8, [1000, 1100])
+    b = orc.plan([8, 16], [1e11, 2e11], [1e15, 9e14], [1, 2], [1.0, 0.9], 0.5, 64, 1e12, 2e8, 2e8, [1000, 1100],
+                 head_on_all=1)
+    assert (a.c, a.K, a.t_total) == (b.c, b.K, b.t_total)
 
 
 def test_tile_count_bruteforce(orc):
