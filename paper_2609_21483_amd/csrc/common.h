@@ -26,7 +26,7 @@ constexpr int MAX_EL = 64;      // local experts
 constexpr int MAX_S = 8;        // shared experts
 constexpr int MAX_SEG = MAX_EL + MAX_S;
 constexpr int MAX_K = 8;        // chunk count limit
-constexpr int NLVL = 16;       // readiness levels of the row tiles of a stage
+constexpr int NLVL = 1;        // readiness levels of the routed row tiles of a stage
 constexpr int MAX_TOPK = 8;
 constexpr int MAX_E = 512;
 constexpr int KOPT = 4;         // chunk options with stored offsets: K = 1, 2, 4, 8

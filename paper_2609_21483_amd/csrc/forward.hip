@@ -90,7 +90,13 @@ __device__ __forceinline__ int class_slabs(int ns, int x) { return ns > x ? (ns 
 // tile mt of a segment of `rows` rows is complete once the fraction
 // min((mt + 1) * BM, rows) / rows of the segment is written; its level is
 // that fraction rounded up to a multiple of 1/NLVL (1..NLVL).  Shared-expert
-// rows are read straight from x: level 0, ready at launch.
+// rows are read straight from x: level 0, ready at launch.  With every
+// worker copying rows at the start, the routed row tiles all complete at
+// nearly the same time, and one routed level (NLVL = 1) measures fastest:
+// it keeps the row tiles of one expert and weight slab together, so the
+// tiles running on an XCD share that slab in its L2 (finer levels spread the
+// first claims over every expert and slab and fetch the weights several
+// times over).
 __device__ __forceinline__ int tiles_upto(int rows, int L) {  // routed tiles at level <= L
   const int nmt = (rows + BM - 1) / BM;
   if (L <= 0) return 0;
