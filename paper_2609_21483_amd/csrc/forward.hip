@@ -46,6 +46,8 @@ struct Sched {
 struct Scratch {
   int bc[8];
   long long ntk[KOPT];
+  DevCalib cal;                                        // the calibration table, staged by the prologue
+  double tt[MOE_CALIB_MAX_C * MOE_CALIB_MAX_K];        // T_total of each (c, K) grid point
   int part[NWF];
   int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
   int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
@@ -124,7 +126,8 @@ __device__ __forceinline__ int stage_qph(int s, int K) {
   return (s & 1) ? (j << 1) : (((j - 1) << 1) | 1);
 }
 
-__device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch& W, int K) {
+// sub: the chunk sub-offset tables (a.sub_off, or a copy of them in LDS)
+__device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, Sched& S, Scratch& W, int K) {
   const int tid = threadIdx.x;
   const int ki = kopt_index(K);
   const int nseg = a.El + a.S;
@@ -142,7 +145,7 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, Sched& S, Scratch&
     int q = v / nseg, seg = v % nseg;
     int rows, row0, arow0;
     if (seg < a.El) {
-      const int* so = a.sub_off + ((size_t)ki * a.El + seg) * SUBW;
+      const int* so = sub + ((size_t)ki * a.El + seg) * SUBW;
       row0 = so[q];
       rows = so[q + 1] - so[q];
       arow0 = row0;
@@ -705,10 +708,17 @@ __device__ __forceinline__ bool arrive_and_reduce(const FwdArgs& a, const Sched&
 // Prologue: the routing-derived workload and the plan (sections 3.1-3.3),
 // computed redundantly by every workgroup from a small read of the stats.
 // ===========================================================================
-__device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
+// sub: the chunk sub-offset tables staged in LDS (see moe_megakernel); the
+// calibration table is staged here, in the same round trip.
+__device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, Sched& S, Scratch& W) {
   const int tid = threadIdx.x;
   const int nseg = a.El + a.S;
   if (tid < KOPT) W.ntk[tid] = 0;
+  {
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(a.calib);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(&W.cal);
+    for (int i = tid; i < (int)(sizeof(DevCalib) / 4); i += FNTH) dst[i] = src[i];
+  }
   __syncthreads();
   // GEMM tiles at each stored chunk option (for W_tile of Eq 14)
   for (int ki = 0; ki < KOPT; ++ki) {
@@ -718,7 +728,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
       int q = v / nseg, seg = v % nseg;
       int rows;
       if (seg < a.El) {
-        const int* so = a.sub_off + ((size_t)ki * a.El + seg) * SUBW;
+        const int* so = sub + ((size_t)ki * a.El + seg) * SUBW;
         rows = so[q + 1] - so[q];
       } else {
         int t0 = (int)(((long long)q * a.T + K - 1) / K);
@@ -730,22 +740,35 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
     if (part) atomicAdd((unsigned long long*)&W.ntk[ki], (unsigned long long)part);
   }
   __syncthreads();
+  const bool model = !a.forced && a.mode != MOE_MODE_STATIC;
+  double wc = 0.0, wd = 0.0, wb = 0.0;
+  if (model && tid < WAVE) {
+    // Eq 15 at every grid point, one point per lane of the first wavefront
+    cm_volumes(a.stats, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
+    const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
+    for (int i = tid; i < npt; i += WAVE) W.tt[i] = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
+  }
+  __syncthreads();
   if (tid == 0) {
     moe_plan p;
     if (a.forced) {
       p = a.fplan;
     } else if (a.mode == MOE_MODE_STATIC) {
-      p.c = a.calib->static_c;
+      p.c = W.cal.static_c;
       p.K = 1;
       p.n_steal = 0;
       p.final_all = 0;
       p.t_pred_s = 0.0;
     } else {
-      double wc, wd, wb;
-      cm_volumes(a.stats, a.H, a.F, a.S * a.Tr, a.calib->literal, &wc, &wd, &wb);
+      // Eq 16 in the host model's order: c ascending, then K, first strict minimum
+      const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
+      int bi = 0;
+      double best = W.tt[0];
+      for (int i = 1; i < npt; ++i)
+        if (W.tt[i] < best) { best = W.tt[i]; bi = i; }
       long long nt_by_k[MOE_CALIB_MAX_K];
-      for (int j = 0; j < a.calib->n_k; ++j) nt_by_k[j] = W.ntk[kopt_index(a.calib->kk[j])];
-      cost_model(*a.calib, a.N, wc, wd, wb, nt_by_k, &p);
+      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.ntk[kopt_index(W.cal.kk[j])];
+      cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &p);
     }
     S.c = p.c;
     S.K = p.K;
@@ -914,8 +937,13 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   if (blockIdx.x == 0)
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
 
-  prologue_plan(a, S, W);
-  build_sched(a, S, W, S.K);
+  // the chunk sub-offset tables, staged in the GEMM ring (idle until the
+  // first tile) so that plan and schedule read them from LDS
+  static_assert(KOPT * MAX_EL * SUBW * (int)sizeof(int) <= gemm::RING_BYTES, "sub-offset tables fit the ring");
+  int* sub = reinterpret_cast<int*>(ring);
+  for (int i = tid; i < KOPT * a.El * SUBW; i += FNTH) sub[i] = a.sub_off[i];
+  prologue_plan(a, sub, S, W);
+  build_sched(a, sub, S, W, S.K);
 
   if (tid == 0) {
     W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
@@ -964,7 +992,7 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
-  build_sched(a, S, W, a.serial_K);
+  build_sched(a, a.sub_off, S, W, a.serial_K);
   const int home = xcd_id() & (NXCD - 1);
   int stage = 0;
   uint32_t exhausted = 0;

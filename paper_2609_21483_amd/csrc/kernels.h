@@ -132,17 +132,12 @@ __host__ __device__ inline double cm_t_total(const DevCalib& cb, int ci, int ki,
   return s > t_comm ? s : t_comm;                            // Eq 15 (Eq 7 at K = 1)
 }
 
-__host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_comp, double w_disp,
-                                           double w_comb, const long long* n_tiles_by_k,
-                                           moe_plan* out) {
+// The steal count of Eq 11-14 at the chosen (c*, K*) = grid point (bc, bk)
+// with T_total = best, and the plan.
+__host__ __device__ inline void cm_finish(const DevCalib& cb, int N, double w_comp, double w_disp, double w_comb,
+                                          const long long* n_tiles_by_k, int bc, int bk, double best,
+                                          moe_plan* out) {
 #pragma clang fp contract(off)
-  int bc = 0, bk = 0;
-  double best = cm_t_total(cb, 0, 0, w_comp, w_disp, w_comb);
-  for (int ci = 0; ci < cb.n_c; ++ci)
-    for (int ki = 0; ki < cb.n_k; ++ki) {
-      double t = cm_t_total(cb, ci, ki, w_comp, w_disp, w_comb);
-      if (t < best) { best = t; bc = ci; bk = ki; }
-    }
   // Eq 11 over the window the movement workers have while the GEMMs run:
   // the combine of chunks 0..K-2 (the last chunk's combine runs on all N
   // workers afterwards) and the dispatch, less the first chunk's when all
@@ -166,6 +161,24 @@ __host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_c
   out->n_steal = n_steal;
   out->final_all = 1;
   out->t_pred_s = best;
+}
+
+// Eq 16: argmin of T_total over the grid, c ascending then K ascending, the
+// first strict minimum winning; then the steal count.  (The megakernel's
+// prologue evaluates the grid points in parallel and scans them in the same
+// order, with the same bits.)
+__host__ __device__ inline void cost_model(const DevCalib& cb, int N, double w_comp, double w_disp,
+                                           double w_comb, const long long* n_tiles_by_k,
+                                           moe_plan* out) {
+#pragma clang fp contract(off)
+  int bc = 0, bk = 0;
+  double best = cm_t_total(cb, 0, 0, w_comp, w_disp, w_comb);
+  for (int ci = 0; ci < cb.n_c; ++ci)
+    for (int ki = 0; ki < cb.n_k; ++ki) {
+      double t = cm_t_total(cb, ci, ki, w_comp, w_disp, w_comb);
+      if (t < best) { best = t; bc = ci; bk = ki; }
+    }
+  cm_finish(cb, N, w_comp, w_disp, w_comb, n_tiles_by_k, bc, bk, best, out);
 }
 
 // Volumes of section 3.1 from the routing stats.  With `literal` the moved
