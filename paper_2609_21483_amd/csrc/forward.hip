@@ -47,7 +47,7 @@ struct Scratch {
   int bc[8];
   long long ntk[KOPT];
   DevCalib cal;                                        // the calibration table, staged by the prologue
-  double tt[MOE_CALIB_MAX_C * MOE_CALIB_MAX_K];        // T_total of each (c, K) grid point
+  int st[8];                                           // routing stats (ST_*), staged by the prologue
   int part[NWF];
   int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
   int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
@@ -718,6 +718,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, 
     const uint32_t* src = reinterpret_cast<const uint32_t*>(a.calib);
     uint32_t* dst = reinterpret_cast<uint32_t*>(&W.cal);
     for (int i = tid; i < (int)(sizeof(DevCalib) / 4); i += FNTH) dst[i] = src[i];
+    if (tid >= FNTH - 8) W.st[tid - (FNTH - 8)] = a.stats[tid - (FNTH - 8)];
   }
   __syncthreads();
   // GEMM tiles at each stored chunk option (for W_tile of Eq 14)
@@ -737,18 +738,32 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, 
       }
       part += (long long)ceil_div(rows, BM) * (a.nt0 + a.nt1 * a.nsplit);
     }
-    if (part) atomicAdd((unsigned long long*)&W.ntk[ki], (unsigned long long)part);
+    // one LDS atomic per wavefront (same-address atomics serialise)
+    for (int d = WAVE / 2; d >= 1; d >>= 1) part += __shfl_xor(part, d, WAVE);
+    if ((tid & (WAVE - 1)) == 0 && part) atomicAdd((unsigned long long*)&W.ntk[ki], (unsigned long long)part);
   }
   __syncthreads();
   const bool model = !a.forced && a.mode != MOE_MODE_STATIC;
-  double wc = 0.0, wd = 0.0, wb = 0.0;
+  double wc = 0.0, wd = 0.0, wb = 0.0, best = 0.0;
+  int bi = 0;
   if (model && tid < WAVE) {
-    // Eq 15 at every grid point, one point per lane of the first wavefront
-    cm_volumes(a.stats, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
+    // Eq 15 at every grid point, one point per lane of the first wavefront;
+    // Eq 16 by a wavefront reduction in the host model's order (c ascending,
+    // then K): the smallest T_total, the lowest grid index among equal ones,
+    // which is the first strict minimum of the host's scan
+    cm_volumes(W.st, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
     const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
-    for (int i = tid; i < npt; i += WAVE) W.tt[i] = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
+    bi = -1;
+    for (int i = tid; i < npt; i += WAVE) {
+      const double t = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
+      if (bi < 0 || t < best) { best = t; bi = i; }
+    }
+    for (int d = 1; d < WAVE; d <<= 1) {
+      const double ob = __shfl_xor(best, d, WAVE);
+      const int oi = __shfl_xor(bi, d, WAVE);
+      if (oi >= 0 && (bi < 0 || ob < best || (ob == best && oi < bi))) { best = ob; bi = oi; }
+    }
   }
-  __syncthreads();
   if (tid == 0) {
     moe_plan p;
     if (a.forced) {
@@ -760,12 +775,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, 
       p.final_all = 0;
       p.t_pred_s = 0.0;
     } else {
-      // Eq 16 in the host model's order: c ascending, then K, first strict minimum
-      const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
-      int bi = 0;
-      double best = W.tt[0];
-      for (int i = 1; i < npt; ++i)
-        if (W.tt[i] < best) { best = W.tt[i]; bi = i; }
+      const int nk = W.cal.n_k;
       long long nt_by_k[MOE_CALIB_MAX_K];
       for (int j = 0; j < nk; ++j) nt_by_k[j] = W.ntk[kopt_index(W.cal.kk[j])];
       cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &p);
