@@ -508,7 +508,7 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   gate_mfma_kernel<<<(h->T + 31) / 32, 4 * WAVE, 0, s>>>(g);
   const int tok_blocks = (h->T + (NTH / 16) - 1) / (NTH / 16);
   gate_cand_kernel<<<tok_blocks, NTH, 0, s>>>(g);
-  gate_chain_kernel<<<std::min(4096, std::max(1, (h->T * g.k * 3 / 2 + NTH - 1) / NTH)), NTH, 0, s>>>(g);
+  gate_chain_kernel<<<std::min(16384, std::max(1, (h->T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
   gate_final_kernel<<<tok_blocks, NTH, 0, s>>>(g);
   HIP_TRY(hipGetLastError());
   return moe_build_tables(h, topk_idx, stream);

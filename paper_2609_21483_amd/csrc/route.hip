@@ -261,49 +261,58 @@ __global__ void __launch_bounds__(NTH) gate_cand_kernel(GateArgs a) {
 }
 
 // the defined logit of one (token, expert): fp32, one accumulator, h
-// ascending, each product rounded before the add.  The chain of adds is
-// serial; two register sets take turns so that the loads of the next PF
-// vectors are in flight while the current ones are added.
-constexpr int PF = 8;
+// ascending, each product rounded before the add.  A product of two bf16
+// values is exact in fp32, so fma(x, w, acc) rounds exactly as acc + x*w and
+// saves the multiply on the serial chain.  Two register sets of PF vectors
+// take turns so that the next block's loads are in flight while the current
+// one is added.
+constexpr int PF = 16;
 __device__ __forceinline__ void chain_add(float& acc, const u32x4_t (&xb)[PF], const u32x4_t (&wb)[PF]) {
-#pragma clang fp contract(off)
 #pragma unroll
   for (int i = 0; i < PF; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float p0 = bf16_lo(xb[i][q]) * bf16_lo(wb[i][q]);
-      acc = acc + p0;
-      const float p1 = bf16_hi(xb[i][q]) * bf16_hi(wb[i][q]);
-      acc = acc + p1;
+      acc = __builtin_fmaf(bf16_lo(xb[i][q]), bf16_lo(wb[i][q]), acc);
+      acc = __builtin_fmaf(bf16_hi(xb[i][q]), bf16_hi(wb[i][q]), acc);
     }
 }
 __device__ __forceinline__ float exact_logit(const uint16_t* xr, const uint16_t* wr, int H) {
   const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(xr);
   const u32x4_t* wv = reinterpret_cast<const u32x4_t*>(wr);
-  const int nv = H >> 3;  // H % 64 == 0: nv is a multiple of 8
-  u32x4_t x0[PF], w0[PF], x1[PF], w1[PF];
+  const int nv = H >> 3;       // 16-byte vectors per row
+  const int nb = nv / PF;      // whole blocks of PF vectors
+  u32x4_t xa[PF], wa[PF], xb[PF], wb[PF];
+  auto load = [&](u32x4_t (&xd)[PF], u32x4_t (&wd)[PF], int blk) {
 #pragma unroll
-  for (int i = 0; i < PF; ++i) { x0[i] = xv[i]; w0[i] = wv[i]; }
+    for (int i = 0; i < PF; ++i) { xd[i] = xv[blk * PF + i]; wd[i] = wv[blk * PF + i]; }
+  };
   float acc = 0.0f;
-  int v0 = 0;
-  for (; v0 + 2 * PF <= nv; v0 += 2 * PF) {
-#pragma unroll
-    for (int i = 0; i < PF; ++i) { x1[i] = xv[v0 + PF + i]; w1[i] = wv[v0 + PF + i]; }
-    chain_add(acc, x0, w0);
-    if (v0 + 2 * PF < nv) {
-#pragma unroll
-      for (int i = 0; i < PF; ++i) { x0[i] = xv[v0 + 2 * PF + i]; w0[i] = wv[v0 + 2 * PF + i]; }
+  if (nb > 0) load(xa, wa, 0);
+  for (int b = 0; b < nb; b += 2) {
+    if (b + 1 < nb) load(xb, wb, b + 1);
+    chain_add(acc, xa, wa);
+    if (b + 1 < nb) {
+      if (b + 2 < nb) load(xa, wa, b + 2);
+      chain_add(acc, xb, wb);
     }
-    chain_add(acc, x1, w1);
   }
-  if (v0 < nv) chain_add(acc, x0, w0);  // nv % 16 == 8: one set left, already loaded
+  for (int v = nb * PF; v < nv; ++v) {  // the vectors after the last whole block
+    const u32x4_t x = xv[v], w = wv[v];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc = __builtin_fmaf(bf16_lo(x[q]), bf16_lo(w[q]), acc);
+      acc = __builtin_fmaf(bf16_hi(x[q]), bf16_hi(w[q]), acc);
+    }
+  }
   return acc;
 }
 
-// one lane per chain of the list
-__global__ void __launch_bounds__(NTH) gate_chain_kernel(GateArgs a) {
+// one lane per chain of the list, one wavefront per workgroup: each chain
+// streams two rows of H bf16 values, so the chains are spread over as many
+// CUs as possible (a CU's memory pipeline, not its VALU, bounds a chain)
+__global__ void __launch_bounds__(WAVE) gate_chain_kernel(GateArgs a) {
   const int n = a.stats[ST_CANDS];
-  for (int i = blockIdx.x * NTH + threadIdx.x; i < n; i += gridDim.x * NTH) {
+  for (int i = blockIdx.x * WAVE + threadIdx.x; i < n; i += gridDim.x * WAVE) {
     const int g = a.ch_g[i], e = a.ch_e[i];
     float l = exact_logit(a.x + (size_t)g * a.H, a.wgt + (size_t)e * a.H, a.H);
     if (a.bias) l = l + a.bias[e];
