@@ -505,7 +505,7 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   }
   zero_i32_kernel<<<1, 64, 0, s>>>(g.stats + ST_CANDS, 1);
   gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
-  gate_mfma_kernel<<<(h->T + 31) / 32, 4 * WAVE, 0, s>>>(g);
+  gate_mfma_kernel<<<(h->T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
   const int tok_blocks = (h->T + (NTH / 16) - 1) / (NTH / 16);
   gate_cand_kernel<<<tok_blocks, NTH, 0, s>>>(g);
   gate_chain_kernel<<<std::min(16384, std::max(1, (h->T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);

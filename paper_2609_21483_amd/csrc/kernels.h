@@ -201,6 +201,8 @@ __host__ __device__ inline void cm_volumes(const int32_t* stats, int H, int F, i
   }
 }
 
+constexpr int GATE_WAVES = 4;  // wavefronts per workgroup of gate_mfma_kernel (each sums a quarter of H)
+
 // ---- launch prototypes ---------------------------------------------------------
 __global__ void gate_prep_kernel(GateArgs a);
 __global__ void gate_mfma_kernel(GateArgs a);

@@ -62,11 +62,12 @@ __global__ void __launch_bounds__(NTH) gate_prep_kernel(GateArgs a) {
 // covers recursive fp32 summation of all H products) and the quarters are
 // added through LDS.  Lane l holds token row (l & 31) and expert row (l & 31)
 // of the current 32-expert block at hidden offsets 8 * (l >> 5) .. + 8 of each
-// 16-deep step; GSTEP steps are loaded before their MFMAs.
-constexpr int GATE_EB = 4;   // 32-expert blocks per pass (128 experts)
-constexpr int GSTEP = 4;     // 16-deep steps loaded ahead
-constexpr int GWAVES = 4;
-__global__ void __launch_bounds__(GWAVES * WAVE) gate_mfma_kernel(GateArgs a) {
+// 16-deep step; GSTEP steps are loaded before their MFMAs.  GATE_EB 32-expert
+// blocks are summed per pass over H: one block with 8 steps ahead when E <= 32
+// (the pass streams x with more loads in flight), four with 4 steps ahead
+// otherwise (register budget).
+template <int GATE_EB, int GSTEP, int GWAVES>
+__device__ __forceinline__ void gate_mfma_body(const GateArgs& a) {
   __shared__ float red[GWAVES - 1][32 * 32 * GATE_EB];
   __shared__ float ssr[GWAVES][64];
   const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
@@ -162,6 +163,11 @@ __global__ void __launch_bounds__(GWAVES * WAVE) gate_mfma_kernel(GateArgs a) {
     for (int w = 0; w < GWAVES; ++w) t += ssr[w][lane] + ssr[w][lane ^ 32];
     if (lane < 32 && grow) a.xn[g] = sqrtf(t);
   }
+}
+
+__global__ void __launch_bounds__(GATE_WAVES * WAVE) gate_mfma_kernel(GateArgs a) {
+  if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a);
+  else gate_mfma_body<4, 4, GATE_WAVES>(a);
 }
 
 // lanes of one token's group of GG: reductions stay inside the group
