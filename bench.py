@@ -11,7 +11,8 @@ the window the paper times: end of routing to end of combine), next to the
 static-split and serial baselines measured the same way.  `roofline` rates the
 megakernel (the dominant kernel) against the bf16 MFMA peak; `phases` comes
 from one extra traced launch after the timed region and gives the movement
-workers' HBM rate and the compute workers' MFMA utilisation.
+workers' HBM rate, the compute workers' MFMA utilisation, and SM Active and
+movement/compute overlap (paper_2609_21483_amd.timeline).
 """
 from __future__ import annotations
 
@@ -117,6 +118,8 @@ def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
     span = float(us(wgs["t2"]).max())
     comb_span = float((us(comb["t2"]).max() - us(comb["t1"]).min())) if len(comb) else float("nan")
     per_cu_peak = PEAK_BF16_TFLOPS / 256.0
+    from paper_2609_21483_amd import timeline as TL
+    tl = TL.metrics(tr)
     return {
         "traced_layer_us": span,
         "dispatch_us": disp_end,
@@ -127,6 +130,10 @@ def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
         "compute_workers": n_comp,
         "compute_busy_frac": busy / (n_comp * span) if n_comp else None,
         "mfma_util_while_busy": flops / (busy * 1e-6) / 1e12 / per_cu_peak,
+        "sm_active": tl["sm_active"],
+        "overlap": tl["overlap"],
+        "overlap_of_movement": tl["overlap_of_mov"],
+        "prologue_us": tl["prologue_us"],
         "note": "one traced launch (tracing adds overhead); dispatch includes rows moved by compute workers "
                 "that steal movement while their tiles wait",
     }

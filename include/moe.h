@@ -173,12 +173,14 @@ moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
  * every workgroup appends 32-byte records:
  *   int64 word 0: kind | ticket << 8 | xcd << 20 | id << 32
  *   int64 words 1-3: times t0, t1, t2 from the 100 MHz device clock
+ * (ticket: the recording workgroup's arrival ticket, which fixes its role:
+ * tickets below the plan's c are movement workers; xcd: the XCD it runs on)
  * kind 1 workgroup (id 1 = movement worker): entry, plan + schedule built, exit
  * kind 2 compute tile (id = tile code: stage << 24 | XCD class << 21 |
  *        index): claimed, inputs ready, finished
  * kind 3 dispatch by one movement worker: start, end
  * kind 4 combine unit of one wavefront (id = unit | wave << 24): claimed,
- *        claimed, end
+ *        inputs ready (its GEMM1 row tiles done), end
  * kind 5 dispatch unit of one wavefront (id = unit | wave << 24): start,
  *        rows stored and drained, readiness counted
  * Word 0 of buf holds the number of records written (at most

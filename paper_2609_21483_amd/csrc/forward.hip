@@ -52,6 +52,7 @@ struct Scratch {
   int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
   int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
   int dexh;              // every dispatch unit has been claimed (seen by this workgroup)
+  int ticket;            // this workgroup's arrival ticket (trace records)
   float wwt[NWF][WAVE];  // per wavefront: their weights
 };
 
@@ -357,7 +358,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
   if constexpr (SIG) {
     const uint64_t tr1 = a.trace ? now_ticks() : 0;
     dispatch_count(a, S, u, cur);
-    if (a.trace && lane_id() == 0) trace_rec(a, 5, 0, u | ((long long)wave_id() << 24), tr0, tr1, now_ticks());
+    if (a.trace && lane_id() == 0) trace_rec(a, 5, W.ticket, u | ((long long)wave_id() << 24), tr0, tr1, now_ticks());
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -461,8 +462,10 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
 // A wavefront combines tokens [g0, g0 + nt).  In the megakernel (S given) it
 // first waits until every GEMM1 column tile of each row tile holding one of
 // those tokens' source rows is done: one lane polls per distinct row tile.
-// Returns false when the launch was aborted.
-__device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S, Scratch& W, int g0, int nt) {
+// Returns false when the launch was aborted.  With tracing on, t_ready gets
+// the time the waits ended.
+__device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S, Scratch& W, int g0, int nt,
+                                               uint64_t& t_ready) {
   const int lane = lane_id();
   int* sl = W.wsl[wave_id()];
   float* wt = W.wwt[wave_id()];
@@ -502,6 +505,7 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
       pending &= ~__builtin_amdgcn_ballot_w64(id == tile);
       if (!wave_wait_geq(a, &a.ctl[CTL_READY + (2 * a.mt_max + tile) * CTL_PAD], need)) return false;
     }
+    if (a.trace) t_ready = now_ticks();
   }
   __builtin_amdgcn_wave_barrier();
   switch (ks) {
@@ -927,9 +931,10 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
     const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
     if (u < 0) return true;
     const uint64_t t0 = a.trace ? now_ticks() : 0;
+    uint64_t t1 = t0;
     const int g0 = u * a.ct;
-    if (!combine_tokens(a, &S, W, g0, min(a.ct, a.T - g0))) return false;
-    if (a.trace && lane_id() == 0) trace_rec(a, 4, ticket, u | ((long long)wave_id() << 24), t0, t0, now_ticks());
+    if (!combine_tokens(a, &S, W, g0, min(a.ct, a.T - g0), t1)) return false;
+    if (a.trace && lane_id() == 0) trace_rec(a, 4, ticket, u | ((long long)wave_id() << 24), t0, t1, now_ticks());
   }
 }
 
@@ -957,6 +962,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
 
   if (tid == 0) {
     W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
+    W.ticket = W.bc[0];
     W.dexh = 0;
   }
   __syncthreads();
@@ -1033,7 +1039,8 @@ __global__ void __launch_bounds__(FNTH, 1) serial_combine_kernel(FwdArgs a) {
   const int n = ceil_div(a.T, a.ct);
   for (int u = blockIdx.x * NWF + wave_id(); u < n; u += gridDim.x * NWF) {
     const int g0 = u * a.ct;
-    combine_tokens(a, nullptr, W, g0, min(a.ct, a.T - g0));
+    uint64_t t_unused = 0;
+    combine_tokens(a, nullptr, W, g0, min(a.ct, a.T - g0), t_unused);
   }
 }
 
