@@ -31,6 +31,7 @@ constexpr int NWF = FNTH / WAVE;  // waves per forward workgroup
 struct Sched {
   int K, nseg, G;        // chunks, segments, groups = K*2*nseg
   int n_comp, n_disp, n_comb;
+  int disp0;             // dispatch units [0, disp0) are owned statically (megakernel)
   int c, n_steal, final_all;
   int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
   // per (chunk q, segment) at index q*nseg + seg
@@ -222,10 +223,12 @@ __device__ __forceinline__ void trace_rec(const FwdArgs& a, int kind, int ticket
   r[3] = (long long)t2;
 }
 
-// Movement units are assigned statically: worker w of n (a workgroup index)
-// takes units (i * n + w) * NWF + wave for i = 0, 1, ..., so the units are
-// issued in ascending (token, hence chunk) order across all workers and no
-// queue counter is contended.
+// Dispatch units in the megakernel: the first round is owned statically,
+// wavefront w of the worker with ticket t copying unit t * NWF + w (every
+// worker that moves rows at launch: all of them when compute workers steal
+// movement, else the movement workers), so the launch starts without queue
+// traffic; units are sized so that this round covers all of them whenever T
+// allows.  Later units are claimed from the sharded queue (claim_unit).
 
 // Dispatch (section 4, with dedup): a wavefront copies the rows of tokens
 // [u*dt, u*dt + dt) of unit u; each token row is read once and written to
@@ -392,11 +395,19 @@ __device__ __forceinline__ int claim_unit(const FwdArgs& a, int base, int n_unit
   return -1;
 }
 
+// the next dispatch unit past the statically owned ones, or -1 (at once when
+// every unit is owned statically: no queue reads)
+__device__ __forceinline__ int claim_disp(const FwdArgs& a, const Sched& S, int& shard) {
+  if (S.disp0 >= S.n_disp) return -1;
+  const int v = claim_unit(a, CTL_QD, S.n_disp - S.disp0, shard);
+  return v < 0 ? -1 : S.disp0 + v;
+}
+
 // movement worker: dispatch until every unit is claimed
 __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& S, Scratch& W) {
   int shard = wave_id();
   for (;;) {
-    const int u = claim_unit(a, CTL_QD, S.n_disp, shard);
+    const int u = claim_disp(a, S, shard);
     if (u < 0) break;
     dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
   }
@@ -857,7 +868,7 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
     __syncthreads();
     if (st) return st > 0;
     int shard = wave_id();
-    const int u = claim_unit(a, CTL_QD, S.n_disp, shard);
+    const int u = claim_disp(a, S, shard);
     if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
     else if (lane_id() == 0) W.dexh = 1;
   }
@@ -964,12 +975,19 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
     W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
     W.ticket = W.bc[0];
     W.dexh = 0;
+    S.disp0 = min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF);
   }
   __syncthreads();
   const int ticket = __builtin_amdgcn_readfirstlane(W.bc[0]);
   const bool mover = ticket < S.c;
   const uint64_t t_sched = a.trace ? now_ticks() : 0;
   __syncthreads();
+
+  // this wavefront's statically owned dispatch unit, if any
+  {
+    const int u0 = ticket * NWF + wave_id();
+    if (u0 < S.disp0) dispatch_one<true>(a, &S, W, u0, unit_slot(a, u0));
+  }
 
   bool ok = true;
   if (mover) {
