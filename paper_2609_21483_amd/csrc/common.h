@@ -43,11 +43,11 @@ __host__ __device__ inline int kopt_value(int i) { return 1 << i; }
 constexpr int CTL_PAD = 16;
 constexpr int CTL_TICKET = 16;    // arrival ticket -> role
 constexpr int CTL_ABORT = 32;     // set once any wait times out
+constexpr int NSHARD = 64;        // movement-unit queue shards (one per lane of a wavefront)
 constexpr int CTL_QC = 128;       // [NSHARD] combine-unit queue heads (CTL_PAD apart)
-constexpr int NSHARD = 8;         // dispatch-unit queue shards
 constexpr int NXCD = 8;           // XCDs of gfx950 (slab classes of the tile queues)
-constexpr int CTL_QD = 256;       // [NSHARD] dispatch-unit queue heads (CTL_PAD apart)
-constexpr int CTL_READY = 384;    // [mt_max] dispatched rows per row tile (CTL_PAD apart),
+constexpr int CTL_QD = CTL_QC + NSHARD * CTL_PAD;     // [NSHARD] dispatch-unit queue heads
+constexpr int CTL_READY = CTL_QD + NSHARD * CTL_PAD;  // [mt_max] dispatched rows per row tile (CTL_PAD apart),
 // then [mt_max] GEMM0 column tiles finished per row tile (CTL_PAD apart),
 // then [mt_max] GEMM1 (column tile, split) items finished per row tile (CTL_PAD apart)
 static_assert(CTL_QC + NSHARD * CTL_PAD <= CTL_QD, "control block overlap");

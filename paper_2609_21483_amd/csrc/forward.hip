@@ -252,11 +252,7 @@ __device__ __forceinline__ int unit_slot(const FwdArgs& a, int u) {
 // GEMM tile loop (movement stealing) the optimiser cannot hoist the unit's
 // per-lane index and address arithmetic out of that loop and keep it live
 // across the GEMM mainloop.
-__device__ __forceinline__ int lane_here() {
-  int l;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-  return l;
-}
+using gemm::lane_here;
 
 template <bool SIG>
 __device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int u, int cur) {
@@ -380,20 +376,30 @@ __device__ __forceinline__ void dispatch_static(const FwdArgs& a, Scratch& W, in
 
 // Megakernel: movement units are claimed per wavefront from NSHARD queues
 // at ctl[base + shard * CTL_PAD] (unit u is the (u / NSHARD)-th of shard
-// u % NSHARD, so every shard advances in token order).  Trying the shards
-// from `shard` on (a plain read first, so exhausted shards take no atomic),
-// returns the next unit or -1 once all are exhausted.
+// u % NSHARD, so every shard advances in token order).  Lane l reads the
+// head of shard (shard + l) % NSHARD, all in one vector read; the nearest
+// shard with units left takes one atomic.  A shard found exhausted by that
+// atomic reads exhausted from then on, so the loop ends within NSHARD
+// rounds.  Returns the unit, or -1 once every shard is exhausted.
+static_assert(NSHARD == WAVE, "one queue shard per lane");
 __device__ __forceinline__ int claim_unit(const FwdArgs& a, int base, int n_units, int& shard) {
-  for (int tries = 0; tries < NSHARD; ++tries) {
-    int* q = &a.ctl[base + shard * CTL_PAD];
+  const int lane = lane_id();
+  for (int round = 0; round < NSHARD; ++round) {
+    const int sl = (shard + lane) & (NSHARD - 1);
+    const bool open = ld_relaxed(&a.ctl[base + sl * CTL_PAD]) * NSHARD + sl < n_units;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(open);
+    if (!m) return -1;
+    shard = (shard + (int)__builtin_ctzll(m)) & (NSHARD - 1);
     int v = 0;
-    if (lane_id() == 0) v = ld_relaxed(q) * NSHARD + shard < n_units ? fetch_add_relaxed(q, 1) : n_units;
+    if (lane == 0) v = fetch_add_relaxed(&a.ctl[base + shard * CTL_PAD], 1);
     const int u = __builtin_amdgcn_readfirstlane(v) * NSHARD + shard;
     if (u < n_units) return u;
-    shard = shard + 1 == NSHARD ? 0 : shard + 1;
   }
   return -1;
 }
+
+// a wavefront's first shard: spread over the shards by worker and wavefront
+__device__ __forceinline__ int first_shard(const Scratch& W) { return (W.ticket * NWF + wave_id()) & (NSHARD - 1); }
 
 // the next dispatch unit past the statically owned ones, or -1 (at once when
 // every unit is owned statically: no queue reads)
@@ -405,7 +411,7 @@ __device__ __forceinline__ int claim_disp(const FwdArgs& a, const Sched& S, int&
 
 // movement worker: dispatch until every unit is claimed
 __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& S, Scratch& W) {
-  int shard = wave_id();
+  int shard = first_shard(W);
   for (;;) {
     const int u = claim_disp(a, S, shard);
     if (u < 0) break;
@@ -423,7 +429,7 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
 // flight.
 template <int KS>
 __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
-  constexpr int P = KS >= 16 ? 1 : 16 / KS;  // positions per lane per pass
+  constexpr int P = KS >= 2 ? 16 / KS : 8;  // positions per lane per pass (~16 row vectors in flight)
   const int lane = lane_id();
   const int VPR = a.H >> 3;
   const int total = nt * VPR;
@@ -505,8 +511,23 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
       if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
     }
   }
-  sl[lane] = s;
-  wt[lane] = w;
+  // compact each token's present source rows, keeping their order: token t's
+  // r-th present row goes to entry t * kp + r, kp being the most any token of
+  // the unit has, so the passes below keep ~16 present rows in flight per
+  // lane however sparse the local slots are (absent rows add nothing, so the
+  // sum is unchanged)
+  const uint64_t pm = __builtin_amdgcn_ballot_w64(s >= 0);
+  const uint64_t tok = (1ull << ks) - 1;  // ks <= 16
+  int kp = 0;
+  for (int t = 0; t < nt; ++t) kp = max(kp, (int)__builtin_popcountll(pm & (tok << (t * ks))));
+  sl[lane] = -1;
+  __builtin_amdgcn_wave_barrier();
+  if (s >= 0) {
+    const int t = lane / ks;
+    const int r = (int)__builtin_popcountll(pm & ((1ull << lane) - 1) & (tok << (t * ks)));
+    sl[t * kp + r] = s;
+    wt[t * kp + r] = w;
+  }
   if (S) {
     const int need = a.nt1;  // every column tile of the row tile (split ones reduced)
     uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
@@ -519,9 +540,10 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
     if (a.trace) t_ready = now_ticks();
   }
   __builtin_amdgcn_wave_barrier();
-  switch (ks) {
+  switch (kp) {
 #define MOE_COMBINE_CASE(n) \
   case n: combine_body<n>(a, sl, wt, g0, nt); break;
+    case 0:  // no token of the unit has a source row: zero rows
     MOE_COMBINE_CASE(1) MOE_COMBINE_CASE(2) MOE_COMBINE_CASE(3) MOE_COMBINE_CASE(4)
     MOE_COMBINE_CASE(5) MOE_COMBINE_CASE(6) MOE_COMBINE_CASE(7) MOE_COMBINE_CASE(8)
     MOE_COMBINE_CASE(9) MOE_COMBINE_CASE(10) MOE_COMBINE_CASE(11) MOE_COMBINE_CASE(12)
@@ -867,7 +889,7 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
     const int st = W.bc[2];
     __syncthreads();
     if (st) return st > 0;
-    int shard = wave_id();
+    int shard = first_shard(W);
     const int u = claim_disp(a, S, shard);
     if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
     else if (lane_id() == 0) W.dexh = 1;
@@ -937,7 +959,7 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
 // waits only for the row tiles its tokens' rows come from, so the combine of
 // finished tokens starts while the last GEMM tiles run.
 __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S, Scratch& W, int ticket) {
-  int shard = wave_id();
+  int shard = first_shard(W);
   for (;;) {
     const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
     if (u < 0) return true;

@@ -82,6 +82,15 @@ __device__ __forceinline__ T* opaque(T* p) {
   return reinterpret_cast<T*>(opaque((size_t)p));
 }
 
+// Lane id through a volatile asm statement: values derived from it are
+// recomputed where they are used instead of being hoisted out of a persistent
+// loop and kept live (or spilled) across every mainloop.
+__device__ __forceinline__ int lane_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -97,7 +106,7 @@ __device__ __forceinline__ void dma_offsets(DmaOff& o, int lda, int a_rows, int 
   ldb = opaque(ldb);
   a_rows = opaque(a_rows);
   b_rows = opaque(b_rows);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
 #pragma unroll
   for (int i = 0; i < A_INSTR; ++i) {
     const int g = (wave * A_INSTR + i) * 64 + lane;
@@ -132,7 +141,7 @@ struct FragOff {
 };
 
 __device__ __forceinline__ FragOff frag_offsets() {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
   const int wm = wave % WM, wn = wave / WM;
   const int ra = wm * TM + (lane & 31), rb = wn * TN + (lane & 31);
   FragOff f;
