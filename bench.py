@@ -7,8 +7,10 @@ dynamic-split megakernel.  Inputs are resident in HBM before timing starts.
 
 Prints one JSON line.  `value` is tokens/s of whole steps; `layer_us` is the
 MoE-layer time alone (the megakernel, from HIP events on its launch stream,
-the window the paper times: end of routing to end of combine), next to the
-static-split and serial baselines measured the same way.  `roofline` rates the
+the window the paper times: end of routing to end of combine).  `baselines`
+holds the static-split and serial modes and the dynamic mode again, all timed
+as back-to-back forward launches in interleaved rounds; `dynamic_speedup` is a
+baseline's time over the dynamic time measured that way.  `roofline` rates the
 megakernel (the dominant kernel) against the bf16 MFMA peak; `phases` comes
 from one extra traced launch after the timed region and gives the movement
 workers' HBM rate, the compute workers' MFMA utilisation, and SM Active and
@@ -46,6 +48,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128)
     ap.add_argument("--modes", default="static,serial", help="baselines timed next to the dynamic mode")
+    ap.add_argument("--rounds", type=int, default=3, help="interleaved rounds of the baseline comparison")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain torch copy of this many MiB (the scale for PMC byte counters)")
     return ap.parse_args()
@@ -238,12 +241,23 @@ def main():
     torch.cuda.synchronize()
     route_us = r_ev[0].elapsed_time(r_ev[1]) * 1e3 / args.steps
 
+    # the baselines next to the dynamic forward, timed the same way (forward
+    # launches back to back on the same routing) in interleaved rounds, so
+    # that clock drift spreads over all modes alike
     baselines = {}
-    for m in [m for m in args.modes.split(",") if m]:
-        us = time_forward(B, layer, x, idx, w, y, m, args.steps, args.warmup, stream)
-        baselines[m] = {"layer_us_median": float(np.median(us)), "tokens_per_s": shape.T / (float(np.median(us)) * 1e-6),
-                        "dynamic_speedup": float(np.median(us)) / lat}
-        print(f"[bench] {m} done", file=sys.stderr, flush=True)
+    modes = [m for m in args.modes.split(",") if m]
+    if modes:
+        runs = {m: [] for m in ["dynamic"] + modes}
+        for _ in range(args.rounds):
+            for m in runs:
+                runs[m] += time_forward(B, layer, x, idx, w, y, m, args.steps, 2, stream)
+        dyn = float(np.median(runs["dynamic"]))
+        baselines["dynamic_same_timing"] = {"layer_us_median": dyn}
+        for m in modes:
+            med = float(np.median(runs[m]))
+            baselines[m] = {"layer_us_median": med, "tokens_per_s": shape.T / (med * 1e-6),
+                            "dynamic_speedup": med / dyn}
+        print(f"[bench] baselines done ({args.rounds} interleaved rounds)", file=sys.stderr, flush=True)
     phases = traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops)
     if args.copy_probe_mib:
         n = args.copy_probe_mib << 20
