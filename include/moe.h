@@ -169,10 +169,16 @@ moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
 /* Timeline trace of the megakernel (a measurement aid for the schedule of
  * sections 3-4: worker roles, tile waits, movement phases).  buf is caller-
  * owned device memory of `bytes` bytes, or NULL to turn tracing off.  Each
- * later moe_forward in a non-serial mode first clears the record counter, then
- * every workgroup appends 32-byte records:
- *   int64 word 0: kind | ticket << 8 | xcd << 20 | id << 32
- *   int64 words 1-3: times t0, t1, t2 from the 100 MHz device clock
+ * later moe_forward in a non-serial mode writes, per wavefront of the launch
+ * (S = n_workers * 8 wavefronts, segment b * 8 + w for wavefront w of
+ * workgroup b), up to R records into that wavefront's own segment:
+ *   bytes 0-63: int32 header: magic 0x31435254, S, R, the int64 word offset
+ *     of segment 0
+ *   bytes 64..: int32 record count of each segment (S of them), padded to
+ *     a multiple of 64 bytes
+ *   then S segments of R records of 32 bytes:
+ *     int64 word 0: kind | ticket << 8 | xcd << 20 | id << 32
+ *     int64 words 1-3: times t0, t1, t2 from the 100 MHz device clock
  * (ticket: the recording workgroup's arrival ticket, which fixes its role:
  * tickets below the plan's c are movement workers; xcd: the XCD it runs on)
  * kind 1 workgroup (id 1 = movement worker): entry, plan + schedule built, exit
@@ -183,10 +189,12 @@ moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
  *        inputs ready (its GEMM1 row tiles done), end
  * kind 5 dispatch unit of one wavefront (id = unit | wave << 24): start,
  *        rows stored and drained, readiness counted
- * Word 0 of buf holds the number of records written (at most
- * (bytes - 64) / 32 are stored); records start at byte 64.  The layout of a
+ * R = (bytes - header and counts) / 32 / S; records past R are dropped.  A
+ * wavefront appends with a counter of its own (no global atomics).  The
+ * counts and header are written at the end of the launch.  The layout of a
  * trace follows the handle's current plan; it changes nothing else.
- * Errors: MOE_ERR_INVALID_ARG for a non-NULL buf with bytes < 96. */
+ * Errors: MOE_ERR_INVALID_ARG for a non-NULL buf too small for one record per
+ * wavefront. */
 moe_status moe_set_trace(moe_handle* h, void* buf, int64_t bytes);
 
 /* Workspace size in bytes and its region offsets (host out-parameters). */

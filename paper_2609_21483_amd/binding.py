@@ -173,16 +173,25 @@ def moe_set_trace(h: int, buf, nbytes: int = 0) -> None:
 TRACE_KINDS = {1: "workgroup", 2: "tile", 3: "dispatch", 4: "combine", 5: "dispatch unit"}
 
 
+TRACE_MAGIC = 0x31435254
+
+
 def read_trace(buf) -> "np.ndarray":
-    """Decode a trace buffer into a structured array (kind, ticket, xcd, id,
-    t0, t1, t2), times in device-clock ticks of 10 ns."""
+    """Decode a trace buffer (see moe_set_trace) into one structured array
+    (kind, ticket, xcd, id, t0, t1, t2) of every wavefront's records, times in
+    device-clock ticks of 10 ns.  An empty array if no launch wrote it."""
     import numpy as np
-    raw = buf.cpu().numpy().view(np.int64)
-    n = min(int(raw[0]) & 0xFFFFFFFF, (raw.size * 8 - 64) // 32)
-    rec = raw[8:8 + 4 * n].reshape(n, 4)
+    dt = [("kind", "i4"), ("ticket", "i4"), ("xcd", "i4"), ("id", "i8"), ("t0", "i8"), ("t1", "i8"), ("t2", "i8")]
+    raw = buf.cpu().numpy().view(np.uint8)
+    hdr = raw[:64].view(np.int32)
+    if int(hdr[0]) != TRACE_MAGIC:
+        return np.zeros(0, dtype=dt)
+    nseg, cap, rec0 = int(hdr[1]), int(hdr[2]), int(hdr[3])
+    counts = raw[64:64 + 4 * nseg].view(np.int32)
+    recs = raw[rec0 * 8:rec0 * 8 + nseg * cap * 32].view(np.int64).reshape(nseg, cap, 4)
+    rec = np.concatenate([recs[i, :min(int(counts[i]), cap)] for i in range(nseg)] + [np.zeros((0, 4), np.int64)])
     w0 = rec[:, 0]
-    out = np.zeros(n, dtype=[("kind", "i4"), ("ticket", "i4"), ("xcd", "i4"), ("id", "i8"),
-                             ("t0", "i8"), ("t1", "i8"), ("t2", "i8")])
+    out = np.zeros(len(rec), dtype=dt)
     out["kind"] = w0 & 0xFF
     out["ticket"] = (w0 >> 8) & 0xFFF
     out["xcd"] = (w0 >> 20) & 0xFFF

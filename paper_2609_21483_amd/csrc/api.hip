@@ -54,7 +54,7 @@ struct moe_handle {
   long long timeout_ticks = 200000000LL;  // 2 s at 100 MHz
   int inject_stall = 0;
   long long* trace = nullptr;
-  int trace_cap = 0;
+  int trace_cap = 0, trace_rec0 = 0;
 };
 
 namespace {
@@ -295,6 +295,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.inject_stall = h->inject_stall;
   a.trace = h->trace;
   a.trace_cap = h->trace_cap;
+  a.trace_rec0 = h->trace_rec0;
   a.serial_K = 1;
   return a;
 }
@@ -516,9 +517,16 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
 
 moe_status moe_set_trace(moe_handle* h, void* buf, int64_t bytes) {
   if (!h) return fail(MOE_ERR_INVALID_ARG, "handle is NULL");
-  if (buf && bytes < 96) return fail(MOE_ERR_INVALID_ARG, "trace buffer needs at least 96 bytes");
+  // header, one record count per wavefront of the launch (64-byte aligned),
+  // then one segment of trace_cap records per wavefront
+  const int64_t nseg = (int64_t)h->N * (FNTH / WAVE);
+  const int64_t hdr = TRACE_HDR + (4 * nseg + 63) / 64 * 64;
+  if (buf && bytes < hdr + 32 * nseg)
+    return fail(MOE_ERR_INVALID_ARG, "trace buffer needs at least %lld bytes (one record per wavefront)",
+                (long long)(hdr + 32 * nseg));
   h->trace = static_cast<long long*>(buf);
-  h->trace_cap = buf ? (int)std::min<int64_t>((bytes - 64) / 32, 1 << 30) : 0;
+  h->trace_rec0 = (int)(hdr / 8);
+  h->trace_cap = buf ? (int)std::min<int64_t>((bytes - hdr) / 32 / nseg, 1 << 20) : 0;
   return MOE_OK;
 }
 
@@ -547,7 +555,6 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     serial_combine_kernel<<<h->N, FNTH, 0, s>>>(a);
     HIP_TRY(hipGetLastError());
   } else {
-    if (h->trace) zero_i32_kernel<<<1, 64, 0, s>>>(reinterpret_cast<int32_t*>(h->trace), 2);
     void* args[] = {&a};
     HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(FNTH), args, 0, s));
   }

@@ -53,6 +53,10 @@ constexpr int CTL_READY = CTL_QD + NSHARD * CTL_PAD;  // [mt_max] dispatched row
 static_assert(CTL_QC + NSHARD * CTL_PAD <= CTL_QD, "control block overlap");
 static_assert(CTL_QD + NSHARD * CTL_PAD <= CTL_READY, "control block overlap");
 
+// timeline trace buffer: header word 0 holds this tag (format of the layout below)
+constexpr int TRACE_MAGIC = 0x31435254;  // "TRC1"
+constexpr int TRACE_HDR = 64;            // header bytes; per-segment counts follow
+
 // stats words written by the table builder
 constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;
 // written by the gate: candidates whose defined logit was evaluated (all tokens)

@@ -54,6 +54,7 @@ struct Scratch {
   int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
   int dexh;              // every dispatch unit has been claimed (seen by this workgroup)
   int ticket;            // this workgroup's arrival ticket (trace records)
+  int tcnt[NWF];         // trace records written by each wavefront
   float wwt[NWF][WAVE];  // per wavefront: their weights
 };
 
@@ -210,13 +211,17 @@ __device__ __forceinline__ int xcd_id() {
   return v;
 }
 
-// one lane appends one record
-__device__ __forceinline__ void trace_rec(const FwdArgs& a, int kind, int ticket, long long id, uint64_t t0,
-                                          uint64_t t1, uint64_t t2) {
+// One lane of a wavefront appends one record to the wavefront's own segment
+// of the trace buffer (segment blockIdx.x * NWF + wave, trace_cap records):
+// a per-wavefront LDS counter, no global atomics, so tracing does not
+// serialise the workgroups on a shared counter.
+__device__ __forceinline__ void trace_rec(const FwdArgs& a, Scratch& W, int kind, int ticket, long long id,
+                                          uint64_t t0, uint64_t t1, uint64_t t2) {
   if (!a.trace) return;
-  const unsigned long long slot = atomicAdd(reinterpret_cast<unsigned long long*>(a.trace), 1ull);
-  if (slot >= (unsigned long long)a.trace_cap) return;
-  long long* r = a.trace + 8 + 4 * slot;
+  const int wv = wave_id();
+  const int slot = W.tcnt[wv]++;
+  if (slot >= a.trace_cap) return;
+  long long* r = a.trace + a.trace_rec0 + ((size_t)(blockIdx.x * NWF + wv) * a.trace_cap + slot) * 4;
   r[0] = (long long)kind | ((long long)ticket << 8) | ((long long)xcd_id() << 20) | (id << 32);
   r[1] = (long long)t0;
   r[2] = (long long)t1;
@@ -357,7 +362,7 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
   if constexpr (SIG) {
     const uint64_t tr1 = a.trace ? now_ticks() : 0;
     dispatch_count(a, S, u, cur);
-    if (a.trace && lane_id() == 0) trace_rec(a, 5, W.ticket, u | ((long long)wave_id() << 24), tr0, tr1, now_ticks());
+    if (a.trace && lane_id() == 0) trace_rec(a, W, 5, W.ticket, u | ((long long)wave_id() << 24), tr0, tr1, now_ticks());
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -939,7 +944,7 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
     }
     if (threadIdx.x == 0) {
       if (publish) fetch_add_relaxed(&a.ctl[CTL_READY + ((r.ph == 0 ? 1 : 2) * a.mt_max + id) * CTL_PAD], 1);
-      if (a.trace) trace_rec(a, 2, ticket, t, t0, t1, now_ticks());
+      if (a.trace) trace_rec(a, W, 2, ticket, t, t0, t1, now_ticks());
     }
     t = __builtin_amdgcn_readfirstlane(W.bc[1]);  // rewritten only after the next mainloop's barriers
   }
@@ -967,7 +972,7 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
     uint64_t t1 = t0;
     const int g0 = u * a.ct;
     if (!combine_tokens(a, &S, W, g0, min(a.ct, a.T - g0), t1)) return false;
-    if (a.trace && lane_id() == 0) trace_rec(a, 4, ticket, u | ((long long)wave_id() << 24), t0, t1, now_ticks());
+    if (a.trace && lane_id() == 0) trace_rec(a, W, 4, ticket, u | ((long long)wave_id() << 24), t0, t1, now_ticks());
   }
 }
 
@@ -993,6 +998,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   prologue_plan(a, sub, S, W);
   build_sched(a, sub, S, W, S.K);
 
+  if (tid < NWF) W.tcnt[tid] = 0;
   if (tid == 0) {
     W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
     W.ticket = W.bc[0];
@@ -1016,7 +1022,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
     // dispatch: every token row, in token (hence chunk) order
     dispatch_claimed(a, S, W);
     __syncthreads();
-    if (a.trace && tid == 0) trace_rec(a, 3, ticket, 0, t_sched, now_ticks(), 0);
+    if (a.trace && tid == 0) trace_rec(a, W, 3, ticket, 0, t_sched, now_ticks(), 0);
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
     ok = compute_tiles(a, S, W, ring, ticket, S.n_steal);
     if (ok) combine_claimed(a, S, W, ticket);
@@ -1028,7 +1034,17 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   }
   if (a.trace) {
     __syncthreads();
-    if (tid == 0) trace_rec(a, 1, ticket, mover ? 1 : 0, t_entry, t_sched, now_ticks());
+    if (tid == 0) trace_rec(a, W, 1, ticket, mover ? 1 : 0, t_entry, t_sched, now_ticks());
+    __syncthreads();
+    // each wavefront's record count, and (block 0) the header
+    int* hdr = reinterpret_cast<int*>(a.trace);
+    if (tid < NWF) hdr[TRACE_HDR / 4 + blockIdx.x * NWF + tid] = min(W.tcnt[tid], a.trace_cap);
+    if (blockIdx.x == 0 && tid == 0) {
+      hdr[1] = (int)gridDim.x * NWF;
+      hdr[2] = a.trace_cap;
+      hdr[3] = a.trace_rec0;
+      hdr[0] = TRACE_MAGIC;
+    }
   }
 }
 

@@ -95,8 +95,9 @@ struct FwdArgs {
   uint16_t* O;
   float* part;    // split-K partials of GEMM1, fp32 [nsplit][prow][H] (nsplit > 1)
   size_t prow;    // rows per split in part (the capacity of O)
-  long long* trace;  // timeline records (NULL: off); word 0 counts records
-  int trace_cap;     // records that fit
+  long long* trace;  // timeline buffer (NULL: off), see moe_set_trace
+  int trace_cap;     // records per wavefront segment
+  int trace_rec0;    // int64 word offset of the first segment
   // control
   int32_t* ctl;       // this launch's control set
   int32_t* ctl_next;  // cleared for the next launch

@@ -103,6 +103,20 @@ def test_calls_without_workspace_fail_cleanly():
         B.moe_destroy(h)
 
 
+def test_trace_buffer_must_hold_a_record_per_wavefront():
+    h = B.moe_init(cfg_for(W.TINY))  # 256 workers x 8 wavefronts
+    try:
+        lib = B.library()
+        need = 64 + 4 * 2048 + 32 * 2048
+        with pytest.raises(B.MoeError) as ei:
+            B._check("moe_set_trace", lib.moe_set_trace(h, C.c_void_p(1 << 20), need - 1))
+        assert ei.value.status == B.MOE_ERR_INVALID_ARG
+        B._check("moe_set_trace", lib.moe_set_trace(h, C.c_void_p(1 << 20), need))
+        B._check("moe_set_trace", lib.moe_set_trace(h, None, 0))
+    finally:
+        B.moe_destroy(h)
+
+
 def test_default_calibration_is_valid_and_static_split_is_deepep_fraction():
     h = B.moe_init(cfg_for(W.MIXTRAL_EP4))
     try:

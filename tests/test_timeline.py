@@ -64,3 +64,30 @@ def test_ablation_summary_table():
     assert "| w | 100.0 | 120.0 (c 32) | 90.0 | 130.0 | 110.0 (24) | -20.0% | +25.0% | +10.0% |" in md
     assert "| w | (32, 1) | 90.0 | (24, 1) | 88.0 | 2.3% |" in md
     assert "| w | full | 90.0% | 5.0% | 40.0% | 15.0 |" in md
+
+
+def test_read_trace_decodes_wavefront_segments():
+    torch = pytest.importorskip("torch")
+    B = pytest.importorskip("paper_2609_21483_amd.binding", reason="libmoe.so not built")
+    nseg, cap = 3, 2
+    hdr = 64 + ((4 * nseg + 63) // 64) * 64
+    buf = np.zeros(hdr + nseg * cap * 32, dtype=np.uint8)
+    buf[:16].view(np.int32)[:] = [B.TRACE_MAGIC, nseg, cap, hdr // 8]
+    buf[64:64 + 4 * nseg].view(np.int32)[:] = [1, 0, 5]  # the last count exceeds cap: cap records are kept
+    recs = buf[hdr:].view(np.int64).reshape(nseg, cap, 4)
+
+    def word0(kind, ticket, xcd, id_):
+        return kind | (ticket << 8) | (xcd << 20) | (id_ << 32)
+
+    recs[0, 0] = [word0(2, 7, 3, (1 << 24) | 5), 10, 20, 30]
+    recs[1, 0] = [word0(9, 9, 9, 9), 0, 0, 0]  # beyond segment 1's count: not a record
+    recs[2, 0] = [word0(5, 255, 7, 4 | (3 << 24)), 1, 2, 3]
+    recs[2, 1] = [word0(1, 4095, 0, 1), 4, 5, 6]
+    tr = B.read_trace(torch.from_numpy(buf))
+    assert list(tr["kind"]) == [2, 5, 1]
+    assert list(tr["ticket"]) == [7, 255, 4095]
+    assert list(tr["xcd"]) == [3, 7, 0]
+    assert list(tr["id"]) == [(1 << 24) | 5, 4 | (3 << 24), 1]
+    assert list(tr["t0"]) == [10, 1, 4] and list(tr["t2"]) == [30, 3, 6]
+    buf[:4] = 0  # no launch wrote the header
+    assert len(B.read_trace(torch.from_numpy(buf))) == 0
