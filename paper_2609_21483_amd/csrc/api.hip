@@ -173,7 +173,7 @@ void compute_layout(moe_handle* h) {
   L.sub_off = take(sizeof(int32_t) * (size_t)KOPT * El * SUBW);
   L.cnt_rank = take(sizeof(int32_t) * (size_t)El * R);
   L.uniq = take(sizeof(int32_t) * (size_t)R);
-  L.stats = take(sizeof(int32_t) * 16);
+  L.stats = take(sizeof(int32_t) * ST_WORDS);
   L.plan = take(sizeof(moe_plan));
   L.err = take(sizeof(int32_t) * 4);
   h->off_calib = take(sizeof(DevCalib));
@@ -230,6 +230,8 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
   a.e0 = h->cfg.first_local_expert;
   a.El = h->cfg.n_local_experts;
   a.nblk = h->nblk;
+  a.S = h->cfg.n_shared_experts;
+  a.tiles_per_row_tile = h->nt0 + h->nt1 * h->nsplit;
   return a;
 }
 

@@ -61,6 +61,10 @@ constexpr int TRACE_HDR = 64;            // header bytes; per-segment counts fol
 constexpr int ST_X = 0, ST_XLOCAL = 1, ST_XIN = 2, ST_ULOCAL = 3, ST_UIN = 4, ST_BADIDS = 5;
 // written by the gate: candidates whose defined logit was evaluated (all tokens)
 constexpr int ST_CANDS = 8;
+// written by the table builder: GEMM tiles of the layer at each stored chunk
+// option (KOPT words; the cost model's tile counts, Eq 14)
+constexpr int ST_NTK = 10;
+constexpr int ST_WORDS = 16;
 
 // device error word values
 constexpr int ERR_TIMEOUT = 1;

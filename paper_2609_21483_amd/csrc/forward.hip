@@ -46,9 +46,8 @@ struct Sched {
 
 struct Scratch {
   int bc[8];
-  long long ntk[KOPT];
   DevCalib cal;                                        // the calibration table, staged by the prologue
-  int st[8];                                           // routing stats (ST_*), staged by the prologue
+  int st[ST_WORDS];                                    // routing stats (ST_*), staged by the prologue
   int part[NWF];
   int wsl[NWF][WAVE];    // per wavefront: slots of its unit's (token, j) pairs
   int wact[NWF][DT];     // per wavefront: its dispatch unit's tokens that have a local slot
@@ -135,11 +134,12 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, Sc
   const int ki = kopt_index(K);
   const int nseg = a.El + a.S;
   const int g1tiles = a.nt1 * a.nsplit;  // GEMM1 tiles per row tile
+  // chunk token boundaries ceil(q T / K); K is 1, 2, 4 or 8
+  if (tid <= K) S.bnd[tid] = (int)(((long long)tid * a.T + K - 1) >> __builtin_ctz((unsigned)K));
   if (tid == 0) {
     S.K = K;
     S.nseg = nseg;
     S.G = K * 2 * nseg;
-    for (int q = 0; q <= K; ++q) S.bnd[q] = (int)(((long long)q * a.T + K - 1) / K);
     S.n_comb = ceil_div(a.T, a.ct);
     S.n_disp = ceil_div(a.T, a.dt);
   }
@@ -752,37 +752,13 @@ __device__ __forceinline__ bool arrive_and_reduce(const FwdArgs& a, const Sched&
 // ===========================================================================
 // sub: the chunk sub-offset tables staged in LDS (see moe_megakernel); the
 // calibration table is staged here, in the same round trip.
-__device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, Sched& S, Scratch& W) {
+__device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   const int tid = threadIdx.x;
-  const int nseg = a.El + a.S;
-  if (tid < KOPT) W.ntk[tid] = 0;
   {
     const uint32_t* src = reinterpret_cast<const uint32_t*>(a.calib);
     uint32_t* dst = reinterpret_cast<uint32_t*>(&W.cal);
     for (int i = tid; i < (int)(sizeof(DevCalib) / 4); i += FNTH) dst[i] = src[i];
-    if (tid >= FNTH - 8) W.st[tid - (FNTH - 8)] = a.stats[tid - (FNTH - 8)];
-  }
-  __syncthreads();
-  // GEMM tiles at each stored chunk option (for W_tile of Eq 14)
-  for (int ki = 0; ki < KOPT; ++ki) {
-    const int K = kopt_value(ki);
-    long long part = 0;
-    for (int v = tid; v < K * nseg; v += FNTH) {
-      int q = v / nseg, seg = v % nseg;
-      int rows;
-      if (seg < a.El) {
-        const int* so = sub + ((size_t)ki * a.El + seg) * SUBW;
-        rows = so[q + 1] - so[q];
-      } else {
-        int t0 = (int)(((long long)q * a.T + K - 1) / K);
-        int t1 = min((int)(((long long)(q + 1) * a.T + K - 1) / K), a.Tr);
-        rows = max(0, t1 - t0);
-      }
-      part += (long long)ceil_div(rows, BM) * (a.nt0 + a.nt1 * a.nsplit);
-    }
-    // one LDS atomic per wavefront (same-address atomics serialise)
-    for (int d = WAVE / 2; d >= 1; d >>= 1) part += __shfl_xor(part, d, WAVE);
-    if ((tid & (WAVE - 1)) == 0 && part) atomicAdd((unsigned long long*)&W.ntk[ki], (unsigned long long)part);
+    if (tid >= FNTH - ST_WORDS) W.st[tid - (FNTH - ST_WORDS)] = a.stats[tid - (FNTH - ST_WORDS)];
   }
   __syncthreads();
   const bool model = !a.forced && a.mode != MOE_MODE_STATIC;
@@ -819,7 +795,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, const int* sub, 
     } else {
       const int nk = W.cal.n_k;
       long long nt_by_k[MOE_CALIB_MAX_K];
-      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.ntk[kopt_index(W.cal.kk[j])];
+      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.st[ST_NTK + kopt_index(W.cal.kk[j])];
       cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &p);
     }
     S.c = p.c;
@@ -990,19 +966,25 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   if (blockIdx.x == 0)
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
 
+  // arrival ticket (role) first, so that its round trip overlaps the staging
+  int tk = 0;
+  if (tid == 0) {
+    tk = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
+    W.dexh = 0;
+  }
+
   // the chunk sub-offset tables, staged in the GEMM ring (idle until the
-  // first tile) so that plan and schedule read them from LDS
+  // first tile) so that the schedule reads them from LDS
   static_assert(KOPT * MAX_EL * SUBW * (int)sizeof(int) <= gemm::RING_BYTES, "sub-offset tables fit the ring");
   int* sub = reinterpret_cast<int*>(ring);
   for (int i = tid; i < KOPT * a.El * SUBW; i += FNTH) sub[i] = a.sub_off[i];
-  prologue_plan(a, sub, S, W);
+  if (tid == 0) W.bc[0] = tk;
+  prologue_plan(a, S, W);
   build_sched(a, sub, S, W, S.K);
 
   if (tid < NWF) W.tcnt[tid] = 0;
   if (tid == 0) {
-    W.bc[0] = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);
     W.ticket = W.bc[0];
-    W.dexh = 0;
     S.disp0 = min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF);
   }
   __syncthreads();

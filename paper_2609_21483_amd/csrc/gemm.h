@@ -244,7 +244,7 @@ struct OutMap {
   int row_l, col_l;
 };
 __device__ __forceinline__ OutMap out_map(int cols_per_wave) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
   const int wm = wave % WM, wn = wave / WM;
   return {wm * TM + 4 * (lane >> 5), wn * cols_per_wave + (lane & 31)};
 }

@@ -40,6 +40,7 @@ struct TableArgs {
   int32_t* blk_off;
   int32_t* err;
   int T, Tr, R, k, E, e0, El, nblk;
+  int S, tiles_per_row_tile;  // shared experts; GEMM0 + GEMM1 tiles of one row tile (the cost model's tile counts)
 };
 
 struct PackArgs {

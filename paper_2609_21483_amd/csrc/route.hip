@@ -504,8 +504,10 @@ __device__ inline int seg_lower_bound(const TableArgs& a, int le, long long b) {
 
 __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
   __shared__ int uq[64];
+  __shared__ int ntk[KOPT];
   const int tid = threadIdx.x;
   for (int r = tid; r < a.R; r += NTH) uq[r] = 0;
+  if (tid < KOPT) ntk[tid] = 0;
   __syncthreads();
   // per-(expert, rank) counts: rank r owns tokens [r*Tr, (r+1)*Tr)
   for (int v = tid; v < a.El * a.R; v += NTH) {
@@ -526,6 +528,28 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     }
     a.sub_off[v] = val;
   }
+  __syncthreads();  // the block's sub_off stores are visible to the block
+  // GEMM tiles of the layer at each chunk option: every (chunk, segment)
+  // contributes ceil(rows / BM) row tiles of GEMM0 + GEMM1 tiles; shared
+  // experts take rank 0's tokens of the chunk
+  for (int ki = 0; ki < KOPT; ++ki) {
+    const int K = kopt_value(ki), nseg = a.El + a.S;
+    int part = 0;
+    for (int v = tid; v < K * nseg; v += NTH) {
+      const int q = v / nseg, seg = v % nseg;
+      int rows;
+      if (seg < a.El) {
+        const int* so = a.sub_off + ((size_t)ki * a.El + seg) * SUBW;
+        rows = so[q + 1] - so[q];
+      } else {
+        const int t0 = (int)(((long long)q * a.T + K - 1) / K);
+        const int t1 = min((int)(((long long)(q + 1) * a.T + K - 1) / K), a.Tr);
+        rows = max(0, t1 - t0);
+      }
+      part += (rows + BM - 1) / BM * a.tiles_per_row_tile;
+    }
+    if (part) atomicAdd(&ntk[ki], part);
+  }
   // unique tokens per rank (tokens with at least one local pair)
   for (int g = tid; g < a.T; g += NTH)
     if (a.first_slot[g] >= 0) atomicAdd(&uq[g / a.Tr], 1);
@@ -543,6 +567,7 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     a.stats[ST_XIN] = X - xl;
     a.stats[ST_ULOCAL] = uq[0];
     a.stats[ST_UIN] = uin;
+    for (int ki = 0; ki < KOPT; ++ki) a.stats[ST_NTK + ki] = ntk[ki];
   }
 }
 
