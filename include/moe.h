@@ -132,7 +132,10 @@ typedef struct {
   size_t sub_off;     /* int32 [4][E_l][9]: chunk offsets for K = 1,2,4,8 */
   size_t cnt_rank;    /* int32 [E_l][R] */
   size_t uniq;        /* int32 [R] */
-  size_t stats;       /* int32 [16]: X, X_local, X_in, U_local, U_in, ... */
+  size_t stats;       /* int32 [16]: X, X_local, X_in, U_local, U_in, bad ids (0-5);
+                         gate candidates (8); GEMM tiles of the layer at
+                         K = 1, 2, 4, 8 chunks (10-13), written by the table
+                         builder for the cost model (section 3.2, Eq 14) */
   size_t plan;        /* moe_plan of the last megakernel launch */
   size_t err;         /* int32 device error word */
   size_t A;           /* bf16 [X_max + pad][H]: dispatched rows */
