@@ -247,7 +247,13 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
  * regions, y[g] = sum over local j of topk_w[g,j] * FFN(x[g]) (+ the shared
  * experts for rank-0 tokens), 0 for tokens with no local expert.
  * mode: a moe_mode.  forced: host plan overriding the cost model (c, K,
- * n_steal, final_all) in the megakernel modes, or NULL. */
+ * n_steal, final_all) in the megakernel modes, or NULL.
+ * The megakernel modes launch one persistent kernel of n_workers workgroups
+ * that wait on each other, as an ordinary launch on `stream`: all of them
+ * must be resident at once (the first call checks that the GPU holds them:
+ * else MOE_ERR_UNSUPPORTED), and work on other streams that holds CUs while
+ * it runs can keep workers from starting; the waiting ones then stop at the
+ * timeout (moe_set_timeout_ms) with MOE_ERR_TIMEOUT. */
 moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx,
                        const float* topk_w, const void* packed, uint16_t* y,
                        int32_t mode, const moe_plan* forced, void* stream);

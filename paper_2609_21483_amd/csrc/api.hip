@@ -55,6 +55,7 @@ struct moe_handle {
   int inject_stall = 0;
   long long* trace = nullptr;
   int trace_cap = 0, trace_rec0 = 0;
+  bool resident_ok = false;  // the megakernel's N workgroups fit the GPU at once
 };
 
 namespace {
@@ -557,8 +558,24 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     serial_combine_kernel<<<h->N, FNTH, 0, s>>>(a);
     HIP_TRY(hipGetLastError());
   } else {
-    void* args[] = {&a};
-    HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&moe_megakernel), dim3(h->N), dim3(FNTH), args, 0, s));
+    // a persistent kernel: its N workgroups wait on each other, so all of
+    // them must be resident at once (checked once per handle).  It is an
+    // ordinary launch: on an otherwise idle GPU one workgroup lands on each
+    // CU; a cooperative launch would hold it until all earlier work on the
+    // device has drained (~20 us a layer).
+    if (!h->resident_ok) {
+      int dev = 0, cus = 0, per_cu = 0;
+      HIP_TRY(hipGetDevice(&dev));
+      HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+      HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&moe_megakernel),
+                                                           FNTH, 0));
+      if ((long long)cus * per_cu < h->N)
+        return fail(MOE_ERR_UNSUPPORTED, "n_workers = %d exceeds the %lld workgroups the GPU holds at once", h->N,
+                    (long long)cus * per_cu);
+      h->resident_ok = true;
+    }
+    moe_megakernel<<<h->N, FNTH, 0, s>>>(a);
+    HIP_TRY(hipGetLastError());
   }
   h->launch_seq++;
   return MOE_OK;

@@ -953,8 +953,11 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
 }
 
 // ===========================================================================
-// The persistent megakernel: one workgroup per CU, co-resident (cooperative
-// launch).  The first c workgroups to arrive become movement workers.
+// The persistent megakernel: one workgroup per CU, all resident at once (the
+// host checks that the GPU holds N of them).  The first c workgroups to
+// arrive become movement workers.  Every wait ends at the abort word or the
+// timeout, so workers that cannot start (the CUs held by other work) turn
+// into MOE_ERR_TIMEOUT, never a hang.
 // ===========================================================================
 __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   __shared__ Sched S;
