@@ -25,6 +25,7 @@ constexpr int TILE_M = 256, TILE_N = 256, KSTEP = 32, NSTAGE = 4;
 constexpr int NWAVE = 8, WM = 2, WN = 4;
 constexpr int TM = TILE_M / WM, TN = TILE_N / WN;   // 128 x 64 per wave
 constexpr int MB = TM / 32, NB = TN / 32;           // 4 x 2 MFMA blocks
+static_assert(MB == 4, "mainloop dispatches on 0..4 active row blocks");
 constexpr int A_BYTES = TILE_M * KSTEP * 2, B_BYTES = TILE_N * KSTEP * 2;
 constexpr int STAGE_BYTES = A_BYTES + B_BYTES;      // 32 KiB
 constexpr int RING_BYTES = NSTAGE * STAGE_BYTES;    // 128 KiB
@@ -156,27 +157,35 @@ __device__ __forceinline__ FragOff frag_offsets() {
 
 // 32-row blocks are 2048 bytes apart and keep the same swizzle, so every
 // fragment of a slice is a constant offset from the lane's base
+// The fragments and MFMAs of the first MBA 32-row blocks of the wave's rows
+// (the blocks that hold valid rows of the tile; see mainloop)
+template <int MBA>
 __device__ __forceinline__ void load_frags(const char* stage, int kk, const FragOff& fo, bf16x8_t (&af)[MB],
                                            bf16x8_t (&bfr)[NB]) {
-  const char* pa = stage + fo.a[kk];
-  const char* pb = stage + fo.b[kk];
+  if constexpr (MBA > 0) {
+    const char* pa = stage + fo.a[kk];
+    const char* pb = stage + fo.b[kk];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(pa + mb * 2048);
+    for (int mb = 0; mb < MBA; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(pa + mb * 2048);
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(pb + nb * 2048);
+    for (int nb = 0; nb < NB; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(pb + nb * 2048);
+  }
 }
 
+template <int MBA>
 __device__ __forceinline__ void mfma_block(Acc& acc, const bf16x8_t (&af)[MB], const bf16x8_t (&bfr)[NB]) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+  for (int mb = 0; mb < MBA; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
       acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
 }
 
-// acc += A[0..a_rows) . B[0..b_rows)^T over k in [0, Kd); Kd % 32 == 0.
-// ring: RING_BYTES of LDS.  Ends with a barrier (the ring may be reused).
-__device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int ldb,
+// The mainloop of a wave that computes its first MBA 32-row blocks.  Every
+// instance issues the same DMA and passes the same barriers, so the waves of
+// a workgroup may run different instances.
+template <int MBA>
+__device__ __forceinline__ void mainloop_mb(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int ldb,
                                          int b_rows, int Kd, char* ring) {
   const int nk = Kd / KSTEP;
   DmaOff o;
@@ -202,31 +211,51 @@ __device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, i
   compiler_fence();
   bf16x8_t fa0[MB], fb0[NB], fa1[MB], fb1[NB];
   const FragOff fo = frag_offsets();
-  load_frags(st(0), 0, fo, fa0, fb0);
+  load_frags<MBA>(st(0), 0, fo, fa0, fb0);
   int s = 0;
   for (; s < nk - 3; ++s) {  // steady state: the stage 3 ahead is always issued
-    load_frags(st(s), 1, fo, fa1, fb1);
-    mfma_block(acc, fa0, fb0);
+    load_frags<MBA>(st(s), 1, fo, fa1, fb1);
+    mfma_block<MBA>(acc, fa0, fb0);
     wait_vm<INSTR>();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(s + 3);
-    load_frags(st(s + 1), 0, fo, fa0, fb0);
-    mfma_block(acc, fa1, fb1);
+    load_frags<MBA>(st(s + 1), 0, fo, fa0, fb0);
+    mfma_block<MBA>(acc, fa1, fb1);
   }
   for (; s < nk; ++s) {  // drain
-    load_frags(st(s), 1, fo, fa1, fb1);
-    mfma_block(acc, fa0, fb0);
+    load_frags<MBA>(st(s), 1, fo, fa1, fb1);
+    mfma_block<MBA>(acc, fa0, fb0);
     if (s + 1 < nk) {
       if (s + 2 < nk) wait_vm<INSTR>(); else wait_vm<0>();
       __builtin_amdgcn_s_barrier();
       compiler_fence();
-      load_frags(st(s + 1), 0, fo, fa0, fb0);
+      load_frags<MBA>(st(s + 1), 0, fo, fa0, fb0);
     }
-    mfma_block(acc, fa1, fb1);
+    mfma_block<MBA>(acc, fa1, fb1);
   }
   __builtin_amdgcn_s_barrier();
   compiler_fence();
+}
+
+// acc += A[0..a_rows) . B[0..b_rows)^T over k in [0, Kd); Kd % 32 == 0.
+// ring: RING_BYTES of LDS.  Ends with a barrier (the ring may be reused).
+// A wave computes only the 32-row blocks of its rows that hold valid rows
+// (a_rows): the last row tile of an expert is often nearly empty, and its
+// padding rows would otherwise cost as much MFMA work as valid ones.  Their
+// accumulators stay zero and are never stored.
+__device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int ldb,
+                                         int b_rows, int Kd, char* ring) {
+  const int wm = opaque((int)(threadIdx.x >> 6)) % WM;
+  const int left = opaque(a_rows) - wm * TM;
+  const int mba = left <= 0 ? 0 : (left >= TM ? MB : (left + 31) / 32);
+  switch (mba) {
+    case MB: mainloop_mb<MB>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
+    case 3: mainloop_mb<3>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
+    case 2: mainloop_mb<2>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
+    case 1: mainloop_mb<1>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
+    default: mainloop_mb<0>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
+  }
 }
 
 __device__ __forceinline__ void zero(Acc& acc) {
