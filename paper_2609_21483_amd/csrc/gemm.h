@@ -3,6 +3,9 @@
 //
 // Workgroup of 8 wave64s (2 per SIMD), wave grid 2 (rows) x 4 (columns), each
 // wave owns 128 x 64 outputs = 4 x 2 MFMA blocks (128 accumulator registers).
+// The tile's eight 32-row blocks alternate between the two wave rows (wave
+// row wm takes blocks wm, wm + 2, wm + 4, wm + 6), so a partly filled row
+// tile spreads its valid rows over all four SIMDs.
 // A and B stream through a 4-stage LDS ring of BK = 32 deep stages filled by
 // direct global->LDS loads (global_load_lds_dwordx4), issued 3 stages ahead.
 // Rows are 64 bytes; their 16-byte granules are XOR-swizzled by (row >> 1) & 3
@@ -144,7 +147,7 @@ struct FragOff {
 __device__ __forceinline__ FragOff frag_offsets() {
   const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
   const int wm = wave % WM, wn = wave / WM;
-  const int ra = wm * TM + (lane & 31), rb = wn * TN + (lane & 31);
+  const int ra = wm * 32 + (lane & 31), rb = wn * TN + (lane & 31);
   FragOff f;
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
@@ -155,10 +158,10 @@ __device__ __forceinline__ FragOff frag_offsets() {
   return f;
 }
 
-// 32-row blocks are 2048 bytes apart and keep the same swizzle, so every
-// fragment of a slice is a constant offset from the lane's base
-// The fragments and MFMAs of the first MBA 32-row blocks of the wave's rows
-// (the blocks that hold valid rows of the tile; see mainloop)
+// A wave's 32-row blocks are 64 rows (4096 bytes) apart and keep the same
+// swizzle, so every fragment of a slice is a constant offset from the lane's
+// base.  These load and multiply the first MBA blocks of the wave's rows (the
+// blocks that hold valid rows of the tile; see mainloop).
 template <int MBA>
 __device__ __forceinline__ void load_frags(const char* stage, int kk, const FragOff& fo, bf16x8_t (&af)[MB],
                                            bf16x8_t (&bfr)[NB]) {
@@ -166,7 +169,7 @@ __device__ __forceinline__ void load_frags(const char* stage, int kk, const Frag
     const char* pa = stage + fo.a[kk];
     const char* pb = stage + fo.b[kk];
 #pragma unroll
-    for (int mb = 0; mb < MBA; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(pa + mb * 2048);
+    for (int mb = 0; mb < MBA; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(pa + mb * (WM * 2048));
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(pb + nb * 2048);
   }
@@ -247,8 +250,8 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const uint16_t* A, int lda
 __device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int ldb,
                                          int b_rows, int Kd, char* ring) {
   const int wm = opaque((int)(threadIdx.x >> 6)) % WM;
-  const int left = opaque(a_rows) - wm * TM;
-  const int mba = left <= 0 ? 0 : (left >= TM ? MB : (left + 31) / 32);
+  const int left = opaque(a_rows) - wm * 32;  // valid rows from the wave's first block on
+  const int mba = left <= 0 ? 0 : min(MB, (left + WM * 32 - 1) / (WM * 32));
   switch (mba) {
     case MB: mainloop_mb<MB>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
     case 3: mainloop_mb<3>(acc, A, lda, a_rows, B, ldb, b_rows, Kd, ring); break;
@@ -275,9 +278,9 @@ struct OutMap {
 __device__ __forceinline__ OutMap out_map(int cols_per_wave) {
   const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
   const int wm = wave % WM, wn = wave / WM;
-  return {wm * TM + 4 * (lane >> 5), wn * cols_per_wave + (lane & 31)};
+  return {wm * 32 + 4 * (lane >> 5), wn * cols_per_wave + (lane & 31)};
 }
-__device__ __forceinline__ int out_dr(int mb, int r) { return mb * 32 + 8 * (r >> 2) + (r & 3); }
+__device__ __forceinline__ int out_dr(int mb, int r) { return mb * (WM * 32) + 8 * (r >> 2) + (r & 3); }
 
 // Epilogues write through 16- or 32-bit buffer stores.  With CP = SC1 the
 // stores are agent-coherent: once they have completed (vmcnt 0) every XCD can
