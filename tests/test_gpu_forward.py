@@ -209,6 +209,32 @@ def test_relaunch_with_new_inputs(B):
         layer.close()
 
 
+def test_more_workers_than_the_gpu_holds_is_refused(B):
+    """The megakernel's workgroups wait on each other, so all of them must be
+    resident at once: a worker count beyond what the GPU holds is refused
+    before any launch (one workgroup fits a CU)."""
+    c = make_case(W.TINY)
+    idx, w = c.oracle_route()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    layer = B.MoeLayer(c.shape, c.w1, c.w3, c.w2, n_workers=2 * cus)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(idx).cuda()
+        w_d = torch.from_numpy(w.astype(np.float32)).cuda()
+        B.moe_build_tables(layer.h, idx_d)
+        y = torch.zeros((c.shape.T, c.shape.hidden), dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(B.MoeError) as ei:
+            layer.forward(x, idx_d, w_d, y, "dynamic")
+        assert ei.value.status == B.MOE_ERR_UNSUPPORTED
+        assert "holds at once" in B.moe_last_error()
+        # the serial kernels have no such constraint
+        layer.forward(x, idx_d, w_d, y, "serial")
+        assert B.moe_sync_status(layer.h) == B.MOE_OK
+        assert rel_err(bf16_to_f64(y), oracle_rows(c, idx, w, np.arange(c.shape.T))) <= TOL
+    finally:
+        layer.close()
+
+
 def test_timeout_path_recovers(B):
     """Host-forced stall: every wait targets an unreachable value, so the
     launch times out on its own bounded waits, reports MOE_ERR_TIMEOUT, and the
