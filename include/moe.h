@@ -209,11 +209,16 @@ moe_status moe_workspace_layout(const moe_handle* h, moe_ws_layout* out);
  * workspace must stay alive and unused by others while the handle uses it. */
 moe_status moe_set_workspace(moe_handle* h, void* ws, size_t bytes, void* stream);
 
-/* Size of the packed expert weights: (E_l + S) * 3 * H * F * 2 bytes. */
+/* Size of the packed expert weights: (E_l + S) * (R(2F) * H + R(H) * F) * 2
+ * bytes, R(n) = n rounded up to a multiple of 256 (the operand slabs of the
+ * GEMM tiles are padded to 256 rows). */
 moe_status moe_packed_weights_size(const moe_handle* h, size_t* bytes);
 
 /* Packs the expert weights into the GEMM operand layout (not part of the
- * layer; done once).  w1, w3: bf16 [E_l][H][F] (gate, up), w2: bf16
+ * layer; done once): each matrix is transposed to k-contiguous rows and
+ * stored as 256-row slabs, one 256 x 32 block per 32-deep k-step, so that
+ * the GEMM tiles stream whole blocks.  The layout is internal to the
+ * library.  w1, w3: bf16 [E_l][H][F] (gate, up), w2: bf16
  * [E_l][F][H] (down); ws1, ws3, ws2 the same for the S shared experts (NULL
  * when S = 0).  packed: device buffer of moe_packed_weights_size bytes. */
 moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w3,

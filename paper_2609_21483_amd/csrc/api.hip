@@ -275,7 +275,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.topk_idx = topk_idx;
   a.topk_w = topk_w;
   a.w13 = static_cast<const uint16_t*>(packed);
-  a.w2t = a.w13 + (size_t)h->nseg * 2 * c.ffn * c.hidden;
+  a.w2t = a.w13 + (size_t)h->nseg * slab_rows(2 * c.ffn) * c.hidden;
   a.y = y;
   a.slot = at<int32_t>(h, h->lay.slot);
   a.sub_off = at<int32_t>(h, h->lay.sub_off);
@@ -421,7 +421,8 @@ moe_status moe_set_workspace(moe_handle* h, void* ws, size_t bytes, void* stream
 
 moe_status moe_packed_weights_size(const moe_handle* h, size_t* bytes) {
   if (!h || !bytes) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
-  *bytes = (size_t)h->nseg * 3 * (size_t)h->cfg.hidden * h->cfg.ffn * sizeof(uint16_t);
+  const long long H = h->cfg.hidden, F = h->cfg.ffn;
+  *bytes = (size_t)h->nseg * (size_t)(slab_rows(2 * F) * H + slab_rows(H) * F) * sizeof(uint16_t);
   return MOE_OK;
 }
 
@@ -433,7 +434,7 @@ moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w
   if (S > 0 && (!ws1 || !ws3 || !ws2)) return fail(MOE_ERR_INVALID_ARG, "shared-expert weights are NULL");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint16_t* w13 = static_cast<uint16_t*>(packed);
-  uint16_t* w2t = w13 + (size_t)h->nseg * 2 * F * H;
+  uint16_t* w2t = w13 + (size_t)h->nseg * slab_rows(2 * F) * H;
   auto launch = [&](const uint16_t* src, uint16_t* dst, int nseg, int rows, int cols, long long stride,
                     int inter, int which) -> moe_status {
     if (nseg == 0) return MOE_OK;
@@ -443,8 +444,17 @@ moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w
     HIP_TRY(hipGetLastError());
     return MOE_OK;
   };
-  const long long s13 = 2LL * F * H, s2 = (long long)H * F;
+  const long long s13 = slab_rows(2 * F) * H, s2 = slab_rows(H) * F;
   moe_status st;
+  auto pad = [&](uint16_t* dst, int R, int K, long long stride) -> moe_status {
+    if (slab_rows(R) == R) return MOE_OK;
+    PadArgs a{dst, h->nseg, R, K, stride};
+    pack_pad_kernel<<<256, NTH, 0, s>>>(a);
+    HIP_TRY(hipGetLastError());
+    return MOE_OK;
+  };
+  if ((st = pad(w13, 2 * F, H, s13)) != MOE_OK) return st;
+  if ((st = pad(w2t, H, F, s2)) != MOE_OK) return st;
   if ((st = launch(w1, w13, El, H, F, s13, 1, 0)) != MOE_OK) return st;
   if ((st = launch(w3, w13, El, H, F, s13, 1, 1)) != MOE_OK) return st;
   if ((st = launch(w2, w2t, El, F, H, s2, 0, 0)) != MOE_OK) return st;

@@ -19,6 +19,18 @@ constexpr int BM = 256;
 constexpr int BN = 256;
 constexpr int MAX_SPLIT = 8;    // split-K factor limit of GEMM1
 
+// Packed expert weights are slab-tiled GEMM B operands: an [R][K] matrix
+// (R output columns, K deep) is stored as ceil(R / 256) slabs of 256 rows;
+// slab j holds its K / 32 k-steps one after the other, each a block of 256
+// rows x 32 bf16 (row r of the block at r * 64 bytes).  Rows past R are zero.
+constexpr int SLAB = 256;
+constexpr int SLAB_K = 32;
+__host__ __device__ inline long long slab_rows(long long R) { return (R + SLAB - 1) / SLAB * SLAB; }
+// element offset of (row n, column k) in a slab-tiled [R][K] matrix
+__host__ __device__ inline long long slab_index(long long n, long long k, long long K) {
+  return ((n / SLAB) * (K / SLAB_K) + k / SLAB_K) * (SLAB * SLAB_K) + (n % SLAB) * SLAB_K + k % SLAB_K;
+}
+
 constexpr int DT = 8;           // most tokens per dispatch unit (one wavefront; DT * top_k <= 64)
 constexpr int CT = 4;           // most tokens per combine unit (one wavefront)
 

@@ -646,25 +646,26 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
   const int n0 = r.nt * BN;
   const uint16_t* Aop;
   const uint16_t* Bop;
-  int ld, b_rows, Kd;
+  int ld, Kd;
+  // B: slab r.nt of the expert's slab-tiled weights (n0 is a multiple of the
+  // slab height, so the slab starts at element n0 * K), then the split's
+  // first k-step block
   if (r.ph == 0) {
     const size_t arow = (size_t)S.arow0[qs] + (size_t)r.mt * BM;
     Aop = (r.seg < a.El ? a.A : a.x) + arow * a.H;
-    Bop = a.w13 + ((size_t)r.seg * 2 * a.F + n0) * a.H;
+    Bop = a.w13 + (size_t)r.seg * slab_rows(2 * a.F) * a.H + (size_t)n0 * a.H;
     ld = a.H;
-    b_rows = 2 * a.F - n0;
     Kd = a.H;
   } else {
     const int kl = a.F / a.nsplit;
     Aop = a.Hb + orow * a.F + (size_t)r.ks * kl;
-    Bop = a.w2t + ((size_t)r.seg * a.H + n0) * a.F + (size_t)r.ks * kl;
+    Bop = a.w2t + (size_t)r.seg * slab_rows(a.H) * a.F + (size_t)n0 * a.F + (size_t)r.ks * kl * SLAB;
     ld = a.F;
-    b_rows = a.H - n0;
     Kd = kl;
   }
   gemm::Acc acc;
   gemm::zero(acc);
-  gemm::mainloop(acc, Aop, ld, r.rows, Bop, ld, b_rows, Kd, ring);
+  gemm::mainloop(acc, Aop, ld, r.rows, Bop, Kd, ring);
   int nxt = -1;
   if (threadIdx.x == 0) nxt = claim_next();
   if (r.ph == 0) {

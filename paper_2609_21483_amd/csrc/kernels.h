@@ -43,12 +43,20 @@ struct TableArgs {
   int S, tiles_per_row_tile;  // shared experts; GEMM0 + GEMM1 tiles of one row tile (the cost model's tile counts)
 };
 
+// One source matrix [rows][cols] per segment, written transposed into a
+// slab-tiled [R][rows] destination (R = cols, or 2 * cols interleaved).
 struct PackArgs {
   const uint16_t* src;
   uint16_t* dst;
   int rows, cols;
   long long seg_stride;
   int interleave, which;
+};
+// Zeroes rows [R, slab_rows(R)) of every segment's slab-tiled [R][K] matrix.
+struct PadArgs {
+  uint16_t* dst;
+  int nseg, R, K;
+  long long seg_stride;
 };
 
 // Calibration table as the kernels read it (copied into the workspace).
@@ -83,8 +91,8 @@ struct FwdArgs {
   const uint16_t* x;
   const int32_t* topk_idx;
   const float* topk_w;
-  const uint16_t* w13;  // packed [E_l+S][2F][H]
-  const uint16_t* w2t;  // packed [E_l+S][H][F]
+  const uint16_t* w13;  // packed [E_l+S] x slab-tiled [2F][H] (gate/up rows interleaved in groups of 32)
+  const uint16_t* w2t;  // packed [E_l+S] x slab-tiled [H][F]
   uint16_t* y;
   // routing tables
   const int32_t* slot;
@@ -217,6 +225,7 @@ __global__ void tab_perm_kernel(TableArgs a);
 __global__ void tab_finalize_kernel(TableArgs a);
 __global__ void zero_i32_kernel(int* p, int n);
 __global__ void pack_transpose_kernel(PackArgs a);
+__global__ void pack_pad_kernel(PadArgs a);
 __global__ void moe_megakernel(FwdArgs a);
 __global__ void serial_dispatch_kernel(FwdArgs a);
 __global__ void serial_gemm0_kernel(FwdArgs a);

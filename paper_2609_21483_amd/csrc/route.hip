@@ -577,10 +577,10 @@ __global__ void zero_i32_kernel(int* p, int n) {
 
 // ---------------------------------------------------------------------------
 // Weight packing (one-off, not part of the layer): transposes each expert's
-// [H][F] / [F][H] matrix into the k-contiguous GEMM operand layout.
+// [H][F] / [F][H] matrix into the slab-tiled GEMM B layout (common.h).
 // W1/W3 go to [2F][H] with 32-column groups interleaved (gate f..f+31, then
 // up f..f+31), so one 64-column slice of GEMM0 holds matching gate and up
-// columns; W2 goes to [H][F].
+// columns; W2 goes to [H][F].  pack_pad_kernel zeroes the slab padding.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(NTH) pack_transpose_kernel(PackArgs a) {
   __shared__ uint16_t tile[32][33];
@@ -598,8 +598,19 @@ __global__ void __launch_bounds__(NTH) pack_transpose_kernel(PackArgs a) {
     int c = c0 + i, r = r0 + tx;  // dst row index is the source column
     if (r < a.rows && c < a.cols) {
       int drow = a.interleave ? (c / 32) * 64 + a.which * 32 + (c % 32) : c;
-      dst[(size_t)drow * a.rows + r] = tile[tx][i];
+      dst[slab_index(drow, r, a.rows)] = tile[tx][i];
     }
+  }
+}
+
+__global__ void __launch_bounds__(NTH) pack_pad_kernel(PadArgs a) {
+  const int pad = (int)(slab_rows(a.R) - a.R);
+  const long long per_seg = (long long)pad * a.K;
+  for (long long v = (long long)blockIdx.x * NTH + threadIdx.x; v < per_seg * a.nseg; v += (long long)gridDim.x * NTH) {
+    const int seg = (int)(v / per_seg);
+    const long long e = v - seg * per_seg;
+    const int n = a.R + (int)(e / a.K), k = (int)(e % a.K);
+    a.dst[seg * a.seg_stride + slab_index(n, k, a.K)] = 0;
   }
 }
 

@@ -64,7 +64,8 @@ def test_init_rejects_bad_calib():
             B.moe_init(c, B.make_calib(**kw))
 
 
-@pytest.mark.parametrize("shape", list(W.WORKLOADS.values()), ids=lambda s: s.name)
+@pytest.mark.parametrize("shape", list(W.WORKLOADS.values()) + [
+    W.MoeShape("padded_slabs", 98, 3, 45, 192, 320, 10, 3, 4, n_shared_experts=1)], ids=lambda s: s.name)
 def test_workspace_layout_covers_buffers(shape):
     h = B.moe_init(cfg_for(shape))
     try:
@@ -81,8 +82,10 @@ def test_workspace_layout_covers_buffers(shape):
         assert L.A + 2 * xmax * shape.hidden <= L.Hbuf
         assert L.Hbuf + 2 * rows * shape.ffn <= L.O
         assert L.O + 2 * rows * shape.hidden <= size
-        assert B.moe_packed_weights_size(h) == (shape.n_local_experts + shape.n_shared_experts) * 3 * \
-            shape.hidden * shape.ffn * 2
+        # weight slabs of the GEMM tiles are padded to 256 rows
+        slab = lambda n: math.ceil(n / 256) * 256
+        assert B.moe_packed_weights_size(h) == (shape.n_local_experts + shape.n_shared_experts) * 2 * \
+            (slab(2 * shape.ffn) * shape.hidden + slab(shape.hidden) * shape.ffn)
         bm, nt0, nt1 = B.moe_tile_geometry(h)
         assert nt0 == math.ceil(2 * shape.ffn / 256) and bm > 0
         # GEMM1 tiles per row tile: column tiles over H times a split-K factor of 1, 2, 4 or 8
