@@ -138,8 +138,11 @@ typedef struct {
                          builder for the cost model (section 3.2, Eq 14) */
   size_t plan;        /* moe_plan of the last megakernel launch */
   size_t err;         /* int32 device error word */
-  size_t A;           /* bf16 [X_max + pad][H]: dispatched rows */
-  size_t Hbuf;        /* bf16 [X_max + S*Tr + pad][F]: SiLU(gate)*up */
+  size_t A;           /* bf16 [X_max + pad][H]: dispatched rows, group-tiled:
+                         row r, column j at element
+                         ((r/32)*(H/32) + j/32)*1024 + (r%32)*32 + j%32 */
+  size_t Hbuf;        /* bf16 [X_max + S*Tr + pad][F]: SiLU(gate)*up,
+                         group-tiled like A (F in place of H) */
   size_t O;           /* bf16 [X_max + S*Tr + pad][H]: expert outputs */
 } moe_ws_layout;
 

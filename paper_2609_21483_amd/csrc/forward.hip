@@ -311,11 +311,14 @@ __device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int 
       for (int j = 0; j < k; ++j) {
         const int s = sl[tok * k + j];
         if ((unsigned)s >= (unsigned)xmax) continue;
+        // A is group-tiled (gemm::AOp): 16-byte chunk c of row s lies in
+        // k-step block c / 4 of group s / 32, at row s % 32 of the block
+        const uint32_t off = ((uint32_t)(s >> 5) * (uint32_t)H * 32u + (uint32_t)(c >> 2) * 1024u +
+                              (uint32_t)(s & 31) * 32u + (uint32_t)(c & 3) * 8u) * 2u;
         if constexpr (SIG) {
-          const uint32_t off = ((uint32_t)s * (uint32_t)H + (uint32_t)c * 8u) * 2u;
           __builtin_amdgcn_raw_buffer_store_b128(val[i], rA, off, 0, 16 /* sc1 */);
         } else {
-          reinterpret_cast<u32x4_t*>(a.A + (size_t)s * H)[c] = val[i];
+          *reinterpret_cast<u32x4_t*>(reinterpret_cast<char*>(a.A) + off) = val[i];
         }
       }
     }
@@ -644,32 +647,38 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
   const int qs = r.q * S.nseg + r.seg;
   const size_t orow = (size_t)S.row0[qs] + (size_t)r.mt * BM;
   const int n0 = r.nt * BN;
-  const uint16_t* Aop;
+  // A: the dispatched rows and h are group-tiled (gemm::AOp); a shared
+  // expert reads the caller's row-major x.  B: slab r.nt of the expert's
+  // slab-tiled weights (n0 is a multiple of the slab height, so the slab
+  // starts at element n0 * K), then the split's first k-step block.
+  gemm::AOp A;
   const uint16_t* Bop;
-  int ld, Kd;
-  // B: slab r.nt of the expert's slab-tiled weights (n0 is a multiple of the
-  // slab height, so the slab starts at element n0 * K), then the split's
-  // first k-step block
+  int Kd;
+  A.rows = r.rows;
   if (r.ph == 0) {
     const size_t arow = (size_t)S.arow0[qs] + (size_t)r.mt * BM;
-    Aop = (r.seg < a.El ? a.A : a.x) + arow * a.H;
+    if (r.seg < a.El) {
+      A = {a.A + (arow >> 5) * (size_t)a.H * gemm::GROUP, a.H, (int)(arow & 31), a.H * gemm::GROUP * 2, r.rows};
+    } else {
+      A = {a.x + arow * a.H, a.H, 0, 0, r.rows};
+    }
     Bop = a.w13 + (size_t)r.seg * slab_rows(2 * a.F) * a.H + (size_t)n0 * a.H;
-    ld = a.H;
     Kd = a.H;
   } else {
     const int kl = a.F / a.nsplit;
-    Aop = a.Hb + orow * a.F + (size_t)r.ks * kl;
+    A = {a.Hb + (orow >> 5) * (size_t)a.F * gemm::GROUP + (size_t)r.ks * kl * gemm::GROUP, a.F, (int)(orow & 31),
+         a.F * gemm::GROUP * 2, r.rows};
     Bop = a.w2t + (size_t)r.seg * slab_rows(a.H) * a.F + (size_t)n0 * a.F + (size_t)r.ks * kl * SLAB;
-    ld = a.F;
     Kd = kl;
   }
   gemm::Acc acc;
   gemm::zero(acc);
-  gemm::mainloop(acc, Aop, ld, r.rows, Bop, Kd, ring);
+  gemm::mainloop(acc, A, Bop, Kd, ring);
   int nxt = -1;
   if (threadIdx.x == 0) nxt = claim_next();
   if (r.ph == 0) {
-    gemm::store_silu_mul<CP>(acc, a.Hb + orow * a.F + n0 / 2, a.F, r.rows, a.F - n0 / 2);
+    gemm::store_silu_mul_tiled<CP>(acc, a.Hb + (orow >> 5) * (size_t)a.F * gemm::GROUP + (size_t)(n0 / 2) * gemm::GROUP,
+                                   (int)(orow & 31), a.F * gemm::GROUP, r.rows, a.F - n0 / 2);
   } else if (a.nsplit == 1) {
     gemm::store_bf16<CP>(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0);
   } else {

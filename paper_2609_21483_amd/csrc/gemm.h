@@ -1,8 +1,10 @@
 // Grouped-GEMM tile for gfx950: C[256 x 256] = A[256 x K] * B[256 x K]^T on
 // bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
 //
-// A is row-major (leading dimension lda).  B, the packed expert weights, is
-// slab-tiled: a slab of 256 rows stores each 32-deep k-step as one 16 KiB
+// A is either row-major (leading dimension lda) or group-tiled: 32-row
+// groups, each 32-deep k-step of a group one 2 KiB block (32 rows x 64
+// bytes), so a tile starting at any row reads whole lines too.  B, the packed
+// expert weights, is slab-tiled: a slab of 256 rows stores each 32-deep k-step as one 16 KiB
 // block (256 rows x 64 bytes), so a stage of B is one contiguous block and
 // every DMA instruction covers eight whole 128-byte lines instead of sixteen
 // half lines of 8 KiB-strided rows (measured at full chip: 10% less time per
@@ -114,16 +116,27 @@ struct DmaOff {
   uint32_t a[A_INSTR], b[B_INSTR];
 };
 
-__device__ __forceinline__ void dma_offsets(DmaOff& o, int lda, int a_rows) {
-  lda = opaque(lda);
-  a_rows = opaque(a_rows);
+// A operand of a tile: row-major from its first row (gstride 0, lda
+// elements per row), or group-tiled: `A` points at the group holding the
+// tile's first row, which is row r0 (0..31) of that group, and consecutive
+// groups are gstride bytes apart.
+struct AOp {
+  const uint16_t* p;
+  int lda, r0, gstride, rows;
+};
+constexpr int GROUP = 32;                      // rows per group of a group-tiled operand
+constexpr int GROUP_STEP = GROUP * KSTEP * 2;  // bytes per k-step block of a group
+
+__device__ __forceinline__ void dma_offsets(DmaOff& o, const AOp& A) {
+  const int lda = opaque(A.lda), a_rows = opaque(A.rows), r0 = opaque(A.r0), gs = opaque(A.gstride);
   const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
 #pragma unroll
   for (int i = 0; i < A_INSTR; ++i) {
     const int g = (wave * A_INSTR + i) * 64 + lane;
     const int row = g >> 2, c = (g & 3) ^ ((row >> 1) & 3);
     const int r = row < a_rows ? row : a_rows - 1;
-    o.a[i] = (uint32_t)(r * lda + c * 8) * 2u;
+    const int p = r0 + r;
+    o.a[i] = gs ? (uint32_t)((p >> 5) * gs + (p & (GROUP - 1)) * (KSTEP * 2) + c * 16) : (uint32_t)(r * lda + c * 8) * 2u;
   }
 #pragma unroll
   for (int i = 0; i < B_INSTR; ++i) {
@@ -194,23 +207,23 @@ __device__ __forceinline__ void mfma_block(Acc& acc, const bf16x8_t (&af)[MB], c
 // instance issues the same DMA and passes the same barriers, so the waves of
 // a workgroup may run different instances.
 template <int MBA>
-__device__ __forceinline__ void mainloop_mb(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int Kd,
-                                         char* ring) {
+__device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16_t* B, int Kd, char* ring) {
   const int nk = Kd / KSTEP;
   DmaOff o;
-  dma_offsets(o, lda, a_rows);
+  dma_offsets(o, A);
+  const int a_step = opaque(A.gstride) ? GROUP_STEP : KSTEP * 2;  // bytes from one k-step of A to the next
   // scalars of the DMA issue: this wave's destinations in stage 0 and the
   // operand bases, pinned in scalar registers
   const int wave = opaque((int)(threadIdx.x >> 6));
   const uint32_t ring0 = (uint32_t)opaque((int)lds_u32(ring));
   const uint32_t la0 = ring0 + (uint32_t)(wave * A_INSTR * 1024);
   const uint32_t lb0 = ring0 + (uint32_t)(A_BYTES + wave * B_INSTR * 1024);
-  const char* Ab = opaque(reinterpret_cast<const char*>(A));
+  const char* Ab = opaque(reinterpret_cast<const char*>(A.p));
   const char* Bb = opaque(reinterpret_cast<const char*>(B));
   auto st = [&](int s) { return ring + (s & (NSTAGE - 1)) * STAGE_BYTES; };
   auto issue = [&](int s) {
     const uint32_t so = (uint32_t)((s & (NSTAGE - 1)) * STAGE_BYTES);
-    issue_stage(la0 + so, lb0 + so, Ab + (size_t)s * (KSTEP * 2), Bb + (size_t)s * B_BYTES, o);
+    issue_stage(la0 + so, lb0 + so, Ab + (size_t)s * a_step, Bb + (size_t)s * B_BYTES, o);
   };
   issue(0);
   if (nk > 1) issue(1);
@@ -247,24 +260,23 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const uint16_t* A, int lda
   compiler_fence();
 }
 
-// acc += A[0..a_rows) . B^T over k in [0, Kd); Kd % 32 == 0.  B points at
+// acc += A[0..A.rows) . B^T over k in [0, Kd); Kd % 32 == 0.  B points at
 // the first k-step block of a 256-row slab of slab-tiled weights.
 // ring: RING_BYTES of LDS.  Ends with a barrier (the ring may be reused).
 // A wave computes only the 32-row blocks of its rows that hold valid rows
 // (a_rows): the last row tile of an expert is often nearly empty, and its
 // padding rows would otherwise cost as much MFMA work as valid ones.  Their
 // accumulators stay zero and are never stored.
-__device__ __forceinline__ void mainloop(Acc& acc, const uint16_t* A, int lda, int a_rows, const uint16_t* B, int Kd,
-                                         char* ring) {
+__device__ __forceinline__ void mainloop(Acc& acc, const AOp& A, const uint16_t* B, int Kd, char* ring) {
   const int wm = opaque((int)(threadIdx.x >> 6)) % WM;
-  const int left = opaque(a_rows) - wm * 32;  // valid rows from the wave's first block on
+  const int left = opaque(A.rows) - wm * 32;  // valid rows from the wave's first block on
   const int mba = left <= 0 ? 0 : min(MB, (left + WM * 32 - 1) / (WM * 32));
   switch (mba) {
-    case MB: mainloop_mb<MB>(acc, A, lda, a_rows, B, Kd, ring); break;
-    case 3: mainloop_mb<3>(acc, A, lda, a_rows, B, Kd, ring); break;
-    case 2: mainloop_mb<2>(acc, A, lda, a_rows, B, Kd, ring); break;
-    case 1: mainloop_mb<1>(acc, A, lda, a_rows, B, Kd, ring); break;
-    default: mainloop_mb<0>(acc, A, lda, a_rows, B, Kd, ring); break;
+    case MB: mainloop_mb<MB>(acc, A, B, Kd, ring); break;
+    case 3: mainloop_mb<3>(acc, A, B, Kd, ring); break;
+    case 2: mainloop_mb<2>(acc, A, B, Kd, ring); break;
+    case 1: mainloop_mb<1>(acc, A, B, Kd, ring); break;
+    default: mainloop_mb<0>(acc, A, B, Kd, ring); break;
   }
 }
 
@@ -316,6 +328,33 @@ __device__ __forceinline__ void store_silu_mul(const Acc& acc, uint16_t* out, in
         const float g = acc[mb][0][r], u = acc[mb][1][r];
         const float hv = (g / (1.0f + __expf(-g))) * u;
         __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(hv), rs, (base + (uint32_t)(dr * ldo)) * 2u, 0, CP);
+      }
+    }
+}
+
+// GEMM0 epilogue into a group-tiled h: `out` points at the k-step block of
+// the tile's first h column in the group holding its first row, which is row
+// r0 of that group; groups are gs elements apart.  The 32 h columns of a
+// wave are one 64-byte row piece of a block.
+template <int CP>
+__device__ __forceinline__ void store_silu_mul_tiled(const Acc& acc, uint16_t* out, int r0, int gs, int out_rows,
+                                                     int out_cols) {
+  r0 = opaque(r0);
+  gs = opaque(gs);
+  const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
+  const OutMap m = out_map(TN / 2);
+  const uint32_t cpart = (uint32_t)((m.col_l >> 5) * (GROUP * KSTEP) + (m.col_l & (KSTEP - 1)));
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int dr = out_dr(mb, r);
+      if (m.row_l + dr < out_rows && m.col_l < out_cols) {
+        const float g = acc[mb][0][r], u = acc[mb][1][r];
+        const float hv = (g / (1.0f + __expf(-g))) * u;
+        const int p = r0 + m.row_l + dr;
+        const uint32_t off = (uint32_t)((p >> 5) * gs + (p & (GROUP - 1)) * KSTEP) + cpart;
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(hv), rs, off * 2u, 0, CP);
       }
     }
 }

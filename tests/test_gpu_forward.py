@@ -68,8 +68,12 @@ def check_case(B, c, rows=None, forced=(), check_A=False, gemm1_split=0):
                 assert torch.equal(y.view(torch.int16), first.view(torch.int16)), f"{key} differs from dynamic"
         if check_A:
             tab = O.route_tables(idx, shape.n_src_ranks, shape.tokens_per_rank, 0, shape.n_local_experts)
-            A = layer.ws_view("A", torch.int16, tab.X * shape.hidden).cpu().numpy().view(np.uint16)
-            assert np.array_equal(A.reshape(tab.X, shape.hidden), O.dispatch(c.xu, tab, shape.top_k))
+            # the dispatched rows are stored in 32-row groups, each group's 32-column
+            # k-steps one 32 x 32 block after the other (the layout of moe.h)
+            G, H = -(-tab.X // 32), shape.hidden
+            A = layer.ws_view("A", torch.int16, G * 32 * H).cpu().numpy().view(np.uint16)
+            A = A.reshape(G, H // 32, 32, 32).transpose(0, 2, 1, 3).reshape(G * 32, H)[:tab.X]
+            assert np.array_equal(A, O.dispatch(c.xu, tab, shape.top_k))
         return err
     finally:
         layer.close()
