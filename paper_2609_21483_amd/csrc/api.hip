@@ -517,11 +517,9 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
     const double g1 = (H - 1.0) * u / (1.0 - (H - 1.0) * u), g2 = H * u2 / (1.0 - H * u2);
     g.bound = (float)(1.01 * (g1 + g2));
   }
-  zero_i32_kernel<<<1, 64, 0, s>>>(g.stats + ST_CANDS, 1);
   gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
   gate_mfma_kernel<<<(h->T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
   const int tok_blocks = (h->T + (NTH / 16) - 1) / (NTH / 16);
-  gate_cand_kernel<<<tok_blocks, NTH, 0, s>>>(g);
   gate_chain_kernel<<<std::min(16384, std::max(1, (h->T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
   gate_final_kernel<<<tok_blocks, NTH, 0, s>>>(g);
   HIP_TRY(hipGetLastError());

@@ -216,7 +216,6 @@ constexpr int GATE_WAVES = 4;  // wavefronts per workgroup of gate_mfma_kernel (
 // ---- launch prototypes ---------------------------------------------------------
 __global__ void gate_prep_kernel(GateArgs a);
 __global__ void gate_mfma_kernel(GateArgs a);
-__global__ void gate_cand_kernel(GateArgs a);
 __global__ void gate_chain_kernel(GateArgs a);
 __global__ void gate_final_kernel(GateArgs a);
 __global__ void tab_count_kernel(TableArgs a);

@@ -38,6 +38,7 @@ __global__ void __launch_bounds__(NTH) gate_prep_kernel(GateArgs a) {
   __shared__ float part[NTH / WAVE];
   const int e = blockIdx.x;
   const int tid = threadIdx.x;
+  if (e == 0 && tid == 0) a.stats[ST_CANDS] = 0;  // the candidate pass counts the chains from here
   float ss = 0.0f;
   for (int h = tid; h < a.H; h += NTH) {
     const uint16_t v = a.wg[(size_t)h * a.E + e];
@@ -165,10 +166,6 @@ __device__ __forceinline__ void gate_mfma_body(const GateArgs& a) {
   }
 }
 
-__global__ void __launch_bounds__(GATE_WAVES * WAVE) gate_mfma_kernel(GateArgs a) {
-  if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a);
-  else gate_mfma_body<4, 4, GATE_WAVES>(a);
-}
 
 // lanes of one token's group of GG: reductions stay inside the group
 constexpr int GG = 16;
@@ -195,14 +192,13 @@ __device__ __forceinline__ void interval(const GateArgs& a, int g, int e, float 
   d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
 }
 
-// Candidates: tau = k-th largest lower end; every expert whose upper end
-// reaches tau becomes a chain (g, e) of the chain list, in expert order per
-// token.  A workgroup takes its chain range with one atomic.
-__global__ void __launch_bounds__(NTH) gate_cand_kernel(GateArgs a) {
-  __shared__ int cnt[GTOK];
-  __shared__ int base_s;
+// Candidates of the GTOK tokens from g0 on (one workgroup of NTH threads):
+// tau = k-th largest lower end; every expert whose upper end reaches tau
+// becomes a chain (g, e) of the chain list, in expert order per token.  The
+// workgroup takes its chain range with one atomic.
+__device__ __forceinline__ void cand_tokens(const GateArgs& a, int g0, int* cnt, int& base_s) {
   const int tid = threadIdx.x, grp = tid / GG, gl = tid % GG;
-  const int g = blockIdx.x * GTOK + grp;
+  const int g = g0 + grp;
   const bool valid = g < a.T;
   const int gs = valid ? g : 0;
   const float xn = a.xn[gs];
@@ -264,6 +260,22 @@ __global__ void __launch_bounds__(NTH) gate_cand_kernel(GateArgs a) {
       a.ch_e[pos] = gl + GG * i;
       ++pos;
     }
+}
+
+// Approximate logits of 32 tokens, then their candidates: the workgroup's
+// logits and norms are in memory after the barrier (workgroup scope), so the
+// candidate pass needs no launch of its own.
+__global__ void __launch_bounds__(GATE_WAVES * WAVE) gate_mfma_kernel(GateArgs a) {
+  static_assert(GATE_WAVES * WAVE == NTH && 32 % GTOK == 0, "candidate pass geometry");
+  __shared__ int cnt[GTOK];
+  __shared__ int base_s;
+  if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a);
+  else gate_mfma_body<4, 4, GATE_WAVES>(a);
+  __syncthreads();
+  for (int sub = 0; sub < 32 / GTOK; ++sub) {
+    cand_tokens(a, blockIdx.x * 32 + sub * GTOK, cnt, base_s);
+    __syncthreads();
+  }
 }
 
 // the defined logit of one (token, expert): fp32, one accumulator, h
@@ -492,43 +504,74 @@ __global__ void __launch_bounds__(NTH) tab_perm_kernel(TableArgs a) {
   a.first_slot[g] = first;
 }
 
-// first slot of expert le whose token index is >= b (segment is sorted by token)
-__device__ inline int seg_lower_bound(const TableArgs& a, int le, long long b) {
+// Lower bounds in an expert's segment of slots (tokens ascending): the first
+// slot of expert le whose token is >= b.  The workgroup first stages the
+// token of every STRIDE-th slot in LDS (samp); a search narrows to one
+// window of STRIDE slots there and finishes with a binary search of
+// log2(STRIDE) global reads.
+constexpr int FIN_SAMP = 4096;
+__device__ inline int slot_token(const TableArgs& a, int p) { return a.inv[p] / a.k; }
+__device__ inline int seg_lower_bound(const TableArgs& a, const int* samp, int stride, int le, long long b) {
   int lo = a.off[le], hi = a.off[le + 1];
+  int jlo = (lo + stride - 1) / stride, jhi = (hi + stride - 1) / stride;  // samples at slots in [lo, hi)
+  int j0 = jlo, j1 = jhi;
+  while (j0 < j1) {  // first sample whose token is >= b
+    const int mid = (j0 + j1) >> 1;
+    if ((long long)samp[mid] < b) j0 = mid + 1; else j1 = mid;
+  }
+  if (j0 > jlo) lo = (j0 - 1) * stride + 1;  // the sample before has a token < b
+  if (j0 < jhi) hi = j0 * stride;            // this sample has a token >= b
   while (lo < hi) {
-    int mid = (lo + hi) >> 1;
-    if ((long long)(a.inv[mid] / a.k) < b) lo = mid + 1; else hi = mid;
+    const int mid = (lo + hi) >> 1;
+    if ((long long)slot_token(a, mid) < b) lo = mid + 1; else hi = mid;
   }
   return lo;
 }
 
+// One workgroup.  Lower bounds at the rank boundaries (per-(expert, rank)
+// counts) and at the chunk boundaries of every chunk option (sub_off) form
+// one item space, one search per item and thread; the tile counts of the
+// cost model are then taken from the workgroup's copy of sub_off.
 __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
   __shared__ int uq[64];
   __shared__ int ntk[KOPT];
+  __shared__ int samp[FIN_SAMP];
+  __shared__ int rb[MAX_EL * 65];              // [El][R + 1] lower bounds at rank boundaries
+  __shared__ int so_l[KOPT * MAX_EL * SUBW];   // this workgroup's copy of sub_off
   const int tid = threadIdx.x;
+  const int X = a.off[a.El];
+  int stride = 64;
+  while ((X + stride - 1) / stride > FIN_SAMP) stride *= 2;
   for (int r = tid; r < a.R; r += NTH) uq[r] = 0;
   if (tid < KOPT) ntk[tid] = 0;
+  for (int j = tid; j * stride < X; j += NTH) samp[j] = slot_token(a, j * stride);
   __syncthreads();
-  // per-(expert, rank) counts: rank r owns tokens [r*Tr, (r+1)*Tr)
-  for (int v = tid; v < a.El * a.R; v += NTH) {
-    int le = v / a.R, r = v % a.R;
-    a.cnt_rank[v] = seg_lower_bound(a, le, (long long)(r + 1) * a.Tr) -
-                    seg_lower_bound(a, le, (long long)r * a.Tr);
-  }
-  // chunk offsets: chunk(g) = floor(g*K/T) >= q  <=>  g >= ceil(q*T/K)
-  for (int v = tid; v < KOPT * a.El * SUBW; v += NTH) {
-    int ki = v / (a.El * SUBW);
-    int rem = v % (a.El * SUBW);
-    int le = rem / SUBW, q = rem % SUBW;
-    int K = kopt_value(ki);
-    int val = 0;
-    if (q <= K) {
-      long long b = ((long long)q * a.T + K - 1) / K;
-      val = seg_lower_bound(a, le, b);
+  // unique tokens per rank (tokens with at least one local pair)
+  for (int g = tid; g < a.T; g += NTH)
+    if (a.first_slot[g] >= 0) atomicAdd(&uq[g / a.Tr], 1);
+  const int n_rank = a.El * (a.R + 1), n_sub = KOPT * a.El * SUBW;
+  for (int v = tid; v < n_rank + n_sub; v += NTH) {
+    if (v < n_rank) {
+      // rank r owns tokens [r*Tr, (r+1)*Tr)
+      const int le = v / (a.R + 1), r = v % (a.R + 1);
+      rb[v] = seg_lower_bound(a, samp, stride, le, (long long)r * a.Tr);
+    } else {
+      // chunk offsets: chunk(g) = floor(g*K/T) >= q  <=>  g >= ceil(q*T/K)
+      const int w = v - n_rank;
+      const int ki = w / (a.El * SUBW), rem = w % (a.El * SUBW);
+      const int le = rem / SUBW, q = rem % SUBW;
+      const int K = kopt_value(ki);
+      int val = 0;
+      if (q <= K) val = seg_lower_bound(a, samp, stride, le, ((long long)q * a.T + K - 1) / K);
+      a.sub_off[w] = val;
+      so_l[w] = val;
     }
-    a.sub_off[v] = val;
   }
-  __syncthreads();  // the block's sub_off stores are visible to the block
+  __syncthreads();
+  for (int v = tid; v < a.El * a.R; v += NTH) {
+    const int le = v / a.R, r = v % a.R;
+    a.cnt_rank[v] = rb[le * (a.R + 1) + r + 1] - rb[le * (a.R + 1) + r];
+  }
   // GEMM tiles of the layer at each chunk option: every (chunk, segment)
   // contributes ceil(rows / BM) row tiles of GEMM0 + GEMM1 tiles; shared
   // experts take rank 0's tokens of the chunk
@@ -539,7 +582,7 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
       const int q = v / nseg, seg = v % nseg;
       int rows;
       if (seg < a.El) {
-        const int* so = a.sub_off + ((size_t)ki * a.El + seg) * SUBW;
+        const int* so = so_l + (ki * a.El + seg) * SUBW;
         rows = so[q + 1] - so[q];
       } else {
         const int t0 = (int)(((long long)q * a.T + K - 1) / K);
@@ -550,16 +593,11 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     }
     if (part) atomicAdd(&ntk[ki], part);
   }
-  // unique tokens per rank (tokens with at least one local pair)
-  for (int g = tid; g < a.T; g += NTH)
-    if (a.first_slot[g] >= 0) atomicAdd(&uq[g / a.Tr], 1);
   __syncthreads();
   for (int r = tid; r < a.R; r += NTH) a.uniq[r] = uq[r];
-  __syncthreads();
   if (tid == 0) {
-    int X = a.off[a.El];
     int xl = 0;
-    for (int le = 0; le < a.El; ++le) xl += a.cnt_rank[le * a.R + 0];
+    for (int le = 0; le < a.El; ++le) xl += rb[le * (a.R + 1) + 1] - rb[le * (a.R + 1)];
     int uin = 0;
     for (int r = 1; r < a.R; ++r) uin += uq[r];
     a.stats[ST_X] = X;
