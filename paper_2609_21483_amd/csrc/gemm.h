@@ -151,10 +151,13 @@ __device__ __forceinline__ void dma_offsets(DmaOff& o, const AOp& A) {
 // register that was loaded from memory before it: a reload in front of the
 // loop would otherwise make the compiler wait for every outstanding DMA at
 // each iteration.
+template <bool ADMA>
 __device__ __forceinline__ void issue_stage(uint32_t lds_a, uint32_t lds_b, const char* Ak, const char* Bk,
                                             const DmaOff& o) {
+  if constexpr (ADMA) {
 #pragma unroll
-  for (int i = 0; i < A_INSTR; ++i) dma16(Ak, o.a[i], lds_a + i * 1024);
+    for (int i = 0; i < A_INSTR; ++i) dma16(Ak, o.a[i], lds_a + i * 1024);
+  }
 #pragma unroll
   for (int i = 0; i < B_INSTR; ++i) dma16(Bk, o.b[i], lds_b + i * 1024);
 }
@@ -203,11 +206,16 @@ __device__ __forceinline__ void mfma_block(Acc& acc, const bf16x8_t (&af)[MB], c
       acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
 }
 
-// The mainloop of a wave that computes its first MBA 32-row blocks.  Every
-// instance issues the same DMA and passes the same barriers, so the waves of
-// a workgroup may run different instances.
-template <int MBA>
+// The mainloop of a wave that computes its first MBA 32-row blocks.  Wave w
+// loads A's 32-row block w (its A_INSTR DMA instructions cover those rows)
+// when ADMA, i.e. when the block holds a valid row; a block without one is
+// neither loaded nor read (the waves that would multiply it skip it too), so
+// a nearly empty row tile streams little more than its B operand.  Every
+// instance passes the same barriers, so the waves of a workgroup may run
+// different instances; the DMA waits count this wave's own instructions.
+template <int MBA, bool ADMA>
 __device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16_t* B, int Kd, char* ring) {
+  constexpr int WI = ADMA ? INSTR : B_INSTR;  // DMA instructions of this wave per stage
   const int nk = Kd / KSTEP;
   DmaOff o;
   dma_offsets(o, A);
@@ -223,12 +231,12 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16
   auto st = [&](int s) { return ring + (s & (NSTAGE - 1)) * STAGE_BYTES; };
   auto issue = [&](int s) {
     const uint32_t so = (uint32_t)((s & (NSTAGE - 1)) * STAGE_BYTES);
-    issue_stage(la0 + so, lb0 + so, Ab + (size_t)s * a_step, Bb + (size_t)s * B_BYTES, o);
+    issue_stage<ADMA>(la0 + so, lb0 + so, Ab + (size_t)s * a_step, Bb + (size_t)s * B_BYTES, o);
   };
   issue(0);
   if (nk > 1) issue(1);
   if (nk > 2) issue(2);
-  if (nk > 2) wait_vm<2 * INSTR>(); else if (nk > 1) wait_vm<INSTR>(); else wait_vm<0>();
+  if (nk > 2) wait_vm<2 * WI>(); else if (nk > 1) wait_vm<WI>(); else wait_vm<0>();
   __builtin_amdgcn_s_barrier();
   compiler_fence();
   bf16x8_t fa0[MB], fb0[NB], fa1[MB], fb1[NB];
@@ -238,7 +246,7 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16
   for (; s < nk - 3; ++s) {  // steady state: the stage 3 ahead is always issued
     load_frags<MBA>(st(s), 1, fo, fa1, fb1);
     mfma_block<MBA>(acc, fa0, fb0);
-    wait_vm<INSTR>();
+    wait_vm<WI>();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(s + 3);
@@ -249,7 +257,7 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16
     load_frags<MBA>(st(s), 1, fo, fa1, fb1);
     mfma_block<MBA>(acc, fa0, fb0);
     if (s + 1 < nk) {
-      if (s + 2 < nk) wait_vm<INSTR>(); else wait_vm<0>();
+      if (s + 2 < nk) wait_vm<WI>(); else wait_vm<0>();
       __builtin_amdgcn_s_barrier();
       compiler_fence();
       load_frags<MBA>(st(s + 1), 0, fo, fa0, fb0);
@@ -268,15 +276,27 @@ __device__ __forceinline__ void mainloop_mb(Acc& acc, const AOp& A, const uint16
 // padding rows would otherwise cost as much MFMA work as valid ones.  Their
 // accumulators stay zero and are never stored.
 __device__ __forceinline__ void mainloop(Acc& acc, const AOp& A, const uint16_t* B, int Kd, char* ring) {
-  const int wm = opaque((int)(threadIdx.x >> 6)) % WM;
-  const int left = opaque(A.rows) - wm * 32;  // valid rows from the wave's first block on
+  const int wave = opaque((int)(threadIdx.x >> 6)), wm = wave % WM;
+  const int rows = opaque(A.rows);
+  const int left = rows - wm * 32;  // valid rows from the wave's first block on
   const int mba = left <= 0 ? 0 : min(MB, (left + WM * 32 - 1) / (WM * 32));
-  switch (mba) {
-    case MB: mainloop_mb<MB>(acc, A, B, Kd, ring); break;
-    case 3: mainloop_mb<3>(acc, A, B, Kd, ring); break;
-    case 2: mainloop_mb<2>(acc, A, B, Kd, ring); break;
-    case 1: mainloop_mb<1>(acc, A, B, Kd, ring); break;
-    default: mainloop_mb<0>(acc, A, B, Kd, ring); break;
+  static_assert(A_INSTR * 16 == 32, "wave w's A DMA covers 32-row block w");
+  if (rows > wave * 32) {
+    switch (mba) {
+      case MB: mainloop_mb<MB, true>(acc, A, B, Kd, ring); break;
+      case 3: mainloop_mb<3, true>(acc, A, B, Kd, ring); break;
+      case 2: mainloop_mb<2, true>(acc, A, B, Kd, ring); break;
+      case 1: mainloop_mb<1, true>(acc, A, B, Kd, ring); break;
+      default: mainloop_mb<0, true>(acc, A, B, Kd, ring); break;
+    }
+  } else {
+    switch (mba) {
+      case MB: mainloop_mb<MB, false>(acc, A, B, Kd, ring); break;
+      case 3: mainloop_mb<3, false>(acc, A, B, Kd, ring); break;
+      case 2: mainloop_mb<2, false>(acc, A, B, Kd, ring); break;
+      case 1: mainloop_mb<1, false>(acc, A, B, Kd, ring); break;
+      default: mainloop_mb<0, false>(acc, A, B, Kd, ring); break;
+    }
   }
 }
 
