@@ -55,10 +55,16 @@ def parse():
 
 
 def kernel_sources_hash() -> str:
+    """Hash of the megakernel's sources with comments and whitespace removed,
+    so that an edit of comments alone keeps a traffic measurement valid."""
+    import re
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update("".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 

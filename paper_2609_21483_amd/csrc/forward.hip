@@ -4,13 +4,16 @@
 //
 // Data layout in HBM
 //   x    bf16 [T][H]        staging regions: rank r's rows at r*Tr
-//   A    bf16 [X+pad][H]    dispatched rows, expert-contiguous (slot order)
-//   Hbuf bf16 [X+S*Tr+pad][F]  SiLU(gate)*up per row (shared experts after X)
+//   A    bf16 [X+pad][H]    dispatched rows, expert-contiguous (slot order),
+//                           group-tiled (gemm::AOp)
+//   Hbuf bf16 [X+S*Tr+pad][F]  SiLU(gate)*up per row (shared experts after X),
+//                           group-tiled
 //   O    bf16 [X+S*Tr+pad][H]  expert outputs per row
 //   part fp32 [split][X+S*Tr+pad][H]  split-K partials of GEMM1 (when split)
 //   y    bf16 [T][H]        output staging regions
-//   w13  bf16 [E_l+S][2F][H] gate/up weights, k-contiguous, 32-col interleave
-//   w2t  bf16 [E_l+S][H][F]  down weights, k-contiguous
+//   w13  bf16 [E_l+S][2F][H] gate/up weights, k-contiguous, 32-col interleave,
+//                           slab-tiled (common.h)
+//   w2t  bf16 [E_l+S][H][F]  down weights, k-contiguous, slab-tiled
 #include <type_traits>
 
 #include "common.h"
