@@ -132,6 +132,7 @@ def test_route_ties_and_candidate_overflow(B, bias):
     (2, 300, 16, 4, 16, 0.0),    # every expert local
     (4, 77, 32, 8, 5, 2.5),      # heavy skew: empty local experts
     (2, 513, 64, 6, 16, 1.0),    # more than one table block
+    (4, 10000, 8, 8, 8, 0.0),    # 320000 pairs: the lower-bound search samples every 128th slot
 ])
 def test_build_tables_supplied_routing(B, R, Tr, E, k, El, skew):
     shape = W.MoeShape("t", 99, R, Tr, 64, 64, E, k, El)
