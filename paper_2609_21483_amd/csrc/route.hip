@@ -8,6 +8,7 @@
 // come from block histograms, an ordered scan and wavefront ballots, never
 // from atomic slot claiming.
 #include "common.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace moe {
@@ -68,9 +69,7 @@ __global__ void __launch_bounds__(NTH) gate_prep_kernel(GateArgs a) {
 // (the pass streams x with more loads in flight), four with 4 steps ahead
 // otherwise (register budget).
 template <int GATE_EB, int GSTEP, int GWAVES>
-__device__ __forceinline__ void gate_mfma_body(const GateArgs& a) {
-  __shared__ float red[GWAVES - 1][32 * 32 * GATE_EB];
-  __shared__ float ssr[GWAVES][64];
+__device__ __forceinline__ void gate_mfma_body(const GateArgs& a, float (*red)[32 * 32 * 4], float (*ssr)[64]) {
   const int lane = threadIdx.x & (WAVE - 1), wave = threadIdx.x / WAVE;
   const int g0 = blockIdx.x * 32;
   const int row = lane & 31, kh = (lane >> 5) * 8;
@@ -265,12 +264,108 @@ __device__ __forceinline__ void cand_tokens(const GateArgs& a, int g0, int* cnt,
 // Approximate logits of 32 tokens, then their candidates: the workgroup's
 // logits and norms are in memory after the barrier (workgroup scope), so the
 // candidate pass needs no launch of its own.
+// E <= 32 with a multiple of 64 values of H per wavefront: the same sums,
+// with x and the gate rows staged through a per-wavefront LDS ring by direct
+// global->LDS loads in which 8 lanes fetch one row's 128 contiguous bytes
+// (a load instruction covers 8 rows instead of 32 scattered pieces).  Rows
+// are 64 values (128 bytes) per stage, their 16-byte granules XOR-swizzled
+// by the row index; lane l reads granule 2t + (l >> 5) of row l & 31 for the
+// t-th 16-deep MFMA step of a stage.  Token rows past T and gate rows past E
+// repeat the last valid row; their sums are not stored.
+constexpr int GS_ST = 3;                  // ring stages per wavefront
+constexpr int GS_OPB = 32 * 128;          // bytes per operand and stage
+constexpr int GS_SB = 2 * GS_OPB;         // bytes per stage
+__device__ __forceinline__ void gate_mfma_staged(const GateArgs& a, char* ring_all, float (*red)[32 * 32 * 4],
+                                                 float (*ssr)[64]) {
+  const int lane = gemm::lane_here(), wave = gemm::opaque((int)(threadIdx.x / WAVE));
+  const int g0 = blockIdx.x * 32;
+  const int hq = a.H / GATE_WAVES;  // a multiple of 64 here
+  const int hbeg = wave * hq;
+  const int nb = hq / 64;
+  char* ring = ring_all + wave * (GS_ST * GS_SB);
+  const uint32_t ring0 = gemm::lds_u32(ring);
+  uint32_t xo[4], wo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = i * 8 + (lane >> 3);
+    const int gr = (lane & 7) ^ (r & 7);
+    const int g = min(g0 + r, a.T - 1), e = min(r, a.E - 1);
+    xo[i] = ((uint32_t)g * (uint32_t)a.H + (uint32_t)hbeg) * 2u + (uint32_t)(gr * 16);
+    wo[i] = ((uint32_t)e * (uint32_t)a.H + (uint32_t)hbeg) * 2u + (uint32_t)(gr * 16);
+  }
+  const char* xb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.x));
+  const char* wb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.wgt));
+  auto issue = [&](int b) {
+    const uint32_t st = ring0 + (uint32_t)((b % GS_ST) * GS_SB);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gemm::dma16(xb + (size_t)b * 128, xo[i], st + i * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gemm::dma16(wb + (size_t)b * 128, wo[i], st + GS_OPB + i * 1024);
+  };
+  for (int b = 0; b < GS_ST - 1 && b < nb; ++b) issue(b);
+  f32x16_t acc = f32x16_t{};
+  float ss = 0.0f;
+  const int row = lane & 31, half = lane >> 5;
+  for (int b = 0; b < nb; ++b) {
+    const int later = min(nb - 1 - b, GS_ST - 2);
+    if (later >= 2) gemm::wait_vm<16>();
+    else if (later == 1) gemm::wait_vm<8>();
+    else gemm::wait_vm<0>();
+    const char* st = ring + (b % GS_ST) * GS_SB + row * 128;
+    bf16x8_t xa[4], wa[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int slot = (2 * t + half) ^ (row & 7);
+      xa[t] = *reinterpret_cast<const bf16x8_t*>(st + slot * 16);
+      wa[t] = *reinterpret_cast<const bf16x8_t*>(st + GS_OPB + slot * 16);
+    }
+    // the reads of the stage about to be refilled (read one step ago) are done
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    if (b + GS_ST - 1 < nb) issue(b + GS_ST - 1);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float f = (float)xa[t][q];
+        ss += f * f;
+      }
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[t], wa[t], acc, 0, 0, 0);
+    }
+  }
+  // add the quarters: C[8 (r >> 2) + 4 (l >> 5) + (r & 3)][l & 31]
+  if (wave > 0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[wave - 1][r * WAVE + lane] = acc[r];
+  }
+  ssr[wave][lane] = ss;
+  __syncthreads();
+  if (wave == 0) {
+    const int e = lane & 31;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float v = acc[r];
+#pragma unroll
+      for (int w = 0; w < GATE_WAVES - 1; ++w) v += red[w][r * WAVE + lane];
+      const int gr = g0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (e < a.E && gr < a.T) a.lt[(size_t)gr * a.E + e] = v;
+    }
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < GATE_WAVES; ++w) t += ssr[w][lane] + ssr[w][lane ^ 32];
+    if (lane < 32 && g0 + lane < a.T) a.xn[g0 + lane] = sqrtf(t);
+  }
+}
+
 __global__ void __launch_bounds__(GATE_WAVES * WAVE) gate_mfma_kernel(GateArgs a) {
   static_assert(GATE_WAVES * WAVE == NTH && 32 % GTOK == 0, "candidate pass geometry");
   __shared__ int cnt[GTOK];
   __shared__ int base_s;
-  if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a);
-  else gate_mfma_body<4, 4, GATE_WAVES>(a);
+  __shared__ float red[GATE_WAVES - 1][32 * 32 * 4];
+  __shared__ float ssr[GATE_WAVES][64];
+  __shared__ __align__(16) char ring[GATE_WAVES * GS_ST * GS_SB];
+  if (a.E <= 32 && (a.H / GATE_WAVES) % 64 == 0) gate_mfma_staged(a, ring, red, ssr);
+  else if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a, red, ssr);
+  else gate_mfma_body<4, 4, GATE_WAVES>(a, red, ssr);
   __syncthreads();
   for (int sub = 0; sub < 32 / GTOK; ++sub) {
     cand_tokens(a, blockIdx.x * 32 + sub * GTOK, cnt, base_s);
