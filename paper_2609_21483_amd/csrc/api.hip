@@ -44,7 +44,7 @@ struct moe_handle {
   moe_calib calib{};
   DevCalib dcal{};
   moe_ws_layout lay{};
-  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_ctl[2] = {0, 0}, off_part = 0;
+  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_blk_bad = 0, off_ctl[2] = {0, 0}, off_part = 0;
   size_t off_gwt = 0, off_glt = 0, off_gxn = 0, off_gwn = 0;  // gate scratch
   size_t off_chg = 0, off_che = 0, off_chl = 0, off_tb = 0, off_tn = 0;
   char* ws = nullptr;
@@ -189,6 +189,7 @@ void compute_layout(moe_handle* h) {
   h->off_tn = take(sizeof(int32_t) * (size_t)T);
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
+  h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
   h->off_ctl[0] = take(sizeof(int32_t) * (size_t)h->ctl_words);
   h->off_ctl[1] = take(sizeof(int32_t) * (size_t)h->ctl_words);
   const size_t orows = (size_t)h->xmax + (size_t)S * c.tokens_per_rank + BM;
@@ -222,6 +223,7 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
   a.stats = at<int32_t>(h, h->lay.stats);
   a.blk_cnt = at<int32_t>(h, h->off_blk_cnt);
   a.blk_off = at<int32_t>(h, h->off_blk_off);
+  a.blk_bad = at<int32_t>(h, h->off_blk_bad);
   a.err = at<int32_t>(h, h->lay.err);
   a.T = h->T;
   a.Tr = h->cfg.tokens_per_rank;
@@ -472,7 +474,6 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
   if (!topk_idx) return fail(MOE_ERR_INVALID_ARG, "topk_idx is NULL");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   TableArgs a = table_args(h, topk_idx);
-  zero_i32_kernel<<<1, 64, 0, s>>>(a.stats, ST_CANDS);
   tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_scan_kernel<<<1, NTH, 0, s>>>(a);
   tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);

@@ -38,6 +38,7 @@ struct TableArgs {
   int32_t* stats;
   int32_t* blk_cnt;
   int32_t* blk_off;
+  int32_t* blk_bad;    // [nblk] tokens with an invalid or repeated id, per table block
   int32_t* err;
   int T, Tr, R, k, E, e0, El, nblk;
   int S, tiles_per_row_tile;  // shared experts; GEMM0 + GEMM1 tiles of one row tile (the cost model's tile counts)

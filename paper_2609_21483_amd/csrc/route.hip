@@ -509,8 +509,10 @@ __device__ inline int local_expert(const TableArgs& a, const int* ids, int j, bo
 
 __global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
   __shared__ int hist[MAX_SEG];
+  __shared__ int nbad;
   const int tid = threadIdx.x;
   for (int i = tid; i < a.El; i += NTH) hist[i] = 0;
+  if (tid == 0) nbad = 0;
   __syncthreads();
   const int g = blockIdx.x * TB + tid;
   bool bad = false;
@@ -523,11 +525,12 @@ __global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
     }
   }
   if (bad) {
-    atomicAdd(&a.stats[ST_BADIDS], 1);
+    atomicAdd(&nbad, 1);
     atomicOr(a.err, ERR_ROUTING);
   }
   __syncthreads();
   for (int i = tid; i < a.El; i += NTH) a.blk_cnt[(size_t)blockIdx.x * a.El + i] = hist[i];
+  if (tid == 0) a.blk_bad[blockIdx.x] = nbad;
 }
 
 __global__ void __launch_bounds__(NTH) tab_scan_kernel(TableArgs a) {
@@ -547,6 +550,11 @@ __global__ void __launch_bounds__(NTH) tab_scan_kernel(TableArgs a) {
     int s = 0;
     for (int le = 0; le < a.El; ++le) { a.off[le] = s; s += tot[le]; }
     a.off[a.El] = s;
+    // the table builder's stats words: the bad-id count here, the rest in
+    // tab_finalize (words it does not write stay zero)
+    int bad = 0;
+    for (int b = 0; b < a.nblk; ++b) bad += a.blk_bad[b];
+    for (int w = 0; w < ST_CANDS; ++w) a.stats[w] = w == ST_BADIDS ? bad : 0;
   }
 }
 

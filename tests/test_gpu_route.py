@@ -147,23 +147,25 @@ def test_build_tables_supplied_routing(B, R, Tr, E, k, El, skew):
         hd.close()
 
 
-def test_bad_routing_ids_are_flagged(B):
-    shape = W.MoeShape("t", 99, 2, 40, 64, 64, 8, 2, 4)
+@pytest.mark.parametrize("Tr,rows", [(40, (5, 9, 11)), (300, (5, 290, 580))])  # one table block; three
+def test_bad_routing_ids_are_flagged(B, Tr, rows):
+    shape = W.MoeShape("t", 99, 2, Tr, 64, 64, 8, 2, 4)
     idx_ref, _ = W.random_routing(shape.T, 8, 2, seed=3)
     bad = idx_ref.copy()
-    bad[5, 1] = 8          # out of range
-    bad[9, 1] = bad[9, 0]  # repeated in a row
-    bad[11, 0] = -1
+    r0, r1, r2 = rows
+    bad[r0, 1] = 8           # out of range
+    bad[r1, 1] = bad[r1, 0]  # repeated in a row
+    bad[r2, 0] = -1
     hd = Handle(B, shape)
     try:
         B.moe_build_tables(hd.h, torch.from_numpy(bad).cuda())
         assert B.moe_sync_status(hd.h) == B.MOE_ERR_ROUTING
         # the flagged pairs are treated as not local; everything else is intact
         clean = bad.copy()
-        clean[5, 1] = 100
-        clean[9, 1] = 100
-        clean[11, 0] = 100
-        tab = O.route_tables(clean, 2, 40, 0, 4)
+        clean[r0, 1] = 100
+        clean[r1, 1] = 100
+        clean[r2, 0] = 100
+        tab = O.route_tables(clean, 2, Tr, 0, 4)
         assert np.array_equal(hd.view("slot", shape.T * 2).reshape(-1, 2), tab.slot)
         assert hd.view("stats", 16)[5] == 3
         assert B.moe_sync_status(hd.h) == B.MOE_OK  # the error word was cleared
