@@ -41,11 +41,25 @@ __global__ void __launch_bounds__(NTH) gate_prep_kernel(GateArgs a) {
   const int tid = threadIdx.x;
   if (e == 0 && tid == 0) a.stats[ST_CANDS] = 0;  // the candidate pass counts the chains from here
   float ss = 0.0f;
-  for (int h = tid; h < a.H; h += NTH) {
-    const uint16_t v = a.wg[(size_t)h * a.E + e];
-    a.wgt[(size_t)e * a.H + h] = v;
-    const float f = bf16_to_f32(v);
-    ss += f * f;
+  // PREP_V loads in flight per thread before their stores (the column of
+  // Wg is strided by E, one 2-byte read per value)
+  constexpr int PREP_V = 16;
+  for (int h0 = 0; h0 < a.H; h0 += PREP_V * NTH) {
+    uint16_t v[PREP_V];
+#pragma unroll
+    for (int i = 0; i < PREP_V; ++i) {
+      const int h = h0 + i * NTH + tid;
+      v[i] = h < a.H ? a.wg[(size_t)h * a.E + e] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int i = 0; i < PREP_V; ++i) {
+      const int h = h0 + i * NTH + tid;
+      if (h < a.H) {
+        a.wgt[(size_t)e * a.H + h] = v[i];
+        const float f = bf16_to_f32(v[i]);
+        ss += f * f;
+      }
+    }
   }
 #pragma unroll
   for (int d = WAVE / 2; d > 0; d >>= 1) ss += __shfl_xor(ss, d, WAVE);
