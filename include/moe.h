@@ -80,6 +80,20 @@ typedef struct {
 #define MOE_CALIB_MAX_C 32
 #define MOE_CALIB_MAX_K 4
 
+/* Which movement work the bubble-steal window of Eq 11 holds (section
+ * 3.2.2 leaves its W_comm undefined). */
+typedef enum {
+  MOE_WINDOW_PLAIN = 0,        /* W_dispatch + W_combine, the volume of Eq 5 */
+  MOE_WINDOW_MOVE_STEAL = 1,   /* (W_dispatch + W_combine)(K-1)/K: compute workers
+                                  whose GEMM0 rows are not dispatched yet copy rows
+                                  themselves, so the first chunk's dispatch runs on
+                                  all N workers before any GEMM tile starts, and the
+                                  last chunk's combine runs on all N workers after
+                                  the GEMMs (section 4); the default */
+  MOE_WINDOW_LAST_COMBINE = 2  /* W_dispatch + W_combine (K-1)/K: only the last
+                                  chunk's combine is outside the window */
+} moe_steal_window;
+
 /* Hardware input of the cost model (section 3, Fig 4a/b, Fig 7a).
  * For grid point i: c[i] movement workers move bw_bytes_per_s[i] payload
  * bytes/s (BW(c)) while N - c[i] compute workers reach comp_flop_per_s[i]
@@ -90,13 +104,11 @@ typedef struct {
  * through the movement workers.  bw_all_bytes_per_s is the rate of all N
  * workers moving together: the last chunk's combine runs on every worker
  * (section 4), so the exposed tail of Eq 6/10 moves at that rate; 0 takes the
- * printed BW(c) instead.  head_on_all = 1 (the default) is the window of
- * Eq 11 under movement stealing: compute workers whose GEMM0 rows are not
- * dispatched yet copy rows themselves, so the first chunk's dispatch runs on
- * all N workers before any GEMM tile starts, and the movement workers' own
- * work while the GEMMs run is the dispatch of chunks 1..K-1 and the combine
- * of chunks 0..K-2, (W_dispatch + W_combine)(K-1)/K; 0 keeps the whole
- * dispatch in that window, W_dispatch + W_combine (K-1)/K. */
+ * printed BW(c) instead.  steal_window selects the window of Eq 11 (a
+ * moe_steal_window); steal_ceil = 1 (the default) rounds Eq 14's share
+ * W_steal / (N W_tile) up to whole tiles, 0 takes its whole part.  With
+ * literal_volumes = 1, bw_all = 0, MOE_WINDOW_PLAIN and steal_ceil = 0 the
+ * model is the printed equations as they stand. */
 typedef struct {
   int32_t n_c;
   int32_t c[MOE_CALIB_MAX_C];            /* ascending, 1 <= c < N */
@@ -109,7 +121,8 @@ typedef struct {
   int32_t literal_volumes;
   int32_t static_c;                      /* split used by MOE_MODE_STATIC */
   double bw_all_bytes_per_s;             /* >= 0; 0: tail at BW(c) */
-  int32_t head_on_all;                   /* 0 or 1 */
+  int32_t steal_window;                  /* a moe_steal_window */
+  int32_t steal_ceil;                    /* 0 or 1 */
 } moe_calib;
 
 /* Execution plan (section 3.3): the split, the chunk count and the steal count. */

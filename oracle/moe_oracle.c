@@ -224,14 +224,19 @@ void orc_plan(const orc_plan_in* in, orc_plan_out* out) {
   out->c = in->c[bc];
   out->K = in->K[bk];
   out->t_total = best;
-  /* bubble stealing at (c*, K*).  Eq 11's communication is what the movement
-   * workers still have to do while the GEMMs run: the combine of chunks
-   * 0..K-2 (the last chunk's combine runs on all N workers after the GEMMs,
-   * section 4) and the dispatch, without the first chunk's when every worker
-   * dispatches it before any GEMM tile can start. */
+  /* bubble stealing at (c*, K*).  Eq 11's communication volume, read as
+   * selected by steal_window (see moe_oracle.h): the plain reading takes the
+   * whole movement volume of Eq 5; the others leave out what every worker
+   * moves outside the window (the last chunk's combine, section 4, and under
+   * movement stealing the first chunk's dispatch). */
   double kd = (double)in->K[bk];
-  double w_win = in->head_on_all ? ((in->w_dispatch + in->w_combine) * (kd - 1.0)) / kd
-                                 : in->w_dispatch + (in->w_combine * (kd - 1.0)) / kd;
+  double w_win;
+  if (in->steal_window == 1)
+    w_win = ((in->w_dispatch + in->w_combine) * (kd - 1.0)) / kd;
+  else if (in->steal_window == 2)
+    w_win = in->w_dispatch + (in->w_combine * (kd - 1.0)) / kd;
+  else
+    w_win = in->w_dispatch + in->w_combine;
   double t_comm = w_win / in->bw[bc];                                  /* Eq 11 */
   double w_partial = t_comm * in->flops[bc];                           /* Eq 12 */
   double w_steal = in->w_comp - w_partial;                             /* Eq 13 */
@@ -240,9 +245,8 @@ void orc_plan(const orc_plan_in* in, orc_plan_out* out) {
   int n_steal = 0;
   if (nt > 0 && in->w_comp > 0.0) {
     double w_tile = in->w_comp / (double)nt;
-    /* Eq 14 gives a share, not a count: a movement worker claims up to the
-     * share rounded up (claims stop anyway once the queue is empty) */
-    n_steal = (int)ceil(w_steal / ((double)in->N * w_tile));           /* Eq 14 */
+    double share = w_steal / ((double)in->N * w_tile);                 /* Eq 14 */
+    n_steal = (int)(in->steal_ceil ? ceil(share) : floor(share));
   }
   out->n_steal = n_steal;
 }

@@ -120,11 +120,21 @@ typedef struct {
    * runs on every worker (section 4), so when bw_all > 0 the exposed tail of
    * Eq 6/10 moves at bw_all, else at BW(c) as printed */
   double bw_all;
-  /* nonzero: the first chunk's dispatch runs on all N workers before any GEMM
-   * tile starts (compute workers copy rows they are waiting for), so the
-   * window of Eq 11 holds (W_dispatch + W_combine)(K-1)/K; zero: the whole
-   * dispatch plus the combine of chunks 0..K-2 */
-  int head_on_all;
+  /* which movement work the window of Eq 11 holds (the paper leaves W_comm
+   * undefined there):
+   *   0  W_dispatch + W_combine, the volume of Eq 5 (the plain reading);
+   *   1  (W_dispatch + W_combine)(K-1)/K: the first chunk's dispatch runs on
+   *      all N workers before any GEMM tile starts (compute workers copy the
+   *      rows they wait for) and the last chunk's combine runs on all N
+   *      workers after the GEMMs (section 4), so neither is left to the
+   *      movement workers while the GEMMs run;
+   *   2  W_dispatch + W_combine (K-1)/K: only the last chunk's combine is
+   *      outside the window. */
+  int steal_window;
+  /* Eq 14 gives each movement worker a share W_steal / (N W_tile) of tiles;
+   * 0 takes its whole part (floor), 1 rounds it up (claims stop anyway once
+   * the compute queue is empty) */
+  int steal_ceil;
 } orc_plan_in;
 
 typedef struct {

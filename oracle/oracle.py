@@ -185,7 +185,8 @@ class PlanIn(C.Structure):
         ("n_k", C.c_int), ("K", C.c_void_p), ("eff", C.c_void_p), ("alpha", C.c_double),
         ("N", C.c_int),
         ("w_comp", C.c_double), ("w_dispatch", C.c_double), ("w_combine", C.c_double),
-        ("n_tiles", C.c_void_p), ("bw_all", C.c_double), ("head_on_all", C.c_int),
+        ("n_tiles", C.c_void_p), ("bw_all", C.c_double), ("steal_window", C.c_int),
+        ("steal_ceil", C.c_int),
     ]
 
 
@@ -206,7 +207,7 @@ class Plan:
 
 class _PlanArgs:
     def __init__(self, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0,
-                 head_on_all=0):
+                 steal_window=0, steal_ceil=0):
         self.c = _c(c, np.int32)
         self.bw = _c(bw, np.float64)
         self.flops = _c(flops, np.float64)
@@ -217,19 +218,28 @@ class _PlanArgs:
         assert self.K.shape == self.eff.shape == self.n_tiles.shape
         self.s = PlanIn(len(self.c), _p(self.c), _p(self.bw), _p(self.flops), len(self.K), _p(self.K),
                         _p(self.eff), float(alpha), int(N), float(w_comp), float(w_dispatch),
-                        float(w_combine), _p(self.n_tiles), float(bw_all), int(head_on_all))
+                        float(w_combine), _p(self.n_tiles), float(bw_all), int(steal_window),
+                        int(steal_ceil))
 
 
-def plan(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0, head_on_all=0) -> Plan:
-    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all, head_on_all)
+def plan(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0, steal_window=0,
+         steal_ceil=0) -> Plan:
+    """Eq 5, 9, 10, 15, 16 over the (c, K) grid, then Eq 11-14 at (c*, K*).
+
+    The defaults are the plain reading of the printed equations: the exposed
+    tail moves at BW(c) (bw_all = 0), Eq 11's window holds W_dispatch +
+    W_combine (steal_window = 0) and Eq 14's share is taken as whole tiles
+    (steal_ceil = 0).  The other values are the readings for one GPU (see
+    moe_oracle.h)."""
+    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all, steal_window,
+                  steal_ceil)
     o = PlanOut()
     lib().orc_plan(C.byref(a.s), C.byref(o))
     return Plan(o.c, o.K, o.n_steal, o.ci, o.ki, o.t_total)
 
 
-def t_total(ci, ki, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0,
-            head_on_all=0) -> float:
-    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all, head_on_all)
+def t_total(ci, ki, c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all=0.0) -> float:
+    a = _PlanArgs(c, bw, flops, K, eff, alpha, N, w_comp, w_dispatch, w_combine, n_tiles, bw_all)
     return lib().orc_t_total(C.byref(a.s), int(ci), int(ki))
 
 

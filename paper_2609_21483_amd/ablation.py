@@ -110,7 +110,7 @@ def run(workload: str, reps: int = 5, rounds: int = 3, log=print) -> dict:
             for j, K in enumerate(Ks):
                 points.append((c, K, B.make_calib([c], [cal.bw_bytes_per_s[i]], [cal.comp_flop_per_s[i]], [K],
                                                   [cal.eff_chunk[j]], cal.alpha, cal.static_c, cal.literal_volumes,
-                                                  cal.bw_all_bytes_per_s, cal.head_on_all)))
+                                                  cal.bw_all_bytes_per_s, cal.steal_window, cal.steal_ceil)))
         runs = {pt[:2]: [] for pt in points}
         plans = {}
         for _ in range(rounds):

@@ -27,6 +27,10 @@ MOE_ERR_TIMEOUT = -4
 MOE_ERR_ROUTING = -5
 MOE_ERR_STATE = -6
 
+MOE_WINDOW_PLAIN = 0
+MOE_WINDOW_MOVE_STEAL = 1
+MOE_WINDOW_LAST_COMBINE = 2
+
 MOE_MODE_DYNAMIC = 0
 MOE_MODE_STATIC = 1
 MOE_MODE_SERIAL = 2
@@ -49,7 +53,7 @@ class moe_calib(C.Structure):
         ("bw_bytes_per_s", C.c_double * CALIB_MAX_C), ("comp_flop_per_s", C.c_double * CALIB_MAX_C),
         ("n_k", C.c_int32), ("k_chunks", C.c_int32 * CALIB_MAX_K), ("eff_chunk", C.c_double * CALIB_MAX_K),
         ("alpha", C.c_double), ("literal_volumes", C.c_int32), ("static_c", C.c_int32),
-        ("bw_all_bytes_per_s", C.c_double), ("head_on_all", C.c_int32),
+        ("bw_all_bytes_per_s", C.c_double), ("steal_window", C.c_int32), ("steal_ceil", C.c_int32),
     ]
 
 
@@ -287,7 +291,7 @@ def make_config(shape, n_workers: int = 0, first_local_expert: int = 0, gemm1_sp
 
 
 def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int = 0, bw_all: float = 0.0,
-               head_on_all: int = 1) -> moe_calib:
+               steal_window: int = 1, steal_ceil: int = 1) -> moe_calib:
     k = moe_calib()
     k.n_c = len(c)
     for i, (cv, b, f) in enumerate(zip(c, bw, flops)):
@@ -299,7 +303,8 @@ def make_calib(c, bw, flops, K, eff, alpha: float, static_c: int, literal: int =
     k.literal_volumes = int(literal)
     k.static_c = int(static_c)
     k.bw_all_bytes_per_s = float(bw_all)
-    k.head_on_all = int(head_on_all)
+    k.steal_window = int(steal_window)
+    k.steal_ceil = int(steal_ceil)
     return k
 
 

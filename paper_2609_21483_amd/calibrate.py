@@ -52,7 +52,7 @@ def load_calib(workload: str, N: int):
     if int(d.get("N", -1)) != N:
         return None
     return B.make_calib(d["c"], d["bw"], d["flops"], d["K"], d["eff"], d["alpha"], d["static_c"], d.get("literal", 0),
-                        d.get("bw_all", 0.0), d.get("head_on_all", 1))
+                        d.get("bw_all", 0.0), d.get("steal_window", 1), d.get("steal_ceil", 1))
 
 
 def _time(fn, reps: int) -> float:
@@ -139,7 +139,7 @@ def calibrate(workload: str, reps: int = 5, c_grid=None, log=print) -> dict:
         static_c = max(1, min(N - 1, int(round(N * 20 / 132 / 8)) * 8))
         return {
             "workload": workload, "N": N, "c": c_grid, "bw": bw, "flops": fl, "K": Ks, "eff": eff,
-            "alpha": alpha, "static_c": static_c, "literal": 0, "bw_all": bw_all, "head_on_all": 1,
+            "alpha": alpha, "static_c": static_c, "literal": 0, "bw_all": bw_all, "steal_window": 1, "steal_ceil": 1,
             "eff_gemm": eff_gemm,
             "sweep": [[c_grid[ci], Ks[ki], t] for ci, ki, t in sweep],
             "device": torch.cuda.get_device_name(0), "date": time.strftime("%Y-%m-%d"),

@@ -115,7 +115,10 @@ moe_status validate_calib(const moe_calib* k, int N) {
   if (k->static_c < 1 || k->static_c >= N) return fail(MOE_ERR_INVALID_ARG, "static_c must be in [1, N-1]");
   if (!(k->bw_all_bytes_per_s >= 0) || !std::isfinite(k->bw_all_bytes_per_s))
     return fail(MOE_ERR_INVALID_ARG, "bw_all must be >= 0 and finite");
-  if (k->head_on_all != 0 && k->head_on_all != 1) return fail(MOE_ERR_INVALID_ARG, "head_on_all must be 0 or 1");
+  if (k->steal_window != MOE_WINDOW_PLAIN && k->steal_window != MOE_WINDOW_MOVE_STEAL &&
+      k->steal_window != MOE_WINDOW_LAST_COMBINE)
+    return fail(MOE_ERR_INVALID_ARG, "steal_window must be a MOE_WINDOW_* value");
+  if (k->steal_ceil != 0 && k->steal_ceil != 1) return fail(MOE_ERR_INVALID_ARG, "steal_ceil must be 0 or 1");
   return MOE_OK;
 }
 
@@ -145,7 +148,8 @@ void default_calib(int N, moe_calib* k) {
   int sc = (int)std::lround(N * 20.0 / 132.0 / 8.0) * 8;  // 20 of 132 SMs, rounded to XCD multiples
   k->static_c = std::min(std::max(sc, 1), N - 1);
   k->bw_all_bytes_per_s = 4.0e12;  // all workers copying together
-  k->head_on_all = 1;
+  k->steal_window = MOE_WINDOW_MOVE_STEAL;
+  k->steal_ceil = 1;
 }
 
 void to_dev(const moe_calib& k, DevCalib* d) {
@@ -158,7 +162,8 @@ void to_dev(const moe_calib& k, DevCalib* d) {
   d->literal = k.literal_volumes;
   d->static_c = k.static_c;
   d->bw_all = k.bw_all_bytes_per_s;
-  d->head_on_all = k.head_on_all;
+  d->steal_window = k.steal_window;
+  d->steal_ceil = k.steal_ceil;
 }
 
 void compute_layout(moe_handle* h) {

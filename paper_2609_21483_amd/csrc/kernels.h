@@ -73,7 +73,8 @@ struct DevCalib {
   int32_t literal;
   int32_t static_c;
   double bw_all;  // > 0: the exposed tail moves at this rate (all N workers)
-  int32_t head_on_all;  // the first chunk's dispatch is outside the Eq 11 window
+  int32_t steal_window;  // MOE_WINDOW_*: the movement volume of the Eq 11 window
+  int32_t steal_ceil;    // Eq 14's share rounded up (1) or down (0)
 };
 
 struct FwdArgs {
@@ -149,12 +150,16 @@ __host__ __device__ inline void cm_finish(const DevCalib& cb, int N, double w_co
                                           const long long* n_tiles_by_k, int bc, int bk, double best,
                                           moe_plan* out) {
 #pragma clang fp contract(off)
-  // Eq 11 over the window the movement workers have while the GEMMs run:
-  // the combine of chunks 0..K-2 (the last chunk's combine runs on all N
-  // workers afterwards) and the dispatch, less the first chunk's when all
-  // workers dispatch it before any GEMM tile starts (movement stealing)
-  double kd = (double)cb.kk[bk];
-  double w_win = cb.head_on_all ? ((w_disp + w_comb) * (kd - 1.0)) / kd : w_disp + (w_comb * (kd - 1.0)) / kd;
+  // Eq 11 over the window the movement workers have while the GEMMs run
+  // (W_comm is not defined there): the whole movement volume of Eq 5
+  // (MOE_WINDOW_PLAIN); less the last chunk's combine, which runs on all N
+  // workers afterwards (MOE_WINDOW_LAST_COMBINE); less also the first chunk's
+  // dispatch when all workers copy it before any GEMM tile starts (movement
+  // stealing, MOE_WINDOW_MOVE_STEAL)
+  const double kd = (double)cb.kk[bk];
+  double w_win = w_disp + w_comb;
+  if (cb.steal_window == MOE_WINDOW_MOVE_STEAL) w_win = ((w_disp + w_comb) * (kd - 1.0)) / kd;
+  else if (cb.steal_window == MOE_WINDOW_LAST_COMBINE) w_win = w_disp + (w_comb * (kd - 1.0)) / kd;
   double t_comm = w_win / cb.bw[bc];                         // Eq 11
   double w_partial = t_comm * cb.fl[bc];                     // Eq 12
   double w_steal = w_comp - w_partial;                       // Eq 13
@@ -163,9 +168,10 @@ __host__ __device__ inline void cm_finish(const DevCalib& cb, int N, double w_co
   int n_steal = 0;
   if (nt > 0 && w_comp > 0.0) {
     double w_tile = w_comp / (double)nt;
-    // Eq 14 gives a share, not a count: a movement worker claims up to the
-    // share rounded up (claims stop anyway once the queue is empty)
-    n_steal = (int)ceil(w_steal / ((double)N * w_tile));    // Eq 14
+    // Eq 14 gives a share, not a count: whole tiles, or the share rounded up
+    // (a movement worker's claims stop anyway once the queue is empty)
+    const double share = w_steal / ((double)N * w_tile);    // Eq 14
+    n_steal = (int)(cb.steal_ceil ? ceil(share) : floor(share));
   }
   out->c = cb.c[bc];
   out->K = cb.kk[bk];

@@ -58,7 +58,7 @@ def test_init_rejects_bad_calib():
     B.moe_destroy(h)
     for bad in [dict(c=[16, 8]), dict(c=[8, 256]), dict(bw=[0.0, 1.0]), dict(K=[1, 3]), dict(eff=[1.0, 1.5]),
                 dict(alpha=2.0), dict(static_c=0), dict(bw_all=-1.0), dict(bw_all=float("inf")),
-                dict(head_on_all=2), dict(head_on_all=-1)]:
+                dict(steal_window=3), dict(steal_window=-1), dict(steal_ceil=2)]:
         kw = {**good, **bad}
         with pytest.raises(B.MoeError):
             B.moe_init(c, B.make_calib(**kw))
@@ -147,11 +147,12 @@ def test_host_cost_model_matches_oracle(orc):
             wc, wd, wb = float(rng.uniform(0, 1e13)), float(rng.uniform(0, 2e9)), float(rng.uniform(0, 2e9))
             nt = rng.integers(0, 5000, len(Ks))
             bw_all = 0.0 if trial % 3 == 0 else float(rng.uniform(1e11, 8e12))
-            head = trial % 2
+            window, ceil_ = trial % 3, (trial // 3) % 2
             B.moe_set_calib(h, B.make_calib(cs, bw, fl, Ks, eff, alpha, static_c=int(cs[0]), bw_all=bw_all,
-                                            head_on_all=head))
+                                            steal_window=window, steal_ceil=ceil_))
             p = B.moe_plan_host(h, wc, wd, wb, list(nt) + [0] * (4 - len(Ks)))
-            o = orc.plan(cs, bw, fl, Ks, eff, alpha, 256, wc, wd, wb, nt, bw_all=bw_all, head_on_all=head)
+            o = orc.plan(cs, bw, fl, Ks, eff, alpha, 256, wc, wd, wb, nt, bw_all=bw_all, steal_window=window,
+                         steal_ceil=ceil_)
             assert (p.c, p.K, p.n_steal) == (o.c, o.K, o.n_steal), trial
             assert p.t_pred_s == o.t_total, trial
     finally:

@@ -328,6 +328,9 @@ def _linear_grid(N, beta, phi, cs):
     return cs, beta * cs.astype(np.float64), phi * (N - cs).astype(np.float64)
 
 
+WINDOWS = {"plain": 0, "move_steal": 1, "last_combine": 2}
+
+
 def test_cost_model_hand_example(orc):
     d = json.load(open(os.path.join(GOLDEN, "cost_model_hand_example.json")))
     args = dict(c=d["c"], bw=d["bw"], flops=d["flops"], K=d["K"], eff=d["eff"], alpha=d["alpha"],
@@ -339,12 +342,15 @@ def test_cost_model_hand_example(orc):
         assert math.isclose(t32, d["expected_t_total_c32"][ki], rel_tol=4e-16)
     assert orc.t_total(1, 0, n_tiles=[1, 1, 1], **args) == 4.5
     assert orc.t_total(2, 2, n_tiles=[1, 1, 1], **args) == 12.0625
-    for n_tiles, n_steal in d["cases_n_tiles"]:
-        p = orc.plan(n_tiles=n_tiles, **args)
-        num, den = d["expected_t_total_min_num_den"]
-        assert (p.c, p.K) == (d["expected_c"], d["expected_K"])
-        assert math.isclose(p.t_total, num / den, rel_tol=5e-16)
-        assert p.n_steal == n_steal
+    for case in d["cases_n_tiles"]:
+        for reading, n_steal in case["n_steal"].items():
+            window, rounding = reading.rsplit("_", 1)
+            p = orc.plan(n_tiles=case["n_tiles"], steal_window=WINDOWS[window], steal_ceil=int(rounding == "ceil"),
+                         **args)
+            num, den = d["expected_t_total_min_num_den"]
+            assert (p.c, p.K) == (d["expected_c"], d["expected_K"])
+            assert math.isclose(p.t_total, num / den, rel_tol=5e-16)
+            assert p.n_steal == n_steal, reading
 
 
 def test_cost_model_hand_example_all_worker_tail(orc):
@@ -353,7 +359,7 @@ def test_cost_model_hand_example_all_worker_tail(orc):
     combine on every worker): Eq 10 becomes 0.5 * 2^34 / (2^36 K) = 1/(8K) s.
     c=16: K=1 max(4 + 1/8, 1.5) = 4.125; K=2 4/0.75 + 1/16 = 259/48; K=4 8 + 1/32.
     c=32: 6.125; 8.0625; 12.03125.  c=8, K=1: 192/56 + 1/8 = 199/56 (minimum).
-    n_steal (Eq 11-14) does not use the tail: 1 and 544 as before."""
+    n_steal (Eq 11-14) does not use the tail: the same counts as without it."""
     d = json.load(open(os.path.join(GOLDEN, "cost_model_hand_example.json")))
     args = dict(c=d["c"], bw=d["bw"], flops=d["flops"], K=d["K"], eff=d["eff"], alpha=d["alpha"],
                 N=d["N"], w_comp=d["w_comp"], w_dispatch=d["w_dispatch"], w_combine=d["w_combine"],
@@ -364,11 +370,11 @@ def test_cost_model_hand_example_all_worker_tail(orc):
     assert orc.t_total(2, 0, n_tiles=[1, 1, 1], **args) == 6.125
     assert orc.t_total(2, 1, n_tiles=[1, 1, 1], **args) == 8.0625
     assert orc.t_total(2, 2, n_tiles=[1, 1, 1], **args) == 12.03125
-    for n_tiles, n_steal in d["cases_n_tiles"]:
-        p = orc.plan(n_tiles=n_tiles, **args)
+    for case in d["cases_n_tiles"]:
+        p = orc.plan(n_tiles=case["n_tiles"], **args)
         assert (p.c, p.K) == (8, 1)
         assert math.isclose(p.t_total, 199 / 56, rel_tol=5e-16)
-        assert p.n_steal == n_steal
+        assert p.n_steal == case["n_steal"]["plain_floor"]
 
 
 def test_cost_model_balance_point(orc):
@@ -426,35 +432,58 @@ def test_cost_model_tie_break_first_minimum(orc):
 
 
 def test_n_steal_formula_by_hand(orc):
-    # Eq 11 counts dispatch plus the combine of chunks 0..K-2 (the last chunk's
-    # combine runs on every worker after the GEMMs).
-    # K = 1: t_comm = 1e9/1e12 = 1 ms; W_partial = 1e-3 * 5e14 = 5e11; W_steal = 4e12 - 5e11 = 3.5e12;
-    # W_tile = 4e12/4000 = 1e9; n_steal = ceil(3.5e12 / (100 * 1e9)) = 35
-    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
+    # The plain reading of Eq 11: W_comm = W_dispatch + W_combine, the volume
+    # of Eq 5, whatever K; Eq 14's share taken as whole tiles.
+    # t_comm = 2e9/1e12 = 2 ms; W_partial = 2e-3 * 5e14 = 1e12; W_steal = 4e12 - 1e12 = 3e12;
+    # W_tile = 4e12/4000 = 1e9; share = 3e12 / (100 * 1e9) = 30
+    for K in (1, 2, 4):
+        p = orc.plan([20], [1e12], [5e14], [K], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
+        assert p.n_steal == 30
+    # a share that is not whole: W_comp = 4.05e12 -> W_steal = 3.05e12, W_tile = 1.0125e9,
+    # share = 3.05e12 / 1.0125e11 = 30.12..: 30 whole tiles, 31 rounded up
+    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4.05e12, 1e9, 1e9, [4000])
+    assert p.n_steal == 30
+    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4.05e12, 1e9, 1e9, [4000], steal_ceil=1)
+    assert p.n_steal == 31
+    # communication longer than the GEMMs: W_partial > W_comp, nothing to steal (Eq 13's max)
+    p = orc.plan([20], [1e10], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_ceil=1)
+    assert p.n_steal == 0
+
+
+def test_n_steal_formula_by_hand_last_combine_window(orc):
+    # Eq 11 window without the last chunk's combine (it runs on every worker
+    # after the GEMMs, section 4): W_dispatch + W_combine (K-1)/K.
+    # K = 1: t_comm = 1e9/1e12 = 1 ms; W_partial = 5e11; W_steal = 3.5e12;
+    # W_tile = 1e9; n_steal = 3.5e12 / (100 * 1e9) = 35
+    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=2)
     assert p.n_steal == 35
     # K = 2: t_comm = (1e9 + 1e9/2)/1e12 = 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12;
-    # n_steal = ceil(3.25e12 / (100 * 1e9)) = ceil(32.5) = 33
-    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000])
+    # share 32.5: 32 whole tiles, 33 rounded up
+    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=2)
+    assert p.n_steal == 32
+    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=2, steal_ceil=1)
     assert p.n_steal == 33
 
 
-def test_n_steal_formula_by_hand_head_on_all(orc):
+def test_n_steal_formula_by_hand_move_steal_window(orc):
     # With every worker dispatching the first chunk before any GEMM tile can
     # start, Eq 11's window is (W_dispatch + W_combine)(K-1)/K.
-    # K = 1: empty window; W_steal = W_comp = 4e12; n_steal = ceil(4e12 / (100 * 1e9)) = 40
-    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    # K = 1: empty window; W_steal = W_comp = 4e12; n_steal = 4e12 / (100 * 1e9) = 40
+    p = orc.plan([20], [1e12], [5e14], [1], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=1)
     assert p.n_steal == 40
     # K = 2: window 2e9 / 2 = 1e9 bytes -> 1 ms; W_partial = 5e11; W_steal = 3.5e12; n_steal = 35
-    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    p = orc.plan([20], [1e12], [5e14], [2], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=1)
     assert p.n_steal == 35
-    # K = 4: window 2e9 * 3/4 = 1.5e9 bytes -> 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12; n_steal = 33
-    p = orc.plan([20], [1e12], [5e14], [4], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], head_on_all=1)
+    # K = 4: window 2e9 * 3/4 = 1.5e9 bytes -> 1.5 ms; W_partial = 7.5e11; W_steal = 3.25e12;
+    # share 32.5: 32 whole tiles, 33 rounded up
+    p = orc.plan([20], [1e12], [5e14], [4], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=1)
+    assert p.n_steal == 32
+    p = orc.plan([20], [1e12], [5e14], [4], [1.0], 1.0, 100, 4e12, 1e9, 1e9, [4000], steal_window=1, steal_ceil=1)
     assert p.n_steal == 33
-    # the window does not enter T_total (Eq 15): same plan and prediction either way
-    a = orc.plan([8, 16], [1e11, 2e11], [1e15, 9e14], [1, 2], [1.0, 0.9], 0.5, 64, 1e12, 2e8, 2e8, [1000, 1100])
-    b = orc.plan([8, 16], [1e11, 2e11], [1e15, 9e14], [1, 2], [1.0, 0.9], 0.5, 64, 1e12, 2e8, 2e8, [1000, 1100],
-                 head_on_all=1)
-    assert (a.c, a.K, a.t_total) == (b.c, b.K, b.t_total)
+    # the window does not enter T_total (Eq 15): same plan and prediction under every reading
+    plans = [orc.plan([8, 16], [1e11, 2e11], [1e15, 9e14], [1, 2], [1.0, 0.9], 0.5, 64, 1e12, 2e8, 2e8,
+                      [1000, 1100], steal_window=w) for w in (0, 1, 2)]
+    assert len({(p.c, p.K, p.t_total) for p in plans}) == 1
 
 
 def test_tile_count_bruteforce(orc):
@@ -484,3 +513,20 @@ def test_volumes_invariants(orc):
     assert wd <= wcb   # X_in^uniq <= X_in (section 3.1)
     wc2, wd2, wcb2 = orc.volumes(tab, H, F, 0, literal=False)
     assert wc2 == wc and wd2 >= wd and wcb2 >= wcb
+    # every row moved: one row per unique token of any rank (brute force over
+    # the routing) and one per local pair
+    U_all = sum(1 for g in range(R * Tr) if np.any(idx[g] < El))
+    assert wd2 == U_all * 2 * H and wcb2 == tab.X * 2 * H
+
+
+def test_volumes_hand_example(orc):
+    """Eq 1-3 on the hand-made routing of tests/golden/volumes_hand_example.json,
+    exact, under both readings of the movement volumes."""
+    d = json.load(open(os.path.join(GOLDEN, "volumes_hand_example.json")))
+    idx = np.array(d["topk_idx"], np.int32)
+    tab = orc.route_tables(idx, d["R"], d["Tr"], d["e0"], d["El"])
+    for shared_rows, w_comp in d["shared_rows_cases"]:
+        for literal, key in ((True, "literal"), (False, "all_rows")):
+            wc, wd, wb = orc.volumes(tab, d["H"], d["F"], shared_rows, literal=literal)
+            assert wc == w_comp
+            assert (wd, wb) == (d[key]["w_dispatch"], d[key]["w_combine"]), key
