@@ -1,20 +1,27 @@
 """MoE-layer benchmark on one MI355X.
 
-One step = one pass of the whole hot path over one batch: top-k routing
-(moe_route: gate logits, softmax, top-k, routing tables) followed by the MoE
-layer (moe_forward: dispatch, GEMM0 + SiLU*up, GEMM1, combine) in the
-dynamic-split megakernel.  Inputs are resident in HBM before timing starts.
+One step = one pass of the whole hot path over one batch of T tokens through
+the workload's stack of layers: for each layer, top-k routing (moe_route: gate
+logits, softmax, top-k, routing tables) and then the MoE layer (moe_forward:
+dispatch, GEMM0 + SiLU*up, GEMM1, combine) in the dynamic-split megakernel.
+The default workload is the 8-layer large fine-grained stack (E=128, k=8,
+H=4096, F=1536, 32 local experts, 4 source ranks x 8192 tokens, a Zipf
+routing skew drawn per layer), the largest configuration that fits one GPU;
+its layers are independent draws sharing one x and run back to back on one
+stream.  Inputs are resident in HBM before timing starts.
 
-Prints one JSON line.  `value` is tokens/s of whole steps; `layer_us` is the
-MoE-layer time alone (the megakernel, from HIP events on its launch stream,
-the window the paper times: end of routing to end of combine).  `baselines`
-holds the static-split and serial modes and the dynamic mode again, all timed
-as back-to-back forward launches in interleaved rounds; `dynamic_speedup` is a
-baseline's time over the dynamic time measured that way.  `roofline` rates the
-megakernel (the dominant kernel) against the bf16 MFMA peak; `phases` comes
-from one extra traced launch after the timed region and gives the movement
-workers' HBM rate, the compute workers' MFMA utilisation, and SM Active and
-movement/compute overlap (paper_2609_21483_amd.timeline).
+Prints one JSON line.  `value` is tokens/s of whole steps (T tokens through
+every layer of the stack, routing included).  `layers` gives each layer's
+plan (c*, K*, n_steal), MoE-layer time (the megakernel, from HIP events on its
+launch stream: the window the paper times, end of routing to end of combine),
+its time with L2 and MALL flushed before each launch, routing time and the
+static-split and serial baselines, all timed as back-to-back stacks in
+interleaved rounds.  `roofline` rates the megakernel (the dominant kernel)
+against the bf16 MFMA peak over the stack's launches; `phases` comes from one
+extra traced launch per layer after the timed region.  `per_config` holds the
+other workloads (one layer each).  `cpu_baseline` times the oracle on a
+bounded sample of rows, single-threaded and on the host cores; the oracle's
+sampled rows are then compared with the GPU's routing and y (`y_check`).
 """
 from __future__ import annotations
 
@@ -36,22 +43,32 @@ METRIC = "MoE-layer µs + tokens/s at 1 GPU; HBM GB/s & MFMA util vs peak"
 KERNEL_SOURCES = ("paper_2609_21483_amd/csrc/forward.hip", "paper_2609_21483_amd/csrc/gemm.h",
                   "paper_2609_21483_amd/csrc/common.h", "paper_2609_21483_amd/csrc/kernels.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "megakernel_traffic.json")
+TOL = 2e-2  # max|y - y_ref| <= TOL * max|y_ref| over the checked rows
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mixtral_ep4")
-    ap.add_argument("--layer", type=int, default=0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=128)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large_stack")
+    ap.add_argument("--layers", default="", help="comma list of layers of the stack (default: all)")
+    ap.add_argument("--extra", default="tiny,mixtral_ep4,fine_zipf,shared_routed",
+                    help="other workloads measured one layer each (per_config)")
     ap.add_argument("--modes", default="static,serial", help="baselines timed next to the dynamic mode")
     ap.add_argument("--rounds", type=int, default=3, help="interleaved rounds of the baseline comparison")
+    ap.add_argument("--reps", type=int, default=5, help="stack runs per mode and round")
+    ap.add_argument("--flush-mib", type=int, default=512, help="scratch written before each flushed launch")
+    ap.add_argument("--no-trace", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=2, help="oracle rows per rank and layer, single-thread leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain torch copy of this many MiB (the scale for PMC byte counters)")
     return ap.parse_args()
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def kernel_sources_hash() -> str:
@@ -82,36 +99,107 @@ def measured_traffic(workload: str):
     return float(rec["bytes_per_launch"])
 
 
-def time_forward(B, layer, x, idx, w, y, mode, steps, warmup, stream):
+class Stack:
+    """The layers of one workload on the GPU: per layer a handle with its own
+    workspace and packed weights, its gate and bias, and its routing and output
+    buffers; x is shared by every layer."""
+
+    def __init__(self, B, W, shape, layers, N, keep_host: bool):
+        import torch
+        from paper_2609_21483_amd.calibrate import load_calib
+        self.shape, self.ids = shape, list(layers)
+        self.calib = load_calib(shape.name, N)
+        self.x_host = W.tokens(shape)
+        self.x = self.x_host.cuda()
+        self.L, self.host = [], []
+        for l in self.ids:
+            log(f"{shape.name} layer {l}: drawing and packing weights")
+            wg, bias = W.gate(shape, l), W.zipf_log_prior(shape, l)
+            ex, sh = W.experts(shape, l), W.shared_experts(shape, l)
+            layer = B.MoeLayer(shape, *ex, *sh, calib=self.calib)
+            d = dict(layer=layer, wg=wg.cuda(), bias=None if bias is None else bias.cuda(),
+                     idx=torch.empty((shape.T, shape.top_k), dtype=torch.int32, device="cuda"),
+                     w=torch.empty((shape.T, shape.top_k), dtype=torch.float32, device="cuda"),
+                     y=torch.empty((shape.T, shape.hidden), dtype=torch.bfloat16, device="cuda"))
+            self.L.append(d)
+            self.host.append(dict(wg=wg, bias=bias, ex=ex, sh=sh) if keep_host else None)
+        torch.cuda.synchronize()
+
+    def route(self, i, stream):
+        d = self.L[i]
+        d["layer"].route(self.x, d["wg"], d["bias"], d["idx"], d["w"], stream=stream)
+
+    def forward(self, i, mode, stream):
+        d = self.L[i]
+        d["layer"].forward(self.x, d["idx"], d["w"], d["y"], mode, stream=stream)
+
+    def check(self, B, stream):
+        for d in self.L:
+            st = B.moe_sync_status(d["layer"].h, stream)
+            if st != B.MOE_OK:
+                raise RuntimeError(B.moe_last_error())
+
+    def close(self):
+        import torch
+        torch.cuda.synchronize()
+        for d in self.L:
+            d["layer"].close()
+        self.L = []
+        self.x = None
+        torch.cuda.synchronize()
+
+
+def time_stack(stack, mode, reps, stream):
+    """Back-to-back stacks of forward launches on the current routing: per
+    layer, the launch durations (us) from HIP events on the launch stream."""
     import torch
-    for _ in range(warmup):
-        layer.forward(x, idx, w, y, mode, stream=stream)
+    n = len(stack.L)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+          for _ in range(reps)]
+    for r in range(reps):
+        for i in range(n):
+            ev[r][i][0].record(stream)
+            stack.forward(i, mode, stream)
+            ev[r][i][1].record(stream)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in ev:
-        a.record(stream)
-        layer.forward(x, idx, w, y, mode, stream=stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    st = B.moe_sync_status(layer.h, stream)
-    if st != B.MOE_OK:
-        raise RuntimeError(f"{mode}: {B.moe_last_error()}")
-    return [a.elapsed_time(b) * 1e3 for a, b in ev]  # us
+    return [[ev[r][i][0].elapsed_time(ev[r][i][1]) * 1e3 for r in range(reps)] for i in range(n)]
 
 
-def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
+def time_flushed(stack, reps, stream, flush):
+    """Per layer, dynamic launches with L2 and MALL flushed before each one (a
+    scratch write outside the events)."""
+    import torch
+    out = []
+    for i in range(len(stack.L)):
+        ts = []
+        for _ in range(reps):
+            flush.zero_()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            stack.forward(i, "dynamic", stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        out.append(ts)
+    return out
+
+
+def traced_phases(B, stack, i, stream, stats, flops):
     """One traced launch: movement bytes over the movers' dispatch window and
     the compute workers' MFMA utilisation over their busy time."""
-    import numpy as np
     import torch
-    buf = torch.zeros(64 + 32 * (1 << 17), dtype=torch.uint8, device="cuda")
-    B.moe_set_trace(layer.h, buf)
+    from paper_2609_21483_amd import timeline as TL
+    d = stack.L[i]
+    shape = stack.shape
+    buf = torch.zeros(64 + 32 * (1 << 18), dtype=torch.uint8, device="cuda")
+    B.moe_set_trace(d["layer"].h, buf)
     try:
-        layer.forward(x, idx, w, y, "dynamic", stream=stream)
+        stack.forward(i, "dynamic", stream)
         torch.cuda.synchronize()
     finally:
-        B.moe_set_trace(layer.h, None)
+        B.moe_set_trace(d["layer"].h, None)
     tr = B.read_trace(buf)
+    del buf
     wgs, tiles, disp, comb = (tr[tr["kind"] == k] for k in (1, 2, 3, 4))
     if len(wgs) == 0:
         return None
@@ -127,7 +215,6 @@ def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
     span = float(us(wgs["t2"]).max())
     comb_span = float((us(comb["t2"]).max() - us(comb["t1"]).min())) if len(comb) else float("nan")
     per_cu_peak = PEAK_BF16_TFLOPS / 256.0
-    from paper_2609_21483_amd import timeline as TL
     tl = TL.metrics(tr)
     return {
         "traced_layer_us": span,
@@ -143,43 +230,189 @@ def traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops):
         "overlap": tl["overlap"],
         "overlap_of_movement": tl["overlap_of_mov"],
         "prologue_us": tl["prologue_us"],
-        "note": "one traced launch (tracing adds overhead); dispatch includes rows moved by compute workers "
-                "that steal movement while their tiles wait",
     }
 
 
-def cpu_baseline(shape, c, rows_n):
-    """The oracle as it stands, single-threaded, on a bounded sample: routing
-    of every token (scaled to the sample's share) plus the layer for the first
-    rows_n/R tokens of each rank."""
-    import numpy as np
-    from oracle import oracle as O
-    from paper_2609_21483_amd import workloads as W
+def layer_stats(stack, i):
+    return stack.L[i]["layer"].ws_view("stats", __import__("torch").int32, 16).cpu().numpy()
 
-    xu = W.as_u16_numpy(c["x"])
+
+def layer_flops(shape, stats):
+    return (int(stats[0]) + shape.n_shared_experts * shape.tokens_per_rank) * 6.0 * shape.hidden * shape.ffn
+
+
+def host_info():
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return {"cpu_model": model, "nproc": os.cpu_count(), "affinity_cpus": aff}
+
+
+def cpu_baseline(stack, W, per_rank, cores):
+    """The oracle as it stands on a bounded sample, timed on the host: for
+    `per_rank` seeded tokens of each source rank and every layer of the stack,
+    routing (gate logits, softmax, top-k of those rows: rows are independent)
+    and the layer's output rows.  First on one thread, then `cores` threads
+    on `cores` times as many rows (the C oracle releases the interpreter lock,
+    so the threads run in parallel).  tokens/s = sampled tokens through all
+    layers / wall time.  Returns the baseline and the oracle's rows of the
+    single-thread leg (for the check against the GPU)."""
+    import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import oracle as O
+
+    shape = stack.shape
+    xu = W.as_u16_numpy(stack.x_host)
+    Tr = shape.tokens_per_rank
+    u16 = W.as_u16_numpy
+
+    def run_rows(li, rows):
+        hst = stack.host[li]
+        lg = O.gate_logits(xu[rows], u16(hst["wg"]), None if hst["bias"] is None else hst["bias"].numpy())
+        idx, w = O.softmax_topk(lg, shape.top_k)
+        ws = [u16(t) for t in hst["sh"]]
+        y = np.empty((len(rows), shape.hidden), np.float64)
+        r0 = rows < Tr  # shared experts apply to rank-0 tokens
+        for sel, tr in ((r0, int(r0.sum())), (~r0, 0)):
+            if sel.any():
+                y[sel] = O.layer_rows(xu[rows[sel]], idx[sel], w[sel], *(u16(t) for t in hst["ex"]), *ws, Tr=tr)
+        return idx, w, y
+
+    samples = [W.sample_tokens(shape, per_rank, seed=900 + l) for l in stack.ids]
     t0 = time.perf_counter()
-    lg = O.gate_logits(xu, W.as_u16_numpy(c["wg"]), None if c["bias"] is None else c["bias"].numpy())
-    idx, w = O.softmax_topk(lg, shape.top_k)
-    tab = O.route_tables(idx, shape.n_src_ranks, shape.tokens_per_rank, 0, shape.n_local_experts)
-    t_route = time.perf_counter() - t0
-    per = max(1, rows_n // shape.n_src_ranks)
-    rows = np.concatenate([r * shape.tokens_per_rank + np.arange(per) for r in range(shape.n_src_ranks)])
-    t1 = time.perf_counter()
-    O.layer_rows(xu, idx, w, *(W.as_u16_numpy(c[k]) for k in ("w1", "w3", "w2")),
-                 *(W.as_u16_numpy(c[k]) for k in ("ws1", "ws3", "ws2")), Tr=shape.tokens_per_rank, rows=rows)
-    t_rows = time.perf_counter() - t1
-    n = rows.shape[0]
-    t = t_route * n / shape.T + t_rows
-    return {"value": n / t, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"routing+tables of all {shape.T} tokens ({t_route:.2f}s, scaled by {n}/{shape.T}) + "
-                      f"layer rows of {n} tokens ({per} per rank, {t_rows:.2f}s), {tab.X} local pairs in total"}
+    ref = [run_rows(i, rows) for i, rows in enumerate(samples)]
+    t1 = time.perf_counter() - t0
+    n1 = len(samples[0])
+    # host cores: each thread takes its own rows of every layer
+    big = [W.sample_tokens(shape, min(Tr, per_rank * cores), seed=1900 + l) for l in stack.ids]
+    shards = [[(i, b[c::cores]) for i, b in enumerate(big)] for c in range(cores)]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(cores) as ex:
+        list(ex.map(lambda sh: [run_rows(i, r) for i, r in sh if len(r)], shards))
+    tc = time.perf_counter() - t0
+    nc = len(big[0])
+    info = host_info()
+    base = {"value": nc / tc, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{nc} seeded tokens ({nc // shape.n_src_ranks} per rank) through all {len(stack.ids)} "
+                      f"layers (routing of those rows + the layer's output rows), {cores} threads, {tc:.1f} s",
+            "single_thread": {"value": n1 / t1, "unit": "tokens/s", "cores": 1,
+                              "sample": f"{n1} tokens through all {len(stack.ids)} layers, {t1:.1f} s"},
+            **info}
+    return base, samples, ref
+
+
+def y_check(stack, samples, ref):
+    """The oracle's sampled rows (from the CPU-baseline leg) against the GPU's
+    routing and output of the last step, layer by layer."""
+    import numpy as np
+    worst, exact, n = 0.0, True, 0
+    for i, (rows, (idx, w, y)) in enumerate(zip(samples, ref)):
+        d = stack.L[i]
+        sel = __import__("torch").from_numpy(rows).cuda()
+        idx_g = d["idx"][sel].cpu().numpy()
+        exact &= bool(np.array_equal(idx_g, idx))
+        yg = d["y"][sel].float().cpu().numpy().astype(np.float64)
+        m = float(np.max(np.abs(y)))
+        worst = max(worst, float(np.max(np.abs(yg - y))) / (m if m > 0 else 1.0))
+        n += len(rows)
+    return {"rows": n, "layers": len(samples), "routing_ids_exact": exact, "max_err_over_max_ref": worst,
+            "tolerance": TOL, "ok": bool(exact and worst <= TOL)}
+
+
+def measure_stack(B, stack, args, stream, flush, trace: bool):
+    """Timed steps, then the baselines, flushed launches and traces."""
+    import numpy as np
+    import torch
+    n = len(stack.L)
+    for _ in range(args.warmup):
+        for i in range(n):
+            stack.route(i, stream)
+            stack.forward(i, "dynamic", stream)
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        for i in range(n):
+            stack.route(i, stream)
+            ev[s][i][0].record(stream)
+            stack.forward(i, "dynamic", stream)
+            ev[s][i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stack.check(B, stream)
+    fwd_us = [[ev[s][i][0].elapsed_time(ev[s][i][1]) * 1e3 for s in range(args.steps)] for i in range(n)]
+    log(f"{stack.shape.name}: timed steps done ({wall * 1e3 / args.steps:.2f} ms per step)")
+    plans = [B.moe_get_plan(d["layer"].h, stream) for d in stack.L]
+    stats = [layer_stats(stack, i) for i in range(n)]
+    flops = [layer_flops(stack.shape, st) for st in stats]
+    # routing alone, per layer
+    route_us = []
+    for i in range(n):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            stack.route(i, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        route_us.append(a.elapsed_time(b) * 1e3 / args.steps)
+    # baselines next to the dynamic mode, timed the same way (back-to-back
+    # stacks on the same routing) in interleaved rounds
+    modes = ["dynamic"] + [m for m in args.modes.split(",") if m]
+    runs = {m: [[] for _ in range(n)] for m in modes}
+    for _ in range(args.rounds):
+        for m in modes:
+            t = time_stack(stack, m, args.reps, stream)
+            for i in range(n):
+                runs[m][i] += t[i]
+    stack.check(B, stream)
+    log(f"{stack.shape.name}: baselines done ({args.rounds} interleaved rounds)")
+    fl = time_flushed(stack, args.reps, stream, flush) if flush is not None else None
+    layers = []
+    for i in range(n):
+        p = plans[i]
+        rec = {"layer": stack.ids[i], "plan": {"c": p.c, "K": p.K, "n_steal": p.n_steal, "final_all": p.final_all,
+                                                "t_pred_us": p.t_pred_s * 1e6},
+               "local_pairs": int(stats[i][0]), "gflop": flops[i] / 1e9,
+               "layer_us": float(np.median(fwd_us[i])),
+               "layer_us_p10_p90": [float(np.percentile(fwd_us[i], 10)), float(np.percentile(fwd_us[i], 90))],
+               "layer_us_flushed": float(np.median(fl[i])) if fl else None,
+               "route_us": route_us[i],
+               "tflops": flops[i] / (float(np.mean(fwd_us[i])) * 1e-6) / 1e12}
+        dyn = float(np.median(runs["dynamic"][i]))
+        rec["baselines"] = {"dynamic_same_timing_us": dyn}
+        for m in modes[1:]:
+            med = float(np.median(runs[m][i]))
+            rec["baselines"][m] = {"layer_us": med, "dynamic_speedup": med / dyn}
+        if trace:
+            rec["phases"] = traced_phases(B, stack, i, stream, stats[i], flops[i])
+        layers.append(rec)
+    tot = {m: float(sum(np.median(runs[m][i]) for i in range(n))) for m in modes}
+    summary = {
+        "steps": args.steps, "ms_per_step": wall * 1e3 / args.steps,
+        "stack_layer_us_total": float(sum(np.median(f) for f in fwd_us)),
+        "stack_route_us_total": float(sum(route_us)),
+        "stack_flops": float(sum(flops)),
+        "mean_launch_us": float(np.mean([np.mean(f) for f in fwd_us])),
+        "baseline_totals_us": tot,
+        "dynamic_speedup_vs": {m: tot[m] / tot["dynamic"] for m in modes[1:]},
+    }
+    return summary, layers
 
 
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the expert-parallel layer; --gpus {args.gpus} is not "
-              "supported (this build runs on exactly one GPU)", file=sys.stderr)
+              "supported: this benchmark runs on exactly one GPU", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -188,126 +421,79 @@ def main():
     from paper_2609_21483_amd import workloads as W
 
     shape = W.WORKLOADS[args.workload]
-    layer_id = args.layer
+    ids = [int(v) for v in args.layers.split(",") if v] or list(range(shape.n_layers))
     torch.cuda.init()
     N = torch.cuda.get_device_properties(0).multi_processor_count
-    print(f"[bench] workload {shape.name} layer {layer_id}: generating inputs", file=sys.stderr, flush=True)
-    c = {"x": W.tokens(shape), "wg": W.gate(shape, layer_id), "bias": W.zipf_log_prior(shape, layer_id)}
-    c["w1"], c["w3"], c["w2"] = W.experts(shape, layer_id)
-    c["ws1"], c["ws3"], c["ws2"] = W.shared_experts(shape, layer_id)
-    from paper_2609_21483_amd.calibrate import load_calib
-    calib = load_calib(shape.name, N)
-    layer = B.MoeLayer(shape, c["w1"], c["w3"], c["w2"], c["ws1"], c["ws3"], c["ws2"], calib=calib)
     stream = torch.cuda.current_stream()
-    x = c["x"].cuda()
-    wg = c["wg"].cuda()
-    bias = None if c["bias"] is None else c["bias"].cuda()
-    idx = torch.empty((shape.T, shape.top_k), dtype=torch.int32, device="cuda")
-    w = torch.empty((shape.T, shape.top_k), dtype=torch.float32, device="cuda")
-    y = torch.empty((shape.T, shape.hidden), dtype=torch.bfloat16, device="cuda")
-    torch.cuda.synchronize()
-    print("[bench] inputs resident; warmup", file=sys.stderr, flush=True)
+    flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device="cuda") if args.flush_mib else None
+    want_cpu = not args.no_cpu_baseline
+    stack = Stack(B, W, shape, ids, N, keep_host=want_cpu)
+    log(f"{shape.name}: inputs resident ({len(ids)} layers); warmup")
+    summary, layers = measure_stack(B, stack, args, stream, flush, trace=not args.no_trace)
 
-    for _ in range(args.warmup):
-        layer.route(x, wg, bias, idx, w, stream=stream)
-        layer.forward(x, idx, w, y, "dynamic", stream=stream)
-    torch.cuda.synchronize()
-    # timed region: whole steps, with events around each megakernel launch
-    fwd_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for a, b in fwd_ev:
-        layer.route(x, wg, bias, idx, w, stream=stream)
-        a.record(stream)
-        layer.forward(x, idx, w, y, "dynamic", stream=stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    st = B.moe_sync_status(layer.h, stream)
-    if st != B.MOE_OK:
-        raise RuntimeError(B.moe_last_error())
-    print("[bench] timed steps done", file=sys.stderr, flush=True)
-    layer_us = [a.elapsed_time(b) * 1e3 for a, b in fwd_ev]
-    ms_per_step = wall * 1e3 / args.steps
-    plan = B.moe_get_plan(layer.h, stream)
-    stats = layer.ws_view("stats", torch.int32, 16).cpu().numpy()
-    X = int(stats[0])
-    S, Tr, H, F = shape.n_shared_experts, shape.tokens_per_rank, shape.hidden, shape.ffn
-    flops = (X + S * Tr) * 6.0 * H * F
-    lat = float(np.median(layer_us))
-    achieved = flops / (float(np.mean(layer_us)) * 1e-6) / 1e12
-
-    # route alone (events), for the report
-    r_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-    r_ev[0].record(stream)
-    for _ in range(args.steps):
-        layer.route(x, wg, bias, idx, w, stream=stream)
-    r_ev[1].record(stream)
-    torch.cuda.synchronize()
-    route_us = r_ev[0].elapsed_time(r_ev[1]) * 1e3 / args.steps
-
-    # the baselines next to the dynamic forward, timed the same way (forward
-    # launches back to back on the same routing) in interleaved rounds, so
-    # that clock drift spreads over all modes alike
-    baselines = {}
-    modes = [m for m in args.modes.split(",") if m]
-    if modes:
-        runs = {m: [] for m in ["dynamic"] + modes}
-        for _ in range(args.rounds):
-            for m in runs:
-                runs[m] += time_forward(B, layer, x, idx, w, y, m, args.steps, 2, stream)
-        dyn = float(np.median(runs["dynamic"]))
-        baselines["dynamic_same_timing"] = {"layer_us_median": dyn}
-        for m in modes:
-            med = float(np.median(runs[m]))
-            baselines[m] = {"layer_us_median": med, "tokens_per_s": shape.T / (med * 1e-6),
-                            "dynamic_speedup": med / dyn}
-        print(f"[bench] baselines done ({args.rounds} interleaved rounds)", file=sys.stderr, flush=True)
-    phases = traced_phases(B, layer, x, idx, w, y, stream, shape, stats, flops)
-    if args.copy_probe_mib:
-        n = args.copy_probe_mib << 20
-        src = torch.empty(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-
+    n = len(ids)
+    flops_per_launch = summary["stack_flops"] / n
+    achieved = flops_per_launch / (summary["mean_launch_us"] * 1e-6) / 1e12
     out = {
         "metric": METRIC,
-        "value": shape.T / (ms_per_step * 1e-3),
+        "value": shape.T / (summary["ms_per_step"] * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": summary["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights, gate-logit routing)",
-        "config": {"workload": f"{shape.name}: EP=4 rank share, E={shape.n_experts} k={shape.top_k} H={H} F={F}, "
-                               f"{shape.n_local_experts} local experts, {shape.n_src_ranks} ranks x {Tr} tokens",
-                   "tokens": shape.T, "local_pairs": X, "layer": layer_id},
-        "layer_us": lat,
-        "layer_us_p10_p90": [float(np.percentile(layer_us, 10)), float(np.percentile(layer_us, 90))],
-        "layer_tokens_per_s": shape.T / (lat * 1e-6),
-        "route_us": route_us,
-        "plan": {"c": plan.c, "K": plan.K, "n_steal": plan.n_steal, "final_all": plan.final_all,
-                 "t_pred_us": plan.t_pred_s * 1e6, "N": N, "calibrated": calib is not None},
-        "baselines": baselines,
+        "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights, gate-logit routing with a seeded per-layer "
+                "Zipf log-prior)",
+        "config": {"workload": f"{shape.name}: {n}-layer stack of EP=4 rank shares, E={shape.n_experts} "
+                               f"k={shape.top_k} H={shape.hidden} F={shape.ffn}, {shape.n_local_experts} local "
+                               f"experts, {shape.n_src_ranks} ranks x {shape.tokens_per_rank} tokens; a step is "
+                               f"routing + MoE layer for every layer",
+                   "tokens": shape.T, "layers": ids},
+        "stack": {**summary, "stack_tokens_per_s_layers_only": shape.T / (summary["stack_layer_us_total"] * 1e-6)},
+        "layers": layers,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(shape.name),
-                     "kernel": "moe_megakernel", "flop_per_launch": flops,
-                     "flop_per_unit": "6*H*F per routed (token, local expert) row and per shared-expert row"},
-        "phases": phases,
+                     "kernel": "moe_megakernel", "flop_per_launch": flops_per_launch,
+                     "flop_per_unit": "6*H*F per routed (token, local expert) row and per shared-expert row; "
+                                      "per launch = the stack's flop / its launches"},
         "context": "paper: 2.89x geomean MoE-layer speedup on 4xH100 SXM, EP=4, BF16 - different hardware and "
                    "baselines, not a target",
     }
-    if not args.no_cpu_baseline:
-        print("[bench] oracle CPU baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(shape, c, args.cpu_rows)
-    layer.close()
+    if want_cpu:
+        log("oracle CPU baseline")
+        cores = max(1, min(16, host_info()["affinity_cpus"]))
+        base, samples, ref = cpu_baseline(stack, W, args.cpu_rows, cores)
+        out["cpu_baseline"] = base
+        out["y_check"] = y_check(stack, samples, ref)
+        log(f"y check: {out['y_check']}")
+    stack.close()
+    del stack
+
+    per = {}
+    for name in [w for w in args.extra.split(",") if w and w != shape.name]:
+        sh = W.WORKLOADS[name]
+        st = Stack(B, W, sh, [0], N, keep_host=False)
+        sargs = argparse.Namespace(**{**vars(args), "steps": max(5, args.steps)})
+        s, l = measure_stack(B, st, sargs, stream, flush, trace=False)
+        per[name] = {"tokens": sh.T, "step_tokens_per_s": sh.T / (s["ms_per_step"] * 1e-3), **l[0]}
+        st.close()
+        del st
+    out["per_config"] = per
+    if args.copy_probe_mib:
+        nb = args.copy_probe_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    del flush
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 
 

@@ -142,7 +142,18 @@ typedef struct {
   size_t inv;         /* int32 [T*min(k,E_l)]: g*k+j of each slot */
   size_t first_slot;  /* int32 [T] */
   size_t off;         /* int32 [E_l+1] */
-  size_t sub_off;     /* int32 [4][E_l][9]: chunk offsets for K = 1,2,4,8 */
+  size_t sub_off;     /* int32 [4][E_l][9]: chunk offsets for K = 1,2,4,8:
+                         entry q of (K option, expert) is the first slot of
+                         chunk q, entry K the expert's end */
+  size_t row_off;     /* int32 [4][E_l+S][9]: the row map of A, Hbuf and O
+                         for K = 1,2,4,8: entry q < K of (K option, segment)
+                         is the first row of chunk q of that segment (local
+                         experts, then shared experts).  The (segment,
+                         chunk) pairs follow each other in segment-major
+                         order, each rounded up to a multiple of 32 rows, so
+                         every one starts on a 32-row group; within one, rows
+                         follow the slots (local experts) or the tokens
+                         (shared experts).  Entries q >= K are 0. */
   size_t cnt_rank;    /* int32 [E_l][R] */
   size_t uniq;        /* int32 [R] */
   size_t stats;       /* int32 [16]: X, X_local, X_in, U_local, U_in, bad ids (0-5);
@@ -151,12 +162,14 @@ typedef struct {
                          builder for the cost model (section 3.2, Eq 14) */
   size_t plan;        /* moe_plan of the last megakernel launch */
   size_t err;         /* int32 device error word */
-  size_t A;           /* bf16 [X_max + pad][H]: dispatched rows, group-tiled:
-                         row r, column j at element
-                         ((r/32)*(H/32) + j/32)*1024 + (r%32)*32 + j%32 */
-  size_t Hbuf;        /* bf16 [X_max + S*Tr + pad][F]: SiLU(gate)*up,
-                         group-tiled like A (F in place of H) */
-  size_t O;           /* bf16 [X_max + S*Tr + pad][H]: expert outputs */
+  size_t A;           /* bf16 [X_max + 256 E_l + 256][H] (X_max = T*min(k, E_l)):
+                         dispatched rows at the rows of the row map of the
+                         launch's chunk count, group-tiled: row r, column j
+                         at element ((r/32)*(H/32) + j/32)*1024 + (r%32)*32 + j%32 */
+  size_t Hbuf;        /* bf16 [rows of A + S*(Tr + 256)][F]: SiLU(gate)*up,
+                         the same row map, group-tiled like A (F in place of H) */
+  size_t O;           /* bf16 [rows of Hbuf][H]: expert outputs, the same row
+                         map, row-major */
 } moe_ws_layout;
 
 /* Creates a handle.  cfg (host) is copied; calib (host) may be NULL for the

@@ -67,7 +67,7 @@ class moe_plan(C.Structure):
 
 class moe_ws_layout(C.Structure):
     _fields_ = [(n, C.c_size_t) for n in (
-        "total", "slot", "inv", "first_slot", "off", "sub_off", "cnt_rank", "uniq", "stats", "plan",
+        "total", "slot", "inv", "first_slot", "off", "sub_off", "row_off", "cnt_rank", "uniq", "stats", "plan",
         "err", "A", "Hbuf", "O")]
 
 

@@ -40,6 +40,7 @@ struct moe_handle {
   moe_config cfg;
   int N = 0;
   int T = 0, xmax = 0, mt_max = 0, ctl_words = 0, nblk = 0, nseg = 0, nt0 = 0, nt1 = 0, nsplit = 1;
+  size_t arows = 0, orows = 0;  // row capacities of A and of Hbuf / O (the padded row map)
   int qx = 0, qxs = 0;
   moe_calib calib{};
   DevCalib dcal{};
@@ -59,6 +60,19 @@ struct moe_handle {
 };
 
 namespace {
+
+// Row capacities of the padded row map (common.h): every (segment, chunk)
+// is rounded up to a 32-row group, at most MAX_K chunks per segment; plus
+// one row tile of slack.  A holds the routed rows, Hbuf and O also the
+// shared experts' rows (rank 0's tokens).
+size_t a_rows(const moe_config& c) {
+  const long long T = (long long)c.n_src_ranks * c.tokens_per_rank;
+  const long long xmax = T * std::min(c.top_k, c.n_local_experts);
+  return (size_t)(xmax + (long long)c.n_local_experts * MAX_K * ROW_ALIGN + BM);
+}
+size_t out_rows(const moe_config& c) {
+  return a_rows(c) + (size_t)c.n_shared_experts * ((size_t)c.tokens_per_rank + MAX_K * ROW_ALIGN);
+}
 
 moe_status validate_cfg(const moe_config* c) {
   if (!c) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
@@ -85,13 +99,12 @@ moe_status validate_cfg(const moe_config* c) {
     return fail(MOE_ERR_INVALID_ARG, "gemm1_split must be 0, 1, 2, 4 or 8");
   if (c->gemm1_split > 1 && c->ffn % (32 * c->gemm1_split))
     return fail(MOE_ERR_INVALID_ARG, "ffn must be a multiple of 32 * gemm1_split");
-  long long xmax = T * (long long)std::min(c->top_k, c->n_local_experts);
-  if (xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM > (1LL << 31) / 2)
-    return fail(MOE_ERR_UNSUPPORTED, "too many routed rows");
+  const long long orows = (long long)out_rows(*c);
+  if (orows > (1LL << 31) / 2) return fail(MOE_ERR_UNSUPPORTED, "too many routed rows");
   // dispatch addresses the row buffer A, the split reduction the output rows
   // O, with 32-bit byte offsets
-  if ((xmax + (long long)c->n_shared_experts * c->tokens_per_rank + BM) * (long long)c->hidden * 2 >= (1LL << 32))
-    return fail(MOE_ERR_UNSUPPORTED, "routed rows (T * min(k, E_l) + S * T_r) x H bf16 exceed 4 GiB");
+  if (orows * (long long)c->hidden * 2 >= (1LL << 32))
+    return fail(MOE_ERR_UNSUPPORTED, "routed rows (T * min(k, E_l) + S * T_r, padded) x H bf16 exceed 4 GiB");
   return MOE_OK;
 }
 
@@ -177,6 +190,7 @@ void compute_layout(moe_handle* h) {
   L.first_slot = take(sizeof(int32_t) * (size_t)T);
   L.off = take(sizeof(int32_t) * (size_t)(El + 1));
   L.sub_off = take(sizeof(int32_t) * (size_t)KOPT * El * SUBW);
+  L.row_off = take(sizeof(int32_t) * (size_t)KOPT * (El + S) * SUBW);
   L.cnt_rank = take(sizeof(int32_t) * (size_t)El * R);
   L.uniq = take(sizeof(int32_t) * (size_t)R);
   L.stats = take(sizeof(int32_t) * ST_WORDS);
@@ -197,12 +211,13 @@ void compute_layout(moe_handle* h) {
   h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
   h->off_ctl[0] = take(sizeof(int32_t) * (size_t)h->ctl_words);
   h->off_ctl[1] = take(sizeof(int32_t) * (size_t)h->ctl_words);
-  const size_t orows = (size_t)h->xmax + (size_t)S * c.tokens_per_rank + BM;
-  L.A = take(sizeof(uint16_t) * ((size_t)h->xmax + BM) * c.hidden);
-  L.Hbuf = take(sizeof(uint16_t) * orows * c.ffn);
-  L.O = take(sizeof(uint16_t) * orows * c.hidden);
+  h->arows = a_rows(c);
+  h->orows = out_rows(c);
+  L.A = take(sizeof(uint16_t) * h->arows * c.hidden);
+  L.Hbuf = take(sizeof(uint16_t) * h->orows * c.ffn);
+  L.O = take(sizeof(uint16_t) * h->orows * c.hidden);
   // split-K partials of GEMM1: fp32 [split][row][H], rows as in O
-  h->off_part = h->nsplit > 1 ? take(sizeof(float) * (size_t)h->nsplit * orows * c.hidden) : 0;
+  h->off_part = h->nsplit > 1 ? take(sizeof(float) * (size_t)h->nsplit * h->orows * c.hidden) : 0;
   L.total = o;
 }
 
@@ -223,6 +238,7 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
   a.first_slot = at<int32_t>(h, h->lay.first_slot);
   a.off = at<int32_t>(h, h->lay.off);
   a.sub_off = at<int32_t>(h, h->lay.sub_off);
+  a.row_off = at<int32_t>(h, h->lay.row_off);
   a.cnt_rank = at<int32_t>(h, h->lay.cnt_rank);
   a.uniq = at<int32_t>(h, h->lay.uniq);
   a.stats = at<int32_t>(h, h->lay.stats);
@@ -286,12 +302,13 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.y = y;
   a.slot = at<int32_t>(h, h->lay.slot);
   a.sub_off = at<int32_t>(h, h->lay.sub_off);
+  a.row_off = at<int32_t>(h, h->lay.row_off);
   a.stats = at<int32_t>(h, h->lay.stats);
   a.A = at<uint16_t>(h, h->lay.A);
   a.Hb = at<uint16_t>(h, h->lay.Hbuf);
   a.O = at<uint16_t>(h, h->lay.O);
   a.part = h->nsplit > 1 ? at<float>(h, h->off_part) : nullptr;
-  a.prow = (size_t)h->xmax + (size_t)h->cfg.n_shared_experts * h->cfg.tokens_per_rank + BM;
+  a.prow = h->orows;
   a.ctl = at<int32_t>(h, h->off_ctl[cur]);
   a.ctl_next = at<int32_t>(h, h->off_ctl[cur ^ 1]);
   a.err = at<int32_t>(h, h->lay.err);

@@ -44,6 +44,17 @@ constexpr int MAX_E = 512;
 constexpr int KOPT = 4;         // chunk options with stored offsets: K = 1, 2, 4, 8
 constexpr int SUBW = 9;         // stored offsets per (K option, expert): K+1 <= 9
 
+// Rows of A, Hbuf and O are grouped 32 to a group (the group-tiled operand
+// layout of gemm.h: one 128-byte line holds two rows of a group).  Every
+// (segment, chunk) starts on a group boundary, so no line holds rows of two
+// segments or chunks: workers on different XCDs (each with its own L2) that
+// wait for different readiness counters never share a line, and no L2 can
+// cache a line of rows that are not written yet.  Row r of segment (seg, q)
+// at chunk option K lies at row_off[kopt(K)][seg][q] + r; the padding rows
+// at the end of a segment are never written nor read.
+constexpr int ROW_ALIGN = 32;
+__host__ __device__ inline int align_rows(int n) { return (n + ROW_ALIGN - 1) / ROW_ALIGN * ROW_ALIGN; }
+
 __host__ __device__ inline int kopt_index(int K) { return K == 1 ? 0 : K == 2 ? 1 : K == 4 ? 2 : 3; }
 __host__ __device__ inline int kopt_value(int i) { return 1 << i; }
 

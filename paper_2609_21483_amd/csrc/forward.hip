@@ -4,11 +4,13 @@
 //
 // Data layout in HBM
 //   x    bf16 [T][H]        staging regions: rank r's rows at r*Tr
-//   A    bf16 [X+pad][H]    dispatched rows, expert-contiguous (slot order),
-//                           group-tiled (gemm::AOp)
-//   Hbuf bf16 [X+S*Tr+pad][F]  SiLU(gate)*up per row (shared experts after X),
-//                           group-tiled
-//   O    bf16 [X+S*Tr+pad][H]  expert outputs per row
+//   A    bf16 [rows][H]     dispatched rows, expert-contiguous, then chunk-
+//                           contiguous within an expert (slot order within a
+//                           chunk); every (expert, chunk) starts on a 32-row
+//                           group (row_off); group-tiled (gemm::AOp)
+//   Hbuf bf16 [rows][F]     SiLU(gate)*up per row (shared experts after the
+//                           routed rows), the same row map, group-tiled
+//   O    bf16 [rows][H]     expert outputs per row, the same row map
 //   part fp32 [split][X+S*Tr+pad][H]  split-K partials of GEMM1 (when split)
 //   y    bf16 [T][H]        output staging regions
 //   w13  bf16 [E_l+S][2F][H] gate/up weights, k-contiguous, 32-col interleave,
@@ -39,8 +41,9 @@ struct Sched {
   int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
   // per (chunk q, segment) at index q*nseg + seg
   int rows[MAX_K * MAX_SEG];
-  int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts)
-  int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A slot or token)
+  int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts), a 32-row group boundary
+  int sbase[MAX_K * MAX_SEG];  // first slot (local expert) or token (shared expert) of the segment
+  int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A row or token)
   int mb[MAX_K * MAX_SEG];     // first row-tile id (counter index)
   int lvl[MAX_K][NLVL + 1];    // row tiles of chunk q at readiness level <= L
   int gstart[MAX_K * 2 * MAX_SEG + 1];
@@ -131,8 +134,10 @@ __device__ __forceinline__ int stage_qph(int s, int K) {
   return (s & 1) ? (j << 1) : (((j - 1) << 1) | 1);
 }
 
-// sub: the chunk sub-offset tables (a.sub_off, or a copy of them in LDS)
-__device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, Sched& S, Scratch& W, int K) {
+// sub, rof: the chunk sub-offset and row-map tables (a.sub_off and
+// a.row_off, or copies of them in LDS)
+__device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, const int* rof, Sched& S, Scratch& W,
+                                            int K) {
   const int tid = threadIdx.x;
   const int ki = kopt_index(K);
   const int nseg = a.El + a.S;
@@ -149,21 +154,22 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, Sc
   __syncthreads();
   for (int v = tid; v < K * nseg; v += FNTH) {
     int q = v / nseg, seg = v % nseg;
-    int rows, row0, arow0;
+    int rows, sbase, arow0;
+    const int row0 = rof[((size_t)ki * nseg + seg) * SUBW + q];
     if (seg < a.El) {
       const int* so = sub + ((size_t)ki * a.El + seg) * SUBW;
-      row0 = so[q];
+      sbase = so[q];
       rows = so[q + 1] - so[q];
       arow0 = row0;
     } else {
-      int s = seg - a.El;
       int t0 = S.bnd[q], t1 = min(S.bnd[q + 1], a.Tr);
       rows = max(0, t1 - t0);
+      sbase = t0;
       arow0 = t0;
-      row0 = a.xmax + s * a.Tr + t0;
     }
     S.rows[v] = rows;
     S.row0[v] = row0;
+    S.sbase[v] = sbase;
     S.arow0[v] = arow0;
     S.mb[v] = ceil_div(rows, BM);
   }
@@ -248,11 +254,39 @@ __device__ __forceinline__ void trace_rec(const FwdArgs& a, Scratch& W, int kind
 // plain stores.  Either way the wavefront drains its stores before its next
 // unit, which measures faster on this GPU than letting them queue.
 
-// this lane's slot entry of unit u (lane = token * k + j), or -1
-__device__ __forceinline__ int unit_slot(const FwdArgs& a, int u) {
-  const int g = u * a.dt;
+// Row in A / Hbuf / O of the local pair (g, j) with slot s >= 0 of local
+// expert le: its (expert, chunk) segment's first row plus its place in the
+// segment (common.h).  With the launch's schedule S the segment comes from
+// LDS; without one (the separate kernels) from the tables, for serial_K.
+__device__ __forceinline__ int pair_row(const FwdArgs& a, const Sched* S, int g, int le, int s) {
+  if (S) {
+    const int v = (int)(((long long)g * S->K) / a.T) * S->nseg + le;
+    return S->row0[v] + (s - S->sbase[v]);
+  }
+  const int K = a.serial_K, ki = kopt_index(K), q = (int)(((long long)g * K) / a.T);
+  return a.row_off[(ki * (a.El + a.S) + le) * SUBW + q] + (s - a.sub_off[(ki * a.El + le) * SUBW + q]);
+}
+
+// Row in Hbuf / O of token g (g < Tr) of shared expert sh.
+__device__ __forceinline__ int shared_row(const FwdArgs& a, const Sched* S, int g, int sh) {
+  if (S) {
+    const int q = (int)(((long long)g * S->K) / a.T), v = q * S->nseg + a.El + sh;
+    return S->row0[v] + (g - S->sbase[v]);
+  }
+  const int K = a.serial_K, ki = kopt_index(K), q = (int)(((long long)g * K) / a.T);
+  const int t0 = (int)(((long long)q * a.T + K - 1) / K);
+  return a.row_off[(ki * (a.El + a.S) + a.El + sh) * SUBW + q] + (g - t0);
+}
+
+// this lane's A row of unit u (lane = token * k + j), or -1 when the pair is
+// not local
+__device__ __forceinline__ int unit_row(const FwdArgs& a, const Sched* S, int u) {
+  const int g0 = u * a.dt;
   const int lane = lane_id();
-  return (g < a.T && lane < min(a.dt, a.T - g) * a.k) ? a.slot[(size_t)g * a.k + lane] : -1;
+  if (g0 >= a.T || lane >= min(a.dt, a.T - g0) * a.k) return -1;
+  const int g = g0 + lane / a.k;
+  const int s = a.slot[(size_t)g0 * a.k + lane];
+  return s < 0 ? -1 : pair_row(a, S, g, a.topk_idx[(size_t)g0 * a.k + lane] - a.e0, s);
 }
 
 // The lane id and the launch constants of a movement unit are defined by
@@ -274,13 +308,12 @@ __device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int 
   const int H = opaque(a.H);
   const int VPR = H >> 3;
   const int T = opaque(a.T);
-  const int xmax = opaque(a.xmax);
   const int dt = opaque(a.dt);
   const int g0 = u * dt;
   const int nt = min(dt, T - g0);
   sl[lane] = cur;
   // tokens with at least one local slot, compacted in token order
-  const uint64_t vm = __builtin_amdgcn_ballot_w64((unsigned)cur < (unsigned)xmax);
+  const uint64_t vm = __builtin_amdgcn_ballot_w64(cur >= 0);
   const bool tact = lane < nt && ((vm >> min(lane * k, 56)) & ((1ull << k) - 1)) != 0;
   const uint64_t am = __builtin_amdgcn_ballot_w64(tact);
   const int na = __builtin_popcountll(am);
@@ -313,7 +346,7 @@ __device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int 
       const int tok = act[t];
       for (int j = 0; j < k; ++j) {
         const int s = sl[tok * k + j];
-        if ((unsigned)s >= (unsigned)xmax) continue;
+        if (s < 0) continue;
         // A is group-tiled (gemm::AOp): 16-byte chunk c of row s lies in
         // k-step block c / 4 of group s / 32, at row s % 32 of the block
         const uint32_t off = ((uint32_t)(s >> 5) * (uint32_t)H * 32u + (uint32_t)(c >> 2) * 1024u +
@@ -338,10 +371,9 @@ __device__ __forceinline__ void dispatch_count(const FwdArgs& a, const Sched* S,
   const int lane = lane_here();
   const int k = opaque(a.k);
   const int T = opaque(a.T);
-  const int xmax = opaque(a.xmax);
   const int g0 = u * opaque(a.dt);
   int id = -1;
-  if ((unsigned)cur < (unsigned)xmax) {
+  if (cur >= 0) {
     const int g = g0 + lane / k;
     const int le = a.topk_idx[(size_t)g * k + (lane % k)] - a.e0;
     if ((unsigned)le < (unsigned)a.El) {
@@ -377,10 +409,10 @@ __device__ __forceinline__ void dispatch_one(const FwdArgs& a, const Sched* S, S
 // fetched while the current one is copied
 __device__ __forceinline__ void dispatch_static(const FwdArgs& a, Scratch& W, int u, int ustride) {
   const int nu = ceil_div(a.T, a.dt);
-  int next = unit_slot(a, u);
+  int next = unit_row(a, nullptr, u);
   for (; u < nu; u += ustride) {
     const int cur = next;
-    next = unit_slot(a, u + ustride);
+    next = unit_row(a, nullptr, u + ustride);
     dispatch_one<false>(a, nullptr, W, u, cur);
   }
 }
@@ -426,7 +458,7 @@ __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& 
   for (;;) {
     const int u = claim_disp(a, S, shard);
     if (u < 0) break;
-    dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
+    dispatch_one<true>(a, &S, W, u, unit_row(a, &S, u));
   }
 }
 
@@ -503,22 +535,23 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
   float w = 1.0f;
   if (lane < nt * ks) {
     const int t = lane / ks, j = lane - t * ks, g = g0 + t;
+    int seg = -1;
     if (j < k) {
       s = a.slot[(size_t)g * k + j];
       w = a.topk_w[(size_t)g * k + j];
-      if ((unsigned)s >= (unsigned)a.xmax) s = -1;
+      if (s >= 0) {
+        seg = a.topk_idx[(size_t)g * k + j] - a.e0;
+        s = pair_row(a, S, g, seg, s);
+      }
     } else if (g < a.Tr) {
-      s = a.xmax + (j - k) * a.Tr + g;
+      seg = a.El + (j - k);
+      s = shared_row(a, S, g, j - k);
     }
     if (S && s >= 0) {
-      const int q = (int)(((long long)g * S->K) / a.T);
-      if (j < k) {
-        const int seg = a.topk_idx[(size_t)g * k + j] - a.e0;
-        id = S->mb[q * S->nseg + seg] + (s - S->row0[q * S->nseg + seg]) / BM;
-      } else {
-        const int seg = a.El + (j - k);
-        id = S->mb[q * S->nseg + seg] + (g - S->bnd[q]) / BM;
-      }
+      // row tile of the source row: its segment's first row tile plus its
+      // place in the segment
+      const int v = (int)(((long long)g * S->K) / a.T) * S->nseg + seg;
+      id = S->mb[v] + (s - S->row0[v]) / BM;
       if ((unsigned)id >= (unsigned)a.mt_max) id = -1;
     }
   }
@@ -885,7 +918,7 @@ __device__ __forceinline__ bool wait_rows(const FwdArgs& a, const Sched& S, Scra
     if (st) return st > 0;
     int shard = first_shard(W);
     const int u = claim_disp(a, S, shard);
-    if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_slot(a, u));
+    if (u >= 0) dispatch_one<true>(a, &S, W, u, unit_row(a, &S, u));
     else if (lane_id() == 0) W.dexh = 1;
   }
 }
@@ -989,14 +1022,17 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
     W.dexh = 0;
   }
 
-  // the chunk sub-offset tables, staged in the GEMM ring (idle until the
-  // first tile) so that the schedule reads them from LDS
-  static_assert(KOPT * MAX_EL * SUBW * (int)sizeof(int) <= gemm::RING_BYTES, "sub-offset tables fit the ring");
+  // the chunk sub-offset and row-map tables, staged in the GEMM ring (idle
+  // until the first tile) so that the schedule reads them from LDS
+  static_assert(KOPT * (2 * MAX_EL + MAX_S) * SUBW * (int)sizeof(int) <= gemm::RING_BYTES,
+                "sub-offset and row-map tables fit the ring");
   int* sub = reinterpret_cast<int*>(ring);
+  int* rof = sub + KOPT * a.El * SUBW;
   for (int i = tid; i < KOPT * a.El * SUBW; i += FNTH) sub[i] = a.sub_off[i];
+  for (int i = tid; i < KOPT * (a.El + a.S) * SUBW; i += FNTH) rof[i] = a.row_off[i];
   if (tid == 0) W.bc[0] = tk;
   prologue_plan(a, S, W);
-  build_sched(a, sub, S, W, S.K);
+  build_sched(a, sub, rof, S, W, S.K);
 
   if (tid < NWF) W.tcnt[tid] = 0;
   if (tid == 0) {
@@ -1012,7 +1048,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   // this wavefront's statically owned dispatch unit, if any
   {
     const int u0 = ticket * NWF + wave_id();
-    if (u0 < S.disp0) dispatch_one<true>(a, &S, W, u0, unit_slot(a, u0));
+    if (u0 < S.disp0) dispatch_one<true>(a, &S, W, u0, unit_row(a, &S, u0));
   }
 
   bool ok = true;
@@ -1062,7 +1098,7 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
-  build_sched(a, a.sub_off, S, W, a.serial_K);
+  build_sched(a, a.sub_off, a.row_off, S, W, a.serial_K);
   const int home = xcd_id() & (NXCD - 1);
   int stage = 0;
   uint32_t exhausted = 0;

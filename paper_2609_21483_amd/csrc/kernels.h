@@ -33,6 +33,7 @@ struct TableArgs {
   int32_t* first_slot;
   int32_t* off;
   int32_t* sub_off;
+  int32_t* row_off;    // [KOPT][E_l + S][SUBW] first A / Hbuf / O row of each (segment, chunk)
   int32_t* cnt_rank;
   int32_t* uniq;
   int32_t* stats;
@@ -85,7 +86,7 @@ struct FwdArgs {
   int dt, ct;     // tokens per dispatch unit (<= DT) and per combine unit (<= CT)
   int move_steal; // compute workers copy dispatch units while their rows are not
                   // ready (dynamic mode; the static split keeps its roles fixed)
-  int xmax;       // rows reserved for routed pairs in A / Hbuf / O
+  int xmax;       // routed pairs at most (T * min(k, E_l))
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
   int qx, qxs;    // word offsets of the [2 MAX_K][NXCD] tile queue heads (megakernel, serial GEMMs)
@@ -99,13 +100,14 @@ struct FwdArgs {
   // routing tables
   const int32_t* slot;
   const int32_t* sub_off;
+  const int32_t* row_off;  // [KOPT][E_l + S][SUBW] first row of each (segment, chunk) in A / Hbuf / O
   const int32_t* stats;
   // intermediate buffers
   uint16_t* A;
   uint16_t* Hb;
   uint16_t* O;
   float* part;    // split-K partials of GEMM1, fp32 [nsplit][prow][H] (nsplit > 1)
-  size_t prow;    // rows per split in part (the capacity of O)
+  size_t prow;    // rows per split in part (the row capacity of Hbuf and O)
   long long* trace;  // timeline buffer (NULL: off), see moe_set_trace
   int trace_cap;     // records per wavefront segment
   int trace_rec0;    // int64 word offset of the first segment

@@ -645,10 +645,24 @@ __device__ inline int seg_lower_bound(const TableArgs& a, const int* samp, int s
   return lo;
 }
 
+// Rows of segment seg (local experts, then shared experts) in chunk q of
+// the K-chunk option ki; so: that option's sub_off table.  A shared expert
+// takes rank 0's tokens of the chunk (tokens [ceil(qT/K), ceil((q+1)T/K))).
+__device__ inline int seg_chunk_rows(const TableArgs& a, const int* so, int ki, int K, int seg, int q) {
+  if (seg < a.El) {
+    const int* e = so + (ki * a.El + seg) * SUBW;
+    return e[q + 1] - e[q];
+  }
+  const int t0 = (int)(((long long)q * a.T + K - 1) / K);
+  const int t1 = min((int)(((long long)(q + 1) * a.T + K - 1) / K), a.Tr);
+  return max(0, t1 - t0);
+}
+
 // One workgroup.  Lower bounds at the rank boundaries (per-(expert, rank)
 // counts) and at the chunk boundaries of every chunk option (sub_off) form
-// one item space, one search per item and thread; the tile counts of the
-// cost model are then taken from the workgroup's copy of sub_off.
+// one item space, one search per item and thread; the row map and the tile
+// counts of the cost model are then taken from the workgroup's copy of
+// sub_off.
 __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
   __shared__ int uq[64];
   __shared__ int ntk[KOPT];
@@ -689,6 +703,30 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     const int le = v / a.R, r = v % a.R;
     a.cnt_rank[v] = rb[le * (a.R + 1) + r + 1] - rb[le * (a.R + 1) + r];
   }
+  // The row map (common.h): for each chunk option, the (segment, chunk)
+  // pairs in segment-major order, each taking its rows rounded up to a
+  // 32-row group; wavefront ki scans option ki.  Entries q >= K are zero.
+  static_assert(NTH / WAVE == KOPT, "one wavefront per chunk option");
+  {
+    const int lane = tid & (WAVE - 1), ki = tid / WAVE, K = kopt_value(ki);
+    const int nseg = a.El + a.S, n = nseg * K;
+    int carry = 0;
+    for (int b = 0; b < n; b += WAVE) {
+      const int v = b + lane;
+      const int seg = v / K, q = v - seg * K;
+      const int sz = v < n ? align_rows(seg_chunk_rows(a, so_l, ki, K, seg, q)) : 0;
+      int x = sz;
+#pragma unroll
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const int y = __shfl_up(x, d, WAVE);
+        if (lane >= d) x += y;
+      }
+      if (v < n) a.row_off[(ki * nseg + seg) * SUBW + q] = carry + x - sz;
+      carry += __shfl(x, WAVE - 1, WAVE);
+    }
+    for (int v = lane; v < nseg * (SUBW - K); v += WAVE)
+      a.row_off[(ki * nseg + v / (SUBW - K)) * SUBW + K + v % (SUBW - K)] = 0;
+  }
   // GEMM tiles of the layer at each chunk option: every (chunk, segment)
   // contributes ceil(rows / BM) row tiles of GEMM0 + GEMM1 tiles; shared
   // experts take rank 0's tokens of the chunk
@@ -697,15 +735,7 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     int part = 0;
     for (int v = tid; v < K * nseg; v += NTH) {
       const int q = v / nseg, seg = v % nseg;
-      int rows;
-      if (seg < a.El) {
-        const int* so = so_l + (ki * a.El + seg) * SUBW;
-        rows = so[q + 1] - so[q];
-      } else {
-        const int t0 = (int)(((long long)q * a.T + K - 1) / K);
-        const int t1 = min((int)(((long long)(q + 1) * a.T + K - 1) / K), a.Tr);
-        rows = max(0, t1 - t0);
-      }
+      const int rows = seg_chunk_rows(a, so_l, ki, K, seg, q);
       part += (rows + BM - 1) / BM * a.tiles_per_row_tile;
     }
     if (part) atomicAdd(&ntk[ki], part);

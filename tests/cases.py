@@ -143,3 +143,54 @@ def rel_err(y_gpu: np.ndarray, y_ref: np.ndarray) -> float:
 
 def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
     return t.float().cpu().numpy().astype(np.float64)
+
+
+# ---- the cost model on the oracle's tables (plan parity) -------------------
+
+def oracle_tiles(B, h, shape, tab, K):
+    T, k = shape.T, shape.top_k
+    El, S, Tr = shape.n_local_experts, shape.n_shared_experts, shape.tokens_per_rank
+    bm, nt0, nt1 = B.moe_tile_geometry(h)
+    sub = O.chunk_offsets(tab, T, k, K)
+    rows = [list(np.diff(sub[le])) for le in range(El)]
+    for _ in range(S):
+        bnd = [(q * T + K - 1) // K for q in range(K + 1)]
+        rows.append([max(0, min(bnd[q + 1], Tr) - bnd[q]) for q in range(K)])
+    return O.tile_count(np.array(rows, np.int32).reshape(El + S, K), bm, nt0, nt1)
+
+
+def oracle_plan(B, h, shape, idx):
+    El, S, Tr = shape.n_local_experts, shape.n_shared_experts, shape.tokens_per_rank
+    tab = O.route_tables(idx, shape.n_src_ranks, Tr, 0, El)
+    cal = B.moe_get_calib(h)
+    Ks = [cal.k_chunks[j] for j in range(cal.n_k)]
+    n_tiles = [oracle_tiles(B, h, shape, tab, K) for K in Ks]
+    wc, wd, wb = O.volumes(tab, shape.hidden, shape.ffn, S * Tr, literal=bool(cal.literal_volumes))
+    n = cal.n_c
+    return O.plan([cal.c[i] for i in range(n)], [cal.bw_bytes_per_s[i] for i in range(n)],
+                  [cal.comp_flop_per_s[i] for i in range(n)], Ks, [cal.eff_chunk[j] for j in range(cal.n_k)],
+                  cal.alpha, n_workers(), wc, wd, wb, n_tiles, bw_all=cal.bw_all_bytes_per_s,
+                  steal_window=cal.steal_window, steal_ceil=cal.steal_ceil)
+
+
+def n_workers():
+    # the persistent workers: one per CU
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+def plain_reading(cal):
+    """The printed cost model as it stands: remote-only volumes (Eq 2-3), the
+    tail at BW(c) (Eq 10), Eq 11's window W_dispatch + W_combine, Eq 14's share
+    as whole tiles."""
+    cal.literal_volumes, cal.bw_all_bytes_per_s, cal.steal_window, cal.steal_ceil = 1, 0.0, 0, 0
+    return cal
+
+
+def check_plan(B, h, shape, idx):
+    """The plan of the last megakernel launch against the oracle's cost model
+    on the oracle's tables: identical integers, identical fp64 bits."""
+    p = B.moe_get_plan(h)
+    o = oracle_plan(B, h, shape, idx)
+    assert (p.c, p.K, p.n_steal, p.final_all) == (o.c, o.K, o.n_steal, 1)
+    assert p.t_pred_s == o.t_total
+    return p

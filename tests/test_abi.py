@@ -72,14 +72,18 @@ def test_workspace_layout_covers_buffers(shape):
         L = B.moe_workspace_layout(h)
         size = B.moe_workspace_size(h)
         assert size == L.total
-        T, k = shape.T, shape.top_k
-        xmax = T * min(k, shape.n_local_experts)
-        rows = xmax + shape.n_shared_experts * shape.tokens_per_rank
-        offs = sorted((getattr(L, n), n) for n in ("slot", "inv", "first_slot", "off", "sub_off", "cnt_rank",
-                                                    "uniq", "stats", "plan", "err", "A", "Hbuf", "O"))
+        T, k, El, S = shape.T, shape.top_k, shape.n_local_experts, shape.n_shared_experts
+        xmax = T * min(k, El)
+        # the row map rounds each of at most 8 chunks of every segment up to 32 rows
+        arows = xmax + El * 8 * 31
+        rows = arows + S * (shape.tokens_per_rank + 8 * 31)
+        offs = sorted((getattr(L, n), n) for n in ("slot", "inv", "first_slot", "off", "sub_off", "row_off",
+                                                    "cnt_rank", "uniq", "stats", "plan", "err", "A", "Hbuf", "O"))
         assert all(o % 256 == 0 for o, _ in offs)
         assert L.slot + 4 * T * k <= L.inv
-        assert L.A + 2 * xmax * shape.hidden <= L.Hbuf
+        assert L.sub_off + 4 * 4 * El * 9 <= L.row_off
+        assert L.row_off + 4 * 4 * (El + S) * 9 <= L.cnt_rank
+        assert L.A + 2 * arows * shape.hidden <= L.Hbuf
         assert L.Hbuf + 2 * rows * shape.ffn <= L.O
         assert L.O + 2 * rows * shape.hidden <= size
         # weight slabs of the GEMM tiles are padded to 256 rows

@@ -12,7 +12,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2609_21483_amd import workloads as W
-from tests.cases import bf16_to_f64, make_case, oracle_rows, pick_rows, rel_err
+from tests.cases import bf16_to_f64, check_plan, make_case, oracle_rows, pick_rows, plain_reading, rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -67,16 +67,50 @@ def check_case(B, c, rows=None, forced=(), check_A=False, gemm1_split=0):
             else:
                 assert torch.equal(y.view(torch.int16), first.view(torch.int16)), f"{key} differs from dynamic"
         if check_A:
-            tab = O.route_tables(idx, shape.n_src_ranks, shape.tokens_per_rank, 0, shape.n_local_experts)
-            # the dispatched rows are stored in 32-row groups, each group's 32-column
-            # k-steps one 32 x 32 block after the other (the layout of moe.h)
-            G, H = -(-tab.X // 32), shape.hidden
-            A = layer.ws_view("A", torch.int16, G * 32 * H).cpu().numpy().view(np.uint16)
-            A = A.reshape(G, H // 32, 32, 32).transpose(0, 2, 1, 3).reshape(G * 32, H)[:tab.X]
-            assert np.array_equal(A, O.dispatch(c.xu, tab, shape.top_k))
+            check_dispatched_rows(B, layer, c, idx, w)
         return err
     finally:
         layer.close()
+
+
+def check_dispatched_rows(B, layer, c, idx, w):
+    """After a forward at each chunk count K, A holds the oracle's dispatched
+    rows (slot order) at the rows of the row map of moe.h, and the row map is
+    the segment-major prefix of the (segment, chunk) row counts, each rounded
+    up to 32 rows."""
+    shape = c.shape
+    El, S, Tr, T, H = shape.n_local_experts, shape.n_shared_experts, shape.tokens_per_rank, shape.T, shape.hidden
+    tab = O.route_tables(idx, shape.n_src_ranks, Tr, 0, El)
+    ref = O.dispatch(c.xu, tab, shape.top_k)
+    x = c.x.cuda()
+    idx_d = torch.from_numpy(np.ascontiguousarray(idx, np.int32)).cuda()
+    w_d = torch.from_numpy(np.ascontiguousarray(w, np.float32)).cuda()
+    B.moe_build_tables(layer.h, idx_d)
+    y = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    nseg = El + S
+    rof = layer.ws_view("row_off", torch.int32, 4 * nseg * 9).cpu().numpy().reshape(4, nseg, 9)
+    for ki, K in enumerate((1, 2, 4, 8)):
+        sub = O.chunk_offsets(tab, T, shape.top_k, K)
+        bnd = [(q * T + K - 1) // K for q in range(K + 1)]
+        rows = [[int(sub[le][q + 1] - sub[le][q]) for q in range(K)] for le in range(El)]
+        rows += [[max(0, min(bnd[q + 1], Tr) - bnd[q]) for q in range(K)] for _ in range(S)]
+        start, at = np.zeros((nseg, K), np.int64), 0
+        for seg in range(nseg):
+            for q in range(K):
+                start[seg, q] = at
+                at += -(-rows[seg][q] // 32) * 32
+        assert np.array_equal(rof[ki, :, :K], start), K
+        assert not rof[ki, :, K:].any()
+        layer.forward(x, idx_d, w_d, y, "dynamic", forced=B.moe_plan(8, K, 3, 1, 0.0))
+        assert B.moe_sync_status(layer.h) == B.MOE_OK
+        # 32-row groups, each group's 32-column k-steps one 32 x 32 block after the other
+        G = -(-int(at) // 32)
+        A = layer.ws_view("A", torch.int16, G * 32 * H).cpu().numpy().view(np.uint16)
+        A = A.reshape(G, H // 32, 32, 32).transpose(0, 2, 1, 3).reshape(G * 32, H)
+        for le in range(El):
+            for q in range(K):
+                n, s0, r0 = rows[le][q], int(sub[le][q]), int(start[le, q])
+                assert np.array_equal(A[r0:r0 + n], ref[s0:s0 + n]), (K, le, q)
 
 
 FORCED_SMALL = [(1, 1, 0, 1), (8, 2, 3, 1), (64, 4, 0, 0), (255, 8, 1000, 1), (40, 1, 0, 0), (128, 8, 2, 0)]
@@ -132,17 +166,86 @@ def test_no_local_pairs(B):
             layer.close()
 
 
-FULL = [("mixtral_ep4", 0), ("fine_zipf", 0), ("shared_routed", 0), ("large_stack", 0), ("large_stack", 5)]
+FULL = [("mixtral_ep4", 0), ("fine_zipf", 0), ("shared_routed", 0)] + [("large_stack", l) for l in range(8)]
 
 
 @pytest.mark.parametrize("name,layer", FULL, ids=[f"{n}-L{l}" for n, l in FULL])
 def test_full_size_sampled_rows(B, name, layer):
+    """A whole layer share at full size, y checked on sampled rows (rows are
+    independent, so a sample is exact) in every mode, under forced chunked
+    plans, and under the cost model's plans on the built-in table, the
+    committed measured table and the plain reading of the printed equations;
+    each plan against the oracle's cost model on the oracle's tables."""
+    from paper_2609_21483_amd.calibrate import load_calib
     shape = W.WORKLOADS[name]
     c = make_case(shape, layer)
-    idx, _ = c.oracle_route()
+    idx, w = c.oracle_route()
     rows = pick_rows(shape, idx, per_rank=16, seed=100 + layer)
-    forced = [(8, 8, 4, 1), (120, 2, 0, 1)] if name == "fine_zipf" else []
-    check_case(B, c, rows=rows, forced=forced)
+    forced = [(8, 8, 4, 1), (120, 2, 0, 1)] if name == "fine_zipf" else [(40, 2, 4, 1), (64, 4, 2, 1)]
+    ml = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(np.ascontiguousarray(idx, np.int32)).cuda()
+        w_d = torch.from_numpy(np.ascontiguousarray(w, np.float32)).cuda()
+        B.moe_build_tables(ml.h, idx_d)
+
+        def fwd(mode, plan=None):
+            y = torch.full((shape.T, shape.hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+            ml.forward(x, idx_d, w_d, y, mode, forced=None if plan is None else B.moe_plan(*plan, 0.0))
+            assert B.moe_sync_status(ml.h) == B.MOE_OK, (mode, plan, B.moe_last_error())
+            return y
+
+        outs = {"dynamic": fwd("dynamic")}
+        check_plan(B, ml.h, shape, idx)
+        outs["static"] = fwd("static")
+        outs["serial"] = fwd("serial")
+        for p in forced:
+            outs[p] = fwd("dynamic", p)
+        measured = load_calib(name, torch.cuda.get_device_properties(0).multi_processor_count)
+        if measured is not None:
+            B.moe_set_calib(ml.h, measured)
+            outs["measured"] = fwd("dynamic")
+            check_plan(B, ml.h, shape, idx)
+            B.moe_set_calib(ml.h, plain_reading(B.moe_calib.from_buffer_copy(measured)))
+            outs["plain"] = fwd("dynamic")
+            check_plan(B, ml.h, shape, idx)
+        y_ref = oracle_rows(c, idx, w, rows)
+        first = outs["dynamic"]
+        sel = torch.from_numpy(rows).cuda()
+        for key, y in outs.items():
+            yg = bf16_to_f64(y[sel])
+            assert np.all(np.isfinite(yg)), key
+            assert rel_err(yg, y_ref) <= TOL, key
+            assert torch.equal(y.view(torch.int16), first.view(torch.int16)), f"{key} differs from dynamic"
+    finally:
+        ml.close()
+
+
+@pytest.mark.parametrize("K", [1, 2, 4])
+def test_run_stages_reproduces_forward(B, K):
+    """moe_run_stages (the stages as separate kernels on n workers, used by
+    the calibration) with every stage gives the forward's y bit for bit."""
+    shape = W.SHARED_ROUTED.with_(tokens_per_rank=512)
+    c = make_case(shape)
+    idx, w = c.oracle_route()
+    ml = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(idx).cuda()
+        w_d = torch.from_numpy(w.astype(np.float32)).cuda()
+        B.moe_build_tables(ml.h, idx_d)
+        y0 = torch.empty((shape.T, shape.hidden), dtype=torch.bfloat16, device="cuda")
+        ml.forward(x, idx_d, w_d, y0, "dynamic")
+        assert B.moe_sync_status(ml.h) == B.MOE_OK
+        rows = pick_rows(shape, idx, per_rank=24, seed=3)
+        assert rel_err(bf16_to_f64(y0[torch.from_numpy(rows).cuda()]), oracle_rows(c, idx, w, rows)) <= TOL
+        for n in (torch.cuda.get_device_properties(0).multi_processor_count, 37):
+            y = torch.full_like(y0, float("nan"))
+            B.moe_run_stages(ml.h, x, idx_d, w_d, ml.packed, y, 15, n, K)
+            assert B.moe_sync_status(ml.h) == B.MOE_OK
+            assert torch.equal(y.view(torch.int16), y0.view(torch.int16)), (K, n)
+    finally:
+        ml.close()
 
 
 def test_route_then_forward_end_to_end(B):
