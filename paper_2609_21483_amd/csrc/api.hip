@@ -36,6 +36,69 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
+namespace {
+
+// The gate's scratch: everything its kernels use besides their inputs and
+// outputs (the transposed gate matrix and its row norms, the approximate
+// logits and token norms, the candidate chains and their exact logits, each
+// token's range of chains, and the chain counter in stats word ST_CANDS).
+struct GateLayout {
+  size_t wgt, lt, xn, wn, chg, che, chl, tb, tn, stats, total;
+};
+GateLayout gate_layout(long long T, long long H, long long E) {
+  GateLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o = align_up(o + bytes, 256); return at; };
+  L.wgt = take(sizeof(uint16_t) * (size_t)(E * H));
+  L.lt = take(sizeof(float) * (size_t)(T * E));
+  L.xn = take(sizeof(float) * (size_t)T);
+  L.wn = take(sizeof(float) * (size_t)E);
+  L.chg = take(sizeof(int32_t) * (size_t)(T * E));
+  L.che = take(sizeof(int32_t) * (size_t)(T * E));
+  L.chl = take(sizeof(float) * (size_t)(T * E));
+  L.tb = take(sizeof(int32_t) * (size_t)T);
+  L.tn = take(sizeof(int32_t) * (size_t)T);
+  L.stats = take(sizeof(int32_t) * ST_WORDS);
+  L.total = o;
+  return L;
+}
+
+// Points the gate's scratch arguments into `base` laid out by L; the chain
+// counter goes to `stats` (a stats block of ST_WORDS words).
+void bind_gate(GateArgs& g, char* base, const GateLayout& L, int32_t* stats) {
+  g.wgt = reinterpret_cast<uint16_t*>(base + L.wgt);
+  g.lt = reinterpret_cast<float*>(base + L.lt);
+  g.xn = reinterpret_cast<float*>(base + L.xn);
+  g.wn = reinterpret_cast<float*>(base + L.wn);
+  g.ch_g = reinterpret_cast<int32_t*>(base + L.chg);
+  g.ch_e = reinterpret_cast<int32_t*>(base + L.che);
+  g.ch_l = reinterpret_cast<float*>(base + L.chl);
+  g.tok_base = reinterpret_cast<int32_t*>(base + L.tb);
+  g.tok_n = reinterpret_cast<int32_t*>(base + L.tn);
+  g.stats = stats;
+}
+
+// Top-k routing (gate logits, softmax, top-k, renormalisation) on a bound
+// GateArgs: the certified filter's kernels in order on `s`.
+moe_status launch_gate(GateArgs& g, hipStream_t s) {
+  // |L - L~| <= (gamma_{H-1}(2^-24) + gamma_H(2^-23)) * sum_h |x_h w_h|: the
+  // defined recursive fp32 sum and an fp32 accumulation of the MFMA products
+  // allowed twice the unit roundoff; sum |x w| <= ||x|| ||w||; 1% for the norms
+  {
+    const double H = (double)g.H, u = std::ldexp(1.0, -24), u2 = std::ldexp(1.0, -23);
+    const double g1 = (H - 1.0) * u / (1.0 - (H - 1.0) * u), g2 = H * u2 / (1.0 - H * u2);
+    g.bound = (float)(1.01 * (g1 + g2));
+  }
+  gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
+  gate_mfma_kernel<<<(g.T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
+  gate_chain_kernel<<<std::min(16384, std::max(1, (g.T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
+  gate_final_kernel<<<(g.T + (NTH / 16) - 1) / (NTH / 16), NTH, 0, s>>>(g);
+  HIP_TRY(hipGetLastError());
+  return MOE_OK;
+}
+
+}  // namespace
+
 struct moe_handle {
   moe_config cfg;
   int N = 0;
@@ -46,8 +109,7 @@ struct moe_handle {
   DevCalib dcal{};
   moe_ws_layout lay{};
   size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_blk_bad = 0, off_ctl[2] = {0, 0}, off_part = 0;
-  size_t off_gwt = 0, off_glt = 0, off_gxn = 0, off_gwn = 0;  // gate scratch
-  size_t off_chg = 0, off_che = 0, off_chl = 0, off_tb = 0, off_tn = 0;
+  size_t off_gate = 0;  // the gate's scratch (gate_layout)
   char* ws = nullptr;
   size_t ws_bytes = 0;
   const int32_t* tables_from = nullptr;
@@ -197,15 +259,7 @@ void compute_layout(moe_handle* h) {
   L.plan = take(sizeof(moe_plan));
   L.err = take(sizeof(int32_t) * 4);
   h->off_calib = take(sizeof(DevCalib));
-  h->off_gwt = take(sizeof(uint16_t) * (size_t)c.n_experts * c.hidden);
-  h->off_glt = take(sizeof(float) * (size_t)T * c.n_experts);
-  h->off_gxn = take(sizeof(float) * (size_t)T);
-  h->off_gwn = take(sizeof(float) * (size_t)c.n_experts);
-  h->off_chg = take(sizeof(int32_t) * (size_t)T * c.n_experts);
-  h->off_che = take(sizeof(int32_t) * (size_t)T * c.n_experts);
-  h->off_chl = take(sizeof(float) * (size_t)T * c.n_experts);
-  h->off_tb = take(sizeof(int32_t) * (size_t)T);
-  h->off_tn = take(sizeof(int32_t) * (size_t)T);
+  h->off_gate = take(gate_layout(T, c.hidden, c.n_experts).total);
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
@@ -518,34 +572,14 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   g.bias = logit_bias;
   g.topk_idx = topk_idx;
   g.topk_w = topk_w;
-  g.wgt = at<uint16_t>(h, h->off_gwt);
-  g.lt = at<float>(h, h->off_glt);
-  g.xn = at<float>(h, h->off_gxn);
-  g.wn = at<float>(h, h->off_gwn);
-  g.ch_g = at<int32_t>(h, h->off_chg);
-  g.ch_e = at<int32_t>(h, h->off_che);
-  g.ch_l = at<float>(h, h->off_chl);
-  g.tok_base = at<int32_t>(h, h->off_tb);
-  g.tok_n = at<int32_t>(h, h->off_tn);
-  g.stats = at<int32_t>(h, h->lay.stats);
   g.T = h->T;
   g.H = h->cfg.hidden;
   g.E = h->cfg.n_experts;
   g.k = top_k;
-  // |L - L~| <= (gamma_{H-1}(2^-24) + gamma_H(2^-23)) * sum_h |x_h w_h|: the
-  // defined recursive fp32 sum and an fp32 accumulation of the MFMA products
-  // allowed twice the unit roundoff; sum |x w| <= ||x|| ||w||; 1% for the norms
-  {
-    const double H = (double)g.H, u = std::ldexp(1.0, -24), u2 = std::ldexp(1.0, -23);
-    const double g1 = (H - 1.0) * u / (1.0 - (H - 1.0) * u), g2 = H * u2 / (1.0 - H * u2);
-    g.bound = (float)(1.01 * (g1 + g2));
-  }
-  gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
-  gate_mfma_kernel<<<(h->T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
-  const int tok_blocks = (h->T + (NTH / 16) - 1) / (NTH / 16);
-  gate_chain_kernel<<<std::min(16384, std::max(1, (h->T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
-  gate_final_kernel<<<tok_blocks, NTH, 0, s>>>(g);
-  HIP_TRY(hipGetLastError());
+  // the chain counter goes to the layer's stats (word ST_CANDS, reported)
+  bind_gate(g, h->ws + h->off_gate, gate_layout(g.T, g.H, g.E), at<int32_t>(h, h->lay.stats));
+  st = launch_gate(g, s);
+  if (st != MOE_OK) return st;
   return moe_build_tables(h, topk_idx, stream);
 }
 
