@@ -266,6 +266,28 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg,
                      const float* logit_bias, int32_t top_k, int32_t* topk_idx,
                      float* topk_w, void* stream);
 
+/* Size of the device scratch of moe_route_topk_static: 96 MiB. */
+#define MOE_ROUTE_STATIC_SCRATCH_BYTES (96u << 20)
+
+/* The top-k routing of moe_route (gate logits, softmax, top-k,
+ * renormalisation; the same kernels and the same results) without a handle
+ * and without allocating anything, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation.  It builds no routing tables (moe_build_tables does).
+ * x: bf16 [T][H], wg: bf16 [H][E], logit_bias: fp32 [E] or NULL; writes
+ * topk_idx int32 [T][top_k] and topk_w fp32 [T][top_k] as moe_route does.
+ * The gate's scratch (its intermediate logits, norms and candidate chains,
+ * about E*H*2 + 16*T*E + 16*T bytes) lives in a static device array of
+ * MOE_ROUTE_STATIC_SCRATCH_BYTES that each GPU the library runs on holds
+ * until the process ends; larger problems are refused with
+ * MOE_ERR_UNSUPPORTED (nothing is launched).  Every call on a GPU shares that
+ * GPU's array and leaves its contents behind: calls that overlap on one GPU
+ * (other streams, other threads) race, so serialise them.  H must be a
+ * multiple of 64 in [64, 16384], E in [1, 512], top_k in [1, min(E, 8)]. */
+moe_status moe_route_topk_static(int32_t T, int32_t H, int32_t E, int32_t top_k, const uint16_t* x,
+                                 const uint16_t* wg, const float* logit_bias, int32_t* topk_idx, float* topk_w,
+                                 void* stream);
+
 /* Builds the routing tables of this GPU's share from topk_idx int32 [T][k]
  * (section 3.1 descriptors and the dispatch permutation): per-(expert, rank)
  * counts, unique-token counts, expert offsets, the slot of each local pair

@@ -99,6 +99,7 @@ _SIGS = {
     "moe_pack_weights": ([_H, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "moe_route": ([_H, _P, _P, _P, C.c_int32, _P, _P, _P], C.c_int),
     "moe_build_tables": ([_H, _P, _P], C.c_int),
+    "moe_route_topk_static": ([C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P], C.c_int),
     "moe_forward": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.POINTER(moe_plan), _P], C.c_int),
     "moe_run_stages": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P], C.c_int),
     "moe_get_plan": ([_H, C.POINTER(moe_plan), _P], C.c_int),
@@ -238,6 +239,13 @@ def moe_pack_weights(h: int, w1, w3, w2, ws1, ws3, ws2, packed: torch.Tensor, st
 def moe_route(h: int, x, wg, logit_bias, top_k: int, topk_idx, topk_w, stream=None) -> None:
     _check("moe_route", _lib.moe_route(h, _ptr(x), _ptr(wg), _ptr(logit_bias), int(top_k), _ptr(topk_idx),
                                        _ptr(topk_w), _stream(stream)))
+
+
+def moe_route_topk_static(T: int, H: int, E: int, top_k: int, x, wg, logit_bias, topk_idx, topk_w,
+                          stream=None) -> None:
+    _check("moe_route_topk_static", _lib.moe_route_topk_static(int(T), int(H), int(E), int(top_k), _ptr(x),
+                                                               _ptr(wg), _ptr(logit_bias), _ptr(topk_idx),
+                                                               _ptr(topk_w), _stream(stream)))
 
 
 def moe_build_tables(h: int, topk_idx, stream=None) -> None:

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "common.h"
@@ -382,6 +383,39 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
 }
 }  // namespace
 
+// ---- routing that allocates nothing ------------------------------------------
+// The gate's scratch for moe_route_topk_static lives in this file-scope
+// device array, so that the entry point needs no allocation.  Each GPU holds
+// its own copy until the process ends.  Host code must not use the array's
+// name as an address (it is a host-side stand-in): its device address is
+// looked up once per device with that device current and kept in
+// g_scratch_ptr, which is what the kernels receive.
+static __device__ __align__(256) unsigned char scratch[MOE_ROUTE_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+
+// the current device's address of `scratch` (looked up on its first use)
+moe_status static_scratch(char** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES)
+    return fail(MOE_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, SCRATCH_MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(MOE_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return MOE_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
@@ -718,6 +752,39 @@ moe_status moe_tile_geometry(const moe_handle* h, int32_t* bm, int32_t* nt0, int
   *nt0 = h->nt0;
   *nt1 = h->nt1 * h->nsplit;
   return MOE_OK;
+}
+
+moe_status moe_route_topk_static(int32_t T, int32_t H, int32_t E, int32_t top_k, const uint16_t* x,
+                                 const uint16_t* wg, const float* logit_bias, int32_t* topk_idx, float* topk_w,
+                                 void* stream) {
+  if (!x || !wg || !topk_idx || !topk_w) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (T < 1 || T > (1 << 22)) return fail(MOE_ERR_INVALID_ARG, "T = %d outside [1, 2^22]", T);
+  if (H < 64 || H % 64 || H > 16384) return fail(MOE_ERR_INVALID_ARG, "H must be a multiple of 64 in [64, 16384]");
+  if (E < 1 || E > MAX_E) return fail(MOE_ERR_INVALID_ARG, "E must be in [1, %d]", MAX_E);
+  if (top_k < 1 || top_k > MAX_TOPK || top_k > E)
+    return fail(MOE_ERR_INVALID_ARG, "top_k must be in [1, min(E, %d)]", MAX_TOPK);
+  const GateLayout L = gate_layout(T, H, E);
+  if (L.total > (size_t)MOE_ROUTE_STATIC_SCRATCH_BYTES)
+    return fail(MOE_ERR_UNSUPPORTED, "T = %d, H = %d, E = %d needs %zu bytes of gate scratch, more than the %zu of "
+                "the static scratch (use moe_route)", T, H, E, L.total, (size_t)MOE_ROUTE_STATIC_SCRATCH_BYTES);
+  char* base = nullptr;
+  moe_status st = static_scratch(&base);
+  if (st != MOE_OK) return st;
+  GateArgs g{};
+  g.x = x;
+  g.wg = wg;
+  g.bias = logit_bias;
+  g.topk_idx = topk_idx;
+  g.topk_w = topk_w;
+  g.T = T;
+  g.H = H;
+  g.E = E;
+  g.k = top_k;
+  // the chain counter (the one word that must start at zero) is cleared by
+  // the first kernel of the gate; every other region is written before it
+  // is read
+  bind_gate(g, base, L, reinterpret_cast<int32_t*>(base + L.stats));
+  return launch_gate(g, reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -161,3 +161,20 @@ def test_host_cost_model_matches_oracle(orc):
             assert p.t_pred_s == o.t_total, trial
     finally:
         B.moe_destroy(h)
+
+
+def test_static_routing_refuses_what_its_scratch_cannot_hold():
+    """moe_route_topk_static checks its arguments and the size of its static
+    scratch on the host and launches nothing when they do not fit."""
+    import types
+    import torch
+    x = torch.zeros(8, dtype=torch.int16)
+    null_stream = types.SimpleNamespace(cuda_stream=0)  # the null stream, without initialising a GPU
+    dummy = [x, x, None, x, x, null_stream]
+    with pytest.raises(B.MoeError) as ei:
+        B.moe_route_topk_static(1 << 21, 4096, 512, 8, *dummy)
+    assert ei.value.status == B.MOE_ERR_UNSUPPORTED and "static scratch" in B.moe_last_error()
+    for T, H, E, k in [(0, 64, 8, 2), (16, 96, 8, 2), (16, 64, 0, 1), (16, 64, 8, 9), (16, 64, 4, 5)]:
+        with pytest.raises(B.MoeError) as ei:
+            B.moe_route_topk_static(T, H, E, k, *dummy)
+        assert ei.value.status == B.MOE_ERR_INVALID_ARG, (T, H, E, k)
