@@ -382,6 +382,7 @@ def measure_stack(B, stack, args, stream, flush, trace: bool):
         rec = {"layer": stack.ids[i], "plan": {"c": p.c, "K": p.K, "n_steal": p.n_steal, "final_all": p.final_all,
                                                 "t_pred_us": p.t_pred_s * 1e6},
                "local_pairs": int(stats[i][0]), "gflop": flops[i] / 1e9,
+               "route_exact_chains": int(stats[i][8]),
                "layer_us": float(np.median(fwd_us[i])),
                "layer_us_p10_p90": [float(np.percentile(fwd_us[i], 10)), float(np.percentile(fwd_us[i], 90))],
                "layer_us_flushed": float(np.median(fl[i])) if fl else None,

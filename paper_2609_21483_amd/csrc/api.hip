@@ -91,9 +91,46 @@ moe_status launch_gate(GateArgs& g, hipStream_t s) {
     g.bound = (float)(1.01 * (g1 + g2));
   }
   gate_prep_kernel<<<g.E, NTH, 0, s>>>(g);
-  gate_mfma_kernel<<<(g.T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
-  gate_chain_kernel<<<std::min(16384, std::max(1, (g.T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
-  gate_final_kernel<<<(g.T + (NTH / 16) - 1) / (NTH / 16), NTH, 0, s>>>(g);
+  if (g.E <= 32) gate_mfma_kernel<<<(g.T + 31) / 32, GATE_WAVES * WAVE, 0, s>>>(g);
+  // more experts: LDS-staged tiles, 128 tokens each when that still gives
+  // every CU a tile, else 64
+  else if (g.E <= 128) {
+    // logits and candidates without leaving LDS, 128 tokens per workgroup
+    // when that still gives every CU a tile, else 64
+    if (g.T >= 128 * 256) gate_tile2_kernel<128><<<(g.T + 127) / 128, 2 * NTH, 0, s>>>(g);
+    else gate_tile2_kernel<64><<<(g.T + 63) / 64, 2 * NTH, 0, s>>>(g);
+  } else {
+    // experts per lane of the candidate pass (16 lanes per token)
+    const int epl = g.E <= 64 ? 4 : g.E <= 128 ? 8 : 32;
+    const bool big = g.T >= 128 * 256;
+    const dim3 grid(big ? (g.T + 127) / 128 : (g.T + 63) / 64);
+    if (big) {
+      if (epl == 4) gate_tile_kernel<128, 4><<<grid, NTH, 0, s>>>(g);
+      else if (epl == 8) gate_tile_kernel<128, 8><<<grid, NTH, 0, s>>>(g);
+      else gate_tile_kernel<128, 32><<<grid, NTH, 0, s>>>(g);
+    } else {
+      if (epl == 4) gate_tile_kernel<64, 4><<<grid, NTH, 0, s>>>(g);
+      else if (epl == 8) gate_tile_kernel<64, 8><<<grid, NTH, 0, s>>>(g);
+      else gate_tile_kernel<64, 32><<<grid, NTH, 0, s>>>(g);
+    }
+  }
+  if (g.E <= 128 && (long long)g.T * g.k >= 32768) {
+    // persistent over ranges of chains, at most T * E of them (with fewer
+    // chains than about 64 ranges, one chain per lane over many small
+    // workgroups spreads them over more CUs)
+    const long long ranges = ((long long)g.T * g.E + GATE_CHAIN_STAGED_W - 1) / GATE_CHAIN_STAGED_W;
+    gate_chain_staged_kernel<<<(int)std::min<long long>(ranges, 256), GATE_CHAIN_STAGED_W, 0, s>>>(g);
+  } else {
+    gate_chain_kernel<<<std::min(16384, std::max(1, (g.T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
+  }
+  {
+    const dim3 grid((g.T + NTH - 1) / NTH);
+    if (g.E <= 16) gate_final_kernel<1><<<grid, NTH, 0, s>>>(g);
+    else if (g.E <= 32) gate_final_kernel<2><<<grid, NTH, 0, s>>>(g);
+    else if (g.E <= 64) gate_final_kernel<4><<<grid, NTH, 0, s>>>(g);
+    else if (g.E <= 128) gate_final_kernel<8><<<grid, NTH, 0, s>>>(g);
+    else gate_final_kernel<32><<<grid, NTH, 0, s>>>(g);
+  }
   HIP_TRY(hipGetLastError());
   return MOE_OK;
 }
@@ -109,7 +146,8 @@ struct moe_handle {
   moe_calib calib{};
   DevCalib dcal{};
   moe_ws_layout lay{};
-  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_blk_bad = 0, off_ctl[2] = {0, 0}, off_part = 0;
+  size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_blk_bad = 0, off_rbnd = 0, off_ctl[2] = {0, 0};
+  size_t off_part = 0;
   size_t off_gate = 0;  // the gate's scratch (gate_layout)
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -264,6 +302,7 @@ void compute_layout(moe_handle* h) {
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
+  h->off_rbnd = take(sizeof(int32_t) * (size_t)El * (R + 1));
   h->off_ctl[0] = take(sizeof(int32_t) * (size_t)h->ctl_words);
   h->off_ctl[1] = take(sizeof(int32_t) * (size_t)h->ctl_words);
   h->arows = a_rows(c);
@@ -300,6 +339,7 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
   a.blk_cnt = at<int32_t>(h, h->off_blk_cnt);
   a.blk_off = at<int32_t>(h, h->off_blk_off);
   a.blk_bad = at<int32_t>(h, h->off_blk_bad);
+  a.rbnd = at<int32_t>(h, h->off_rbnd);
   a.err = at<int32_t>(h, h->lay.err);
   a.T = h->T;
   a.Tr = h->cfg.tokens_per_rank;
@@ -585,7 +625,7 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   TableArgs a = table_args(h, topk_idx);
   tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
-  tab_scan_kernel<<<1, NTH, 0, s>>>(a);
+  tab_scan_kernel<<<1, TAB_SCAN_THREADS, 0, s>>>(a);
   tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_finalize_kernel<<<1, NTH, 0, s>>>(a);
   HIP_TRY(hipGetLastError());

@@ -40,6 +40,7 @@ struct TableArgs {
   int32_t* blk_cnt;
   int32_t* blk_off;
   int32_t* blk_bad;    // [nblk] tokens with an invalid or repeated id, per table block
+  int32_t* rbnd;       // [E_l][R + 1] first slot of each expert at or after each rank boundary
   int32_t* err;
   int T, Tr, R, k, E, e0, El, nblk;
   int S, tiles_per_row_tile;  // shared experts; GEMM0 + GEMM1 tiles of one row tile (the cost model's tile counts)
@@ -225,12 +226,21 @@ constexpr int GATE_WAVES = 4;  // wavefronts per workgroup of gate_mfma_kernel (
 // ---- launch prototypes ---------------------------------------------------------
 __global__ void gate_prep_kernel(GateArgs a);
 __global__ void gate_mfma_kernel(GateArgs a);
+template <int GT_M, int EPL>
+__global__ void gate_tile_kernel(GateArgs a);  // E > 32; GT_M tokens per workgroup (64 or 128),
+                                               // EPL >= E / 16 experts per lane in the candidate pass
 __global__ void gate_chain_kernel(GateArgs a);
-__global__ void gate_final_kernel(GateArgs a);
+__global__ void gate_chain_staged_kernel(GateArgs a);  // E <= 128
+constexpr int GATE_CHAIN_STAGED_W = 512;               // chains per workgroup of gate_chain_staged_kernel
+template <int GT_M>
+__global__ void gate_tile2_kernel(GateArgs a);  // 32 < E <= 128; GT_M tokens per workgroup (64 or 128)
+template <int EPL>
+__global__ void gate_final_kernel(GateArgs a);  // EPL >= E / 16 experts per lane
 __global__ void tab_count_kernel(TableArgs a);
 __global__ void tab_scan_kernel(TableArgs a);
 __global__ void tab_perm_kernel(TableArgs a);
 __global__ void tab_finalize_kernel(TableArgs a);
+constexpr int TAB_SCAN_THREADS = 1024;  // one workgroup of tab_scan_kernel
 __global__ void zero_i32_kernel(int* p, int n);
 __global__ void pack_transpose_kernel(PackArgs a);
 __global__ void pack_pad_kernel(PadArgs a);

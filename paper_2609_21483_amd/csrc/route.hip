@@ -182,7 +182,6 @@ __device__ __forceinline__ void gate_mfma_body(const GateArgs& a, float (*red)[3
 
 // lanes of one token's group of GG: reductions stay inside the group
 constexpr int GG = 16;
-constexpr int GEPL = MAX_E / GG;  // experts per lane
 constexpr int GTOK = NTH / GG;    // tokens per workgroup
 
 __device__ __forceinline__ bool better(float v, int e, float bv, int be) {
@@ -205,74 +204,107 @@ __device__ __forceinline__ void interval(const GateArgs& a, int g, int e, float 
   d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
 }
 
-// Candidates of the GTOK tokens from g0 on (one workgroup of NTH threads):
-// tau = k-th largest lower end; every expert whose upper end reaches tau
-// becomes a chain (g, e) of the chain list, in expert order per token.  The
-// workgroup takes its chain range with one atomic.
-__device__ __forceinline__ void cand_tokens(const GateArgs& a, int g0, int* cnt, int& base_s) {
+// Candidates of the ntok tokens from g0 (one workgroup of NTH threads, GTOK
+// tokens per pass, a token's experts spread over the GG lanes of its group,
+// EPL each): tau = the k-th largest lower end; every expert whose upper end
+// reaches tau becomes a chain (g, e) of the chain list.  A first pass counts
+// each token's candidates, the tile takes its range of the list with one
+// atomic, and a second pass writes each token's chains in ascending expert
+// order (experts of neighbouring chains then differ in their low bits,
+// which spreads the chain kernel's reads of their gate rows over the LDS
+// banks).  t_cnt, t_off, t_tau: ntok entries of workgroup memory.
+template <int EPL>
+__device__ __forceinline__ void cand_tile(const GateArgs& a, int g0, int ntok, int* t_cnt, int* t_off, float* t_tau,
+                                          int& base_s) {
   const int tid = threadIdx.x, grp = tid / GG, gl = tid % GG;
-  const int g = g0 + grp;
-  const bool valid = g < a.T;
-  const int gs = valid ? g : 0;
-  const float xn = a.xn[gs];
-  float lo[GEPL], hi[GEPL];
+  for (int t0 = 0; t0 < ntok; t0 += GTOK) {
+    const int g = g0 + t0 + grp;
+    const bool valid = g < a.T;
+    const int gs = valid ? g : 0;
+    const float xn = a.xn[gs];
+    float lo[EPL], hi[EPL];
 #pragma unroll
-  for (int i = 0; i < GEPL; ++i) {
-    const int e = gl + GG * i;
-    lo[i] = hi[i] = -INFINITY;
-    if (e < a.E) {
-      float l, d;
-      interval(a, gs, e, xn, l, d);
-      lo[i] = l - d;
-      hi[i] = l + d;
+    for (int i = 0; i < EPL; ++i) {
+      const int e = gl + GG * i;
+      lo[i] = hi[i] = -INFINITY;
+      if (e < a.E) {
+        float l, d;
+        interval(a, gs, e, xn, l, d);
+        lo[i] = l - d;
+        hi[i] = l + d;
+      }
+    }
+    float tau = -INFINITY;
+    for (int r = 0; r < a.k; ++r) {
+      float v = -INFINITY;
+      int e = 1 << 30;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i)
+        if (better(lo[i], gl + GG * i, v, e)) { v = lo[i]; e = gl + GG * i; }
+      group_argmax(v, e);
+      tau = v;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i)
+        if (gl + GG * i == e) lo[i] = -INFINITY;
+    }
+    int mine = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) mine += valid && hi[i] >= tau;
+#pragma unroll
+    for (int d = GG / 2; d > 0; d >>= 1) mine += __shfl_xor(mine, d, WAVE);
+    if (gl == 0) {
+      t_cnt[t0 + grp] = mine;
+      t_tau[t0 + grp] = tau;
     }
   }
-  float tau = -INFINITY;
-  for (int r = 0; r < a.k; ++r) {
-    float v = -INFINITY;
-    int e = 1 << 30;
-#pragma unroll
-    for (int i = 0; i < GEPL; ++i)
-      if (better(lo[i], gl + GG * i, v, e)) { v = lo[i]; e = gl + GG * i; }
-    group_argmax(v, e);
-    tau = v;
-#pragma unroll
-    for (int i = 0; i < GEPL; ++i)
-      if (gl + GG * i == e) lo[i] = -INFINITY;
-  }
-  int mine = 0;
-#pragma unroll
-  for (int i = 0; i < GEPL; ++i) mine += valid && hi[i] >= tau;
-  int pre = mine;
-#pragma unroll
-  for (int d = 1; d < GG; d <<= 1) {
-    const int o = __shfl_up(pre, d, GG);
-    if (gl >= d) pre += o;
-  }
-  const int total = __shfl(pre, GG - 1, GG);
-  if (gl == 0) cnt[grp] = total;
   __syncthreads();
-  if (tid == 0) {
-    int t = 0;
-    for (int q = 0; q < GTOK; ++q) { const int c = cnt[q]; cnt[q] = t; t += c; }
-    base_s = atomicAdd(&a.stats[ST_CANDS], t);
-  }
-  __syncthreads();
-  const int tb = base_s + cnt[grp];
-  if (valid && gl == 0) {
-    a.tok_base[g] = tb;
-    a.tok_n[g] = total;
-  }
-  // this lane's candidates, in expert order within the lane; the final pass
-  // does not depend on the order
-  int pos = tb + pre - mine;
+  if (tid < WAVE) {  // exclusive scan of the counts, one atomic for the tile
+    int carry = 0;
+    for (int b = 0; b < ntok; b += WAVE) {
+      const int c = b + tid < ntok ? t_cnt[b + tid] : 0;
+      int x = c;
 #pragma unroll
-  for (int i = 0; i < GEPL; ++i)
-    if (valid && hi[i] >= tau) {
-      a.ch_g[pos] = g;
-      a.ch_e[pos] = gl + GG * i;
-      ++pos;
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const int y = __shfl_up(x, d, WAVE);
+        if (tid >= d) x += y;
+      }
+      if (b + tid < ntok) t_off[b + tid] = carry + x - c;
+      carry += __shfl(x, WAVE - 1, WAVE);
     }
+    if (tid == 0) base_s = atomicAdd(&a.stats[ST_CANDS], carry);
+  }
+  __syncthreads();
+  const int gw = (tid & (WAVE - 1)) / GG;  // the group's place in its wavefront
+  for (int t0 = 0; t0 < ntok; t0 += GTOK) {
+    const int g = g0 + t0 + grp;
+    const bool valid = g < a.T;
+    const int gs = valid ? g : 0;
+    const float xn = a.xn[gs];
+    const float tau = t_tau[t0 + grp];
+    const int tb = base_s + t_off[t0 + grp];
+    if (valid && gl == 0) {
+      a.tok_base[g] = tb;
+      a.tok_n[g] = t_cnt[t0 + grp];
+    }
+    int run = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = gl + GG * i;
+      bool c = false;
+      if (valid && e < a.E) {
+        float l, d;
+        interval(a, gs, e, xn, l, d);
+        c = l + d >= tau;
+      }
+      const uint32_t gm = (uint32_t)(__ballot(c) >> (gw * GG)) & ((1u << GG) - 1);
+      if (c) {
+        const int pos = tb + run + __builtin_popcount(gm & ((1u << gl) - 1));
+        a.ch_g[pos] = g;
+        a.ch_e[pos] = e;
+      }
+      run += __builtin_popcount(gm);
+    }
+  }
 }
 
 // Approximate logits of 32 tokens, then their candidates: the workgroup's
@@ -372,20 +404,392 @@ __device__ __forceinline__ void gate_mfma_staged(const GateArgs& a, char* ring_a
 
 __global__ void __launch_bounds__(GATE_WAVES * WAVE) gate_mfma_kernel(GateArgs a) {
   static_assert(GATE_WAVES * WAVE == NTH && 32 % GTOK == 0, "candidate pass geometry");
-  __shared__ int cnt[GTOK];
+  __shared__ int t_cnt[32], t_off[32];
+  __shared__ float t_tau[32];
   __shared__ int base_s;
   __shared__ float red[GATE_WAVES - 1][32 * 32 * 4];
   __shared__ float ssr[GATE_WAVES][64];
   __shared__ __align__(16) char ring[GATE_WAVES * GS_ST * GS_SB];
-  if (a.E <= 32 && (a.H / GATE_WAVES) % 64 == 0) gate_mfma_staged(a, ring, red, ssr);
-  else if (a.E <= 32) gate_mfma_body<1, 8, GATE_WAVES>(a, red, ssr);
-  else gate_mfma_body<4, 4, GATE_WAVES>(a, red, ssr);
+  // E <= 32 (more experts: gate_tile_kernel)
+  if ((a.H / GATE_WAVES) % 64 == 0) gate_mfma_staged(a, ring, red, ssr);
+  else gate_mfma_body<1, 8, GATE_WAVES>(a, red, ssr);
   __syncthreads();
-  for (int sub = 0; sub < 32 / GTOK; ++sub) {
-    cand_tokens(a, blockIdx.x * 32 + sub * GTOK, cnt, base_s);
-    __syncthreads();
+  cand_tile<2>(a, blockIdx.x * 32, 32, t_cnt, t_off, t_tau, base_s);  // E <= 32: two experts per lane
+}
+
+// E > 32: the approximate logits of a tile of GT_M tokens x GT_N experts per
+// pass over the experts, on v_mfma_f32_32x32x16_bf16 (fp32 accumulation) with
+// both operands streamed through an LDS ring of GT_NS stages of 64-deep
+// k-steps by direct global->LDS loads.  In a load instruction 8 lanes fetch
+// one row's 128 contiguous bytes, so it covers 8 whole lines (x is row-major
+// with 2H-byte rows, the transposed gate too).  A row's 16-byte granules are
+// stored XOR-swizzled by (row & 7), so that the fragment reads of 8 lanes on
+// 8 consecutive rows hit distinct banks.  Four wavefronts in a 2 x 2 grid,
+// each (GT_M / 2) tokens x 64 experts.  Token rows past T and gate rows past
+// E repeat the last valid row; their sums are not stored.  The token norms
+// come from the same x fragments (wavefronts of the first expert column, on
+// the first pass).  Then the candidate pass of the tile's tokens.
+constexpr int GT_N = 128;  // experts per pass
+constexpr int GT_K = 64;   // values per row piece of a stage (128 bytes)
+constexpr int GT_NS = 4;   // ring stages
+
+template <int OUT>
+__device__ __forceinline__ void gt_wait(int outstanding) {
+  // at most `outstanding` stages (OUT DMA instructions each) still in flight
+  if (outstanding >= 2) gemm::wait_vm<2 * OUT>();
+  else if (outstanding == 1) gemm::wait_vm<OUT>();
+  else gemm::wait_vm<0>();
+}
+
+template <int GT_M, int EPL>
+__global__ void __launch_bounds__(NTH) gate_tile_kernel(GateArgs a) {
+  static_assert(NTH == 4 * WAVE && GT_M % 64 == 0 && GT_M % GTOK == 0, "gate tile geometry");
+  constexpr int A_B = GT_M * 2 * GT_K, B_B = GT_N * 2 * GT_K, ST_B = A_B + B_B;
+  constexpr int A_I = A_B / 1024 / 4, B_I = B_B / 1024 / 4;  // DMA instructions per wavefront and stage
+  constexpr int WI = A_I + B_I;
+  constexpr int MBW = GT_M / 64;  // 32-token blocks per wavefront
+  static_assert(GT_NS - 2 <= 2, "gt_wait covers two stages in flight");
+  __shared__ __attribute__((aligned(1024))) char ring[GT_NS * ST_B];
+  __shared__ int t_cnt[GT_M], t_off[GT_M];
+  __shared__ float t_tau[GT_M];
+  __shared__ int base_s;
+  const int lane = gemm::lane_here(), wave = gemm::opaque((int)(threadIdx.x / WAVE));
+  const int wm = wave & 1, wn = wave >> 1;
+  const int g0 = blockIdx.x * GT_M;
+  const int H = gemm::opaque(a.H), nk = H / GT_K;
+  const uint32_t ring0 = (uint32_t)gemm::opaque((int)gemm::lds_u32(ring));
+  // this lane's byte offsets of its DMA rows from the operands' first rows
+  uint32_t ao[A_I];
+#pragma unroll
+  for (int i = 0; i < A_I; ++i) {
+    const int row = (wave * A_I + i) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7);
+    ao[i] = (uint32_t)(min(row, a.T - 1 - g0) * H * 2 + c * 16);
+  }
+  const char* xb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.x + (size_t)g0 * H));
+  float ss[MBW];
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb) ss[mb] = 0.0f;
+  for (int eb = 0; eb < a.E; eb += GT_N) {
+    uint32_t bo[B_I];
+#pragma unroll
+    for (int i = 0; i < B_I; ++i) {
+      const int row = (wave * B_I + i) * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ (row & 7);
+      bo[i] = (uint32_t)(min(row, a.E - 1 - eb) * H * 2 + c * 16);
+    }
+    const char* wb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.wgt + (size_t)eb * H));
+    auto issue = [&](int st) {
+      const uint32_t dst = ring0 + (uint32_t)((st % GT_NS) * ST_B);
+#pragma unroll
+      for (int i = 0; i < A_I; ++i) gemm::dma16(xb + (size_t)st * (2 * GT_K), ao[i], dst + (wave * A_I + i) * 1024);
+#pragma unroll
+      for (int i = 0; i < B_I; ++i)
+        gemm::dma16(wb + (size_t)st * (2 * GT_K), bo[i], dst + A_B + (wave * B_I + i) * 1024);
+    };
+    f32x16_t acc[MBW][2];
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16_t{};
+    for (int st = 0; st < GT_NS - 1 && st < nk; ++st) issue(st);
+    const int ra = wm * (GT_M / 2) + (lane & 31), rb = wn * 64 + (lane & 31);
+    for (int st = 0; st < nk; ++st) {
+      gt_wait<WI>(min(GT_NS - 2, nk - 1 - st));
+      __builtin_amdgcn_s_barrier();
+      gemm::compiler_fence();
+      if (st + GT_NS - 1 < nk) issue(st + GT_NS - 1);
+      const char* sa = ring + (st % GT_NS) * ST_B;
+      const char* sb = sa + A_B;
+#pragma unroll
+      for (int kk = 0; kk < GT_K / 16; ++kk) {
+        const int ch = 2 * kk + (lane >> 5);
+        bf16x8_t af[MBW], bf[2];
+#pragma unroll
+        for (int mb = 0; mb < MBW; ++mb) {
+          const int r = ra + mb * 32;
+          af[mb] = *reinterpret_cast<const bf16x8_t*>(sa + r * 128 + ((ch ^ (r & 7)) << 4));
+        }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const int r = rb + nb * 32;
+          bf[nb] = *reinterpret_cast<const bf16x8_t*>(sb + r * 128 + ((ch ^ (r & 7)) << 4));
+        }
+        if (wn == 0 && eb == 0) {
+#pragma unroll
+          for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              const float f = (float)af[mb][q];
+              ss[mb] += f * f;
+            }
+        }
+#pragma unroll
+        for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bf[nb], acc[mb][nb], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_barrier();  // the ring is refilled by the next pass
+    gemm::compiler_fence();
+    // C[8 (r >> 2) + 4 (l >> 5) + (r & 3)][l & 31] of each 32 x 32 block
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int e = eb + wn * 64 + nb * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int g = g0 + wm * (GT_M / 2) + mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (e < a.E && g < a.T) a.lt[(size_t)g * a.E + e] = acc[mb][nb][r];
+        }
+      }
+  }
+  if (wn == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb) {
+      const float t = ss[mb] + __shfl_xor(ss[mb], 32, WAVE);
+      const int g = g0 + wm * (GT_M / 2) + mb * 32 + lane;
+      if (lane < 32 && g < a.T) a.xn[g] = sqrtf(t);
+    }
+  }
+  __syncthreads();  // the tile's logits and norms are in memory for the candidate pass
+  cand_tile<EPL>(a, g0, GT_M, t_cnt, t_off, t_tau, base_s);
+}
+
+template __global__ void gate_tile_kernel<64, 4>(GateArgs);
+template __global__ void gate_tile_kernel<64, 8>(GateArgs);
+template __global__ void gate_tile_kernel<64, 32>(GateArgs);
+template __global__ void gate_tile_kernel<128, 4>(GateArgs);
+template __global__ void gate_tile_kernel<128, 8>(GateArgs);
+template __global__ void gate_tile_kernel<128, 32>(GateArgs);
+
+// 32 < E <= 128: the approximate logits of GT_M tokens x all experts in one
+// workgroup of 8 wavefronts, then the candidate pass, without the logits
+// leaving LDS.  The operands stream through the same LDS ring as in
+// gate_tile_kernel (64-deep k-steps, 8 lanes per 128-byte row piece, granules
+// XOR-swizzled by row & 7).  Wavefronts 0-3 take the first two 16-deep
+// slices of every k-step, 4-7 the last two, in a 2 x 2 grid of (GT_M / 2)
+// tokens x 64 experts each; the two halves' sums are added through LDS at
+// the end (the bound holds for any order of the approximate sum).  The
+// logits, plus bias, go to an LDS tile of GT_M rows (padded to 129 words so
+// that lanes reading their own rows hit distinct banks); one lane per token
+// then keeps the k largest lower ends of its intervals in a sorted list,
+// takes tau = the k-th, and lists the experts whose upper end reaches tau.
+constexpr int G2_PAD = GT_N + 1;  // words per row of the LDS logit tile
+
+template <int GT_M>
+__global__ void __launch_bounds__(2 * NTH) gate_tile2_kernel(GateArgs a) {
+  constexpr int NW = 8;
+  constexpr int A_B = GT_M * 2 * GT_K, B_B = GT_N * 2 * GT_K, ST_B = A_B + B_B;
+  constexpr int A_I = A_B / 1024 / NW, B_I = B_B / 1024 / NW;  // DMA instructions per wavefront and stage
+  constexpr int WI = A_I + B_I;
+  constexpr int MBW = GT_M / 64;
+  static_assert(A_I >= 1 && B_I >= 1 && GT_M % 64 == 0, "tile geometry");
+  static_assert(GT_M * G2_PAD * 4 <= GT_NS * ST_B && 4 * MBW * 2 * 16 * WAVE * 4 <= GT_NS * ST_B, "ring reuse");
+  __shared__ __attribute__((aligned(1024))) char ring[GT_NS * ST_B];
+  __shared__ float ssq[2][GT_M];  // partial squared norms of the two k halves
+  __shared__ float bias_s[GT_N], wn_s[GT_N];
+  __shared__ int t_cnt[GT_M], t_off[GT_M];
+  __shared__ int base_s;
+  const int lane = gemm::lane_here(), wave = gemm::opaque((int)(threadIdx.x / WAVE));
+  const int kh = wave >> 2, wm = wave & 1, wn = (wave >> 1) & 1;
+  const int g0 = blockIdx.x * GT_M;
+  const int H = gemm::opaque(a.H), nk = H / GT_K;
+  const uint32_t ring0 = (uint32_t)gemm::opaque((int)gemm::lds_u32(ring));
+  for (int e = threadIdx.x; e < GT_N; e += 2 * NTH) {
+    bias_s[e] = (a.bias && e < a.E) ? a.bias[e] : 0.0f;
+    wn_s[e] = e < a.E ? a.wn[e] : 0.0f;
+  }
+  uint32_t ao[A_I], bo[B_I];
+#pragma unroll
+  for (int i = 0; i < A_I; ++i) {
+    const int row = (wave * A_I + i) * 8 + (lane >> 3);
+    ao[i] = (uint32_t)(min(row, a.T - 1 - g0) * H * 2 + (((lane & 7) ^ (row & 7)) << 4));
+  }
+#pragma unroll
+  for (int i = 0; i < B_I; ++i) {
+    const int row = (wave * B_I + i) * 8 + (lane >> 3);
+    bo[i] = (uint32_t)(min(row, a.E - 1) * H * 2 + (((lane & 7) ^ (row & 7)) << 4));
+  }
+  const char* xb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.x + (size_t)g0 * H));
+  const char* wb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.wgt));
+  auto issue = [&](int st) {
+    const uint32_t dst = ring0 + (uint32_t)((st % GT_NS) * ST_B);
+#pragma unroll
+    for (int i = 0; i < A_I; ++i) gemm::dma16(xb + (size_t)st * (2 * GT_K), ao[i], dst + (wave * A_I + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < B_I; ++i)
+      gemm::dma16(wb + (size_t)st * (2 * GT_K), bo[i], dst + A_B + (wave * B_I + i) * 1024);
+  };
+  f32x16_t acc[MBW][2];
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16_t{};
+  float ss[MBW];
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb) ss[mb] = 0.0f;
+  for (int st = 0; st < GT_NS - 1 && st < nk; ++st) issue(st);
+  const int ra = wm * (GT_M / 2) + (lane & 31), rb = wn * 64 + (lane & 31);
+  for (int st = 0; st < nk; ++st) {
+    gt_wait<WI>(min(GT_NS - 2, nk - 1 - st));
+    __builtin_amdgcn_s_barrier();
+    gemm::compiler_fence();
+    if (st + GT_NS - 1 < nk) issue(st + GT_NS - 1);
+    const char* sa = ring + (st % GT_NS) * ST_B;
+    const char* sb = sa + A_B;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int ch = 2 * (2 * kh + k2) + (lane >> 5);
+      bf16x8_t af[MBW], bf[2];
+#pragma unroll
+      for (int mb = 0; mb < MBW; ++mb) {
+        const int r = ra + mb * 32;
+        af[mb] = *reinterpret_cast<const bf16x8_t*>(sa + r * 128 + ((ch ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int r = rb + nb * 32;
+        bf[nb] = *reinterpret_cast<const bf16x8_t*>(sb + r * 128 + ((ch ^ (r & 7)) << 4));
+      }
+      if (wn == 0) {
+#pragma unroll
+        for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float f = (float)af[mb][q];
+            ss[mb] += f * f;
+          }
+      }
+#pragma unroll
+      for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bf[nb], acc[mb][nb], 0, 0, 0);
+    }
+  }
+  __builtin_amdgcn_s_barrier();  // the ring is reused below
+  gemm::compiler_fence();
+  // the second k half's sums, through LDS, into the first half's
+  float* part = reinterpret_cast<float*>(ring);
+  const int pw = wave & 3;  // the partner wavefront's place in its half
+  if (kh == 1) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) part[(((pw * MBW + mb) * 2 + nb) * 16 + r) * WAVE + lane] = acc[mb][nb][r];
+  }
+  if (wn == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb) {
+      const float t = ss[mb] + __shfl_xor(ss[mb], 32, WAVE);
+      if (lane < 32) ssq[kh][wm * (GT_M / 2) + mb * 32 + lane] = t;
+    }
+  }
+  __syncthreads();
+  if (kh == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mb][nb][r] += part[(((pw * MBW + mb) * 2 + nb) * 16 + r) * WAVE + lane];
+  }
+  __syncthreads();
+  // logits plus bias into the tile: C[8 (r >> 2) + 4 (l >> 5) + (r & 3)][l & 31] of each block
+  float* tile = reinterpret_cast<float*>(ring);
+  if (kh == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int e = wn * 64 + nb * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int t = wm * (GT_M / 2) + mb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          float l = acc[mb][nb][r];
+          if (a.bias) l = l + bias_s[e];
+          tile[t * G2_PAD + e] = l;
+        }
+      }
+  }
+  __syncthreads();
+  // candidates, one lane per token: the k largest lower ends (a sorted
+  // list; equal values are all kept, so top[k-1] is the k-th largest)
+  const int t = threadIdx.x;
+  const int g = g0 + t;
+  const bool mine = t < GT_M && g < a.T;
+  float tau = -INFINITY;
+  float xn = 0.0f;
+  int cnt = 0;
+  if (mine) {
+    xn = sqrtf(ssq[0][t] + ssq[1][t]);
+    float top[MAX_TOPK];
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) top[j] = -INFINITY;
+    for (int e = 0; e < a.E; ++e) {
+      const float l = tile[t * G2_PAD + e];
+      float d = a.bound * xn * wn_s[e];
+      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
+      float v = l - d;
+#pragma unroll
+      for (int j = 0; j < MAX_TOPK; ++j) {
+        const float hi = fmaxf(v, top[j]);
+        v = fminf(v, top[j]);
+        top[j] = hi;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j)
+      if (j == a.k - 1) tau = top[j];
+    for (int e = 0; e < a.E; ++e) {
+      const float l = tile[t * G2_PAD + e];
+      float d = a.bound * xn * wn_s[e];
+      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
+      cnt += l + d >= tau;
+    }
+  }
+  if (t < GT_M) t_cnt[t] = cnt;  // 0 for rows past T
+  __syncthreads();
+  if (threadIdx.x < WAVE) {  // exclusive scan of the counts, one atomic for the tile
+    int carry = 0;
+    for (int b = 0; b < GT_M; b += WAVE) {
+      const int c = t_cnt[b + lane];
+      int x = c;
+#pragma unroll
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const int y = __shfl_up(x, d, WAVE);
+        if (lane >= d) x += y;
+      }
+      t_off[b + lane] = carry + x - c;
+      carry += __shfl(x, WAVE - 1, WAVE);
+    }
+    if (lane == 0) base_s = atomicAdd(&a.stats[ST_CANDS], carry);
+  }
+  __syncthreads();
+  if (mine) {
+    int pos = base_s + t_off[t];
+    a.tok_base[g] = pos;
+    a.tok_n[g] = cnt;
+    for (int e = 0; e < a.E; ++e) {
+      const float l = tile[t * G2_PAD + e];
+      float d = a.bound * xn * wn_s[e];
+      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
+      if (l + d >= tau) {
+        a.ch_g[pos] = g;
+        a.ch_e[pos] = e;
+        ++pos;
+      }
+    }
   }
 }
+
+template __global__ void gate_tile2_kernel<64>(GateArgs);
+template __global__ void gate_tile2_kernel<128>(GateArgs);
 
 // the defined logit of one (token, expert): fp32, one accumulator, h
 // ascending, each product rounded before the add.  A product of two bf16
@@ -447,64 +851,150 @@ __global__ void __launch_bounds__(WAVE) gate_chain_kernel(GateArgs a) {
   }
 }
 
-// top-k of the candidates' defined logits (descending, equal logits ->
-// smaller id); softmax normaliser from the defined logits of the candidates
-// and the approximate ones elsewhere (it cancels in the renormalisation)
-__global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a) {
-  __shared__ uint32_t cmask[GTOK][MAX_E / 32];
-  const int tid = threadIdx.x, grp = tid / GG, gl = tid % GG;
-  const int g = blockIdx.x * GTOK + grp;
-  const bool valid = g < a.T;
-  const int gs = valid ? g : 0;
-  for (int i = gl; i < MAX_E / 32; i += GG) cmask[grp][i] = 0u;
-  __builtin_amdgcn_wave_barrier();
-  const int tb = valid ? a.tok_base[g] : 0, tn = valid ? a.tok_n[g] : 0;
-  for (int c = gl; c < tn; c += GG) {
-    const int e = a.ch_e[tb + c];
-    atomicOr(&cmask[grp][e >> 5], 1u << (e & 31));
+// The chains of the list for E <= CH_E: one lane per chain, CH_W chains per
+// workgroup.  For each 64-value block of h the workgroup stages that block of
+// all gate rows in LDS (CH_E rows of 128 bytes, whole lines by direct
+// global->LDS loads, rows past E repeating the last one) in a ring of CH_P
+// stages; a lane reads its gate values from there and its x values straight
+// from global memory into one of CH_P register sets: the chains of one token
+// are adjacent in the list, so a wavefront's load touches few lines.  The
+// 64 products of a block are added in order, each rounded before the add, as
+// in exact_logit.  Granules of a staged row are XOR-swizzled by (row & 7).
+constexpr int CH_W = 512, CH_E = 128, CH_K = 64, CH_P = 4;
+constexpr int CH_DMA = CH_E / 8 / (CH_W / WAVE);  // DMA instructions per wavefront and block
+constexpr int CH_VM = 8 + CH_DMA;                  // vector memory instructions per wavefront and block
+
+template <int OUT>
+__device__ __forceinline__ void ch_wait(int ahead) {
+  if (ahead >= 2) gemm::wait_vm<2 * OUT>();
+  else if (ahead == 1) gemm::wait_vm<OUT>();
+  else gemm::wait_vm<0>();
+}
+
+// One range of CH_W chains from c0 (< n).
+__device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c0, int n) {
+  const int lane = gemm::lane_here(), wave = gemm::opaque((int)(threadIdx.x / WAVE));
+  const int i = c0 + (int)threadIdx.x;
+  const bool live = i < n;
+  const int g = a.ch_g[live ? i : c0], e = a.ch_e[live ? i : c0];
+  const int H = gemm::opaque(a.H), nb = H / CH_K;
+  const uint32_t ring0 = (uint32_t)gemm::opaque((int)gemm::lds_u32(ring));
+  uint32_t wo[CH_DMA];
+#pragma unroll
+  for (int j = 0; j < CH_DMA; ++j) {
+    const int row = (wave * CH_DMA + j) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7);
+    wo[j] = (uint32_t)(min(row, a.E - 1) * H * 2 + c * 16);
   }
-  __builtin_amdgcn_wave_barrier();
+  const char* wb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.wgt));
+  const u32x4_t* xr = reinterpret_cast<const u32x4_t*>(a.x + (size_t)g * H);
+  // block b: LDS stage b % CH_P, x register set b % CH_P
+  u32x4_t xv[CH_P][8];
+  auto issue = [&](int b, u32x4_t (&dst)[8]) {
+    const uint32_t st = ring0 + (uint32_t)((b % CH_P) * (CH_E * 2 * CH_K));
+#pragma unroll
+    for (int j = 0; j < CH_DMA; ++j) gemm::dma16(wb + (size_t)b * (2 * CH_K), wo[j], st + (wave * CH_DMA + j) * 1024);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dst[q] = xr[b * 8 + q];
+  };
+  float acc = 0.0f;
+  const int wrow = e * (2 * CH_K), wsw = e & 7;
+  // block b: wait for its loads (blocks b + 1 and b + 2 may still be in
+  // flight), then, past the barrier that every wavefront reaches only after
+  // adding block b - 1, refill that block's stage and register set with
+  // block b + 3, and add block b
+  auto step = [&](int b, const u32x4_t (&xs)[8], u32x4_t (&refill)[8]) {
+    ch_wait<CH_VM>(min(CH_P - 2, nb - 1 - b));
+    __builtin_amdgcn_s_barrier();
+    gemm::compiler_fence();
+    if (b + CH_P - 1 < nb) issue(b + CH_P - 1, refill);
+    const char* st = ring + (b % CH_P) * (CH_E * 2 * CH_K) + wrow;
+    u32x4_t wv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) wv[q] = *reinterpret_cast<const u32x4_t*>(st + ((q ^ wsw) << 4));
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        acc = __builtin_fmaf(bf16_lo(xs[q][r]), bf16_lo(wv[q][r]), acc);
+        acc = __builtin_fmaf(bf16_hi(xs[q][r]), bf16_hi(wv[q][r]), acc);
+      }
+  };
+  if (0 < nb) issue(0, xv[0]);
+  if (1 < nb) issue(1, xv[1]);
+  if (2 < nb) issue(2, xv[2]);
+  for (int b = 0; b < nb; b += CH_P) {
+    step(b, xv[0], xv[3]);
+    if (b + 1 >= nb) break;
+    step(b + 1, xv[1], xv[0]);
+    if (b + 2 >= nb) break;
+    step(b + 2, xv[2], xv[1]);
+    if (b + 3 >= nb) break;
+    step(b + 3, xv[3], xv[2]);
+  }
+  if (live) a.ch_l[i] = a.bias ? acc + a.bias[e] : acc;
+  // the next range refills every stage
+  __builtin_amdgcn_s_barrier();
+  gemm::compiler_fence();
+}
+
+// Persistent over the ranges of CH_W chains (the chain count is known only
+// on the device).
+__global__ void __launch_bounds__(CH_W) gate_chain_staged_kernel(GateArgs a) {
+  static_assert(CH_P == 4 && CH_E % (8 * (CH_W / WAVE)) == 0, "chain staging geometry");
+  __shared__ __attribute__((aligned(1024))) char ring[CH_P * CH_E * 2 * CH_K];
+  const int n = a.stats[ST_CANDS];
+  for (int c0 = blockIdx.x * CH_W; c0 < n; c0 += gridDim.x * CH_W) chain_range(a, ring, c0, n);
+}
+
+// top-k of the candidates' defined logits (descending, equal logits ->
+// smaller id), one lane per token keeping a sorted list of the k best, then
+// the renormalised softmax weights of the chosen experts: exp(l_j - m) over
+// their sum (the normaliser over all experts cancels in the renormalisation,
+// so it is not formed)
+template <int EPL>
+__global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a) {
+  const int g = blockIdx.x * NTH + threadIdx.x;
+  if (g >= a.T) return;
+  const int tb = a.tok_base[g], tn = a.tok_n[g];
   float tv[MAX_TOPK];
   int ti[MAX_TOPK];
-  for (int r = 0; r < a.k; ++r) {
-    float v = -INFINITY;
-    int e = 1 << 30;
-    for (int c = gl; c < tn; c += GG) {
-      const int ce = a.ch_e[tb + c];
-      const float cv = a.ch_l[tb + c];
-      bool taken = false;
-      for (int q = 0; q < r; ++q) taken |= ti[q] == ce;
-      if (!taken && better(cv, ce, v, e)) { v = cv; e = ce; }
+#pragma unroll
+  for (int j = 0; j < MAX_TOPK; ++j) { tv[j] = -INFINITY; ti[j] = 1 << 30; }
+  for (int c = 0; c < tn; ++c) {
+    float v = a.ch_l[tb + c];
+    int e = a.ch_e[tb + c];
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) {
+      if (better(v, e, tv[j], ti[j])) {
+        const float ov = tv[j];
+        const int oe = ti[j];
+        tv[j] = v;
+        ti[j] = e;
+        v = ov;
+        e = oe;
+      }
     }
-    group_argmax(v, e);
-    tv[r] = v;
-    ti[r] = e;
   }
   const float m = tv[0];
-  const float xn = a.xn[gs];
-  float z = 0.0f;
+  float p[MAX_TOPK];
+  float ps = 0.0f;
 #pragma unroll
-  for (int i = 0; i < GEPL; ++i) {
-    const int e = gl + GG * i;
-    if (e < a.E && !((cmask[grp][e >> 5] >> (e & 31)) & 1u)) {
-      float l, d;
-      interval(a, gs, e, xn, l, d);
-      z += expf(l - m);
-    }
-  }
-  for (int c = gl; c < tn; c += GG) z += expf(a.ch_l[tb + c] - m);
+  for (int j = 0; j < MAX_TOPK; ++j)
+    if (j < a.k) { p[j] = expf(tv[j] - m); ps += p[j]; }
 #pragma unroll
-  for (int d = GG / 2; d > 0; d >>= 1) z += __shfl_xor(z, d, WAVE);
-  if (gl == 0 && valid) {
-    float p[MAX_TOPK];
-    float ps = 0.0f;
-    for (int j = 0; j < a.k; ++j) { p[j] = expf(tv[j] - m) / z; ps += p[j]; }
-    for (int j = 0; j < a.k; ++j) {
+  for (int j = 0; j < MAX_TOPK; ++j)
+    if (j < a.k) {
       a.topk_idx[(size_t)g * a.k + j] = ti[j];
       a.topk_w[(size_t)g * a.k + j] = p[j] / ps;
     }
-  }
 }
+
+template __global__ void gate_final_kernel<1>(GateArgs);
+template __global__ void gate_final_kernel<2>(GateArgs);
+template __global__ void gate_final_kernel<4>(GateArgs);
+template __global__ void gate_final_kernel<8>(GateArgs);
+template __global__ void gate_final_kernel<32>(GateArgs);
 
 // ---------------------------------------------------------------------------
 // Routing tables.  A pair (g, j) is local when id = topk_idx[g,j] is in
@@ -547,38 +1037,82 @@ __global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
   if (tid == 0) a.blk_bad[blockIdx.x] = nbad;
 }
 
-__global__ void __launch_bounds__(NTH) tab_scan_kernel(TableArgs a) {
+// Expert offsets and each table block's offset within every expert: one
+// wavefront per expert scans the block counts 64 at a time.  Also clears
+// the unique-token counts (tab_perm adds to them) and writes the chunk
+// offsets that need no search (chunk 0 starts at the expert's first slot,
+// chunk K ends at its last).
+__global__ void __launch_bounds__(TAB_SCAN_THREADS) tab_scan_kernel(TableArgs a) {
+  constexpr int NW = TAB_SCAN_THREADS / WAVE;
   __shared__ int tot[MAX_SEG];
-  const int tid = threadIdx.x;
-  for (int le = tid; le < a.El; le += NTH) {
-    int run = 0;
-    for (int b = 0; b < a.nblk; ++b) {
-      int c = a.blk_cnt[(size_t)b * a.El + le];
-      a.blk_off[(size_t)b * a.El + le] = run;
-      run += c;
+  __shared__ int badw[NW];
+  __shared__ int offs[MAX_SEG + 1];
+  const int tid = threadIdx.x, lane = tid & (WAVE - 1), wave = tid / WAVE;
+  for (int le = wave; le < a.El; le += NW) {
+    int carry = 0;
+    for (int b0 = 0; b0 < a.nblk; b0 += WAVE) {
+      const int b = b0 + lane;
+      const int c = b < a.nblk ? a.blk_cnt[(size_t)b * a.El + le] : 0;
+      int x = c;
+#pragma unroll
+      for (int d = 1; d < WAVE; d <<= 1) {
+        const int y = __shfl_up(x, d, WAVE);
+        if (lane >= d) x += y;
+      }
+      if (b < a.nblk) a.blk_off[(size_t)b * a.El + le] = carry + x - c;
+      carry += __shfl(x, WAVE - 1, WAVE);
     }
-    tot[le] = run;
+    if (lane == 0) tot[le] = carry;
   }
+  int bad = 0;
+  for (int b = tid; b < a.nblk; b += TAB_SCAN_THREADS) bad += a.blk_bad[b];
+#pragma unroll
+  for (int d = WAVE / 2; d > 0; d >>= 1) bad += __shfl_xor(bad, d, WAVE);
+  if (lane == 0) badw[wave] = bad;
+  for (int r = tid; r < a.R; r += TAB_SCAN_THREADS) a.uniq[r] = 0;
   __syncthreads();
   if (tid == 0) {
     int s = 0;
-    for (int le = 0; le < a.El; ++le) { a.off[le] = s; s += tot[le]; }
+    for (int le = 0; le < a.El; ++le) { offs[le] = s; a.off[le] = s; s += tot[le]; }
+    offs[a.El] = s;
     a.off[a.El] = s;
     // the table builder's stats words: the bad-id count here, the rest in
     // tab_finalize (words it does not write stay zero)
-    int bad = 0;
-    for (int b = 0; b < a.nblk; ++b) bad += a.blk_bad[b];
-    for (int w = 0; w < ST_CANDS; ++w) a.stats[w] = w == ST_BADIDS ? bad : 0;
+    int nb = 0;
+    for (int w = 0; w < NW; ++w) nb += badw[w];
+    for (int w = 0; w < ST_CANDS; ++w) a.stats[w] = w == ST_BADIDS ? nb : 0;
+  }
+  __syncthreads();
+  for (int v = tid; v < KOPT * a.El * SUBW; v += TAB_SCAN_THREADS) {
+    const int ki = v / (a.El * SUBW), le = (v / SUBW) % a.El, q = v % SUBW, K = kopt_value(ki);
+    // an inner boundary ceil(q T / K) at T (fewer tokens than chunks) is in
+    // no table block: every slot of the expert lies before it
+    if (q == 0) a.sub_off[v] = offs[le];
+    else if (q == K || (q < K && ((long long)q * a.T + K - 1) / K >= a.T)) a.sub_off[v] = offs[le + 1];
+    else if (q > K) a.sub_off[v] = 0;
+  }
+  for (int v = tid; v < a.El; v += TAB_SCAN_THREADS) {
+    a.rbnd[v * (a.R + 1)] = offs[v];
+    a.rbnd[v * (a.R + 1) + a.R] = offs[v + 1];
   }
 }
 
+// Slots, inverse and first slots by wavefront ballots (ranks within a
+// block, ordered by token), unique tokens per rank, and the first slot of
+// every expert at or after each rank boundary and each inner chunk boundary
+// that falls in this block: the expert's offset, plus the block's offset in
+// it, plus its selections in the block before the boundary token.
 __global__ void __launch_bounds__(NTH) tab_perm_kernel(TableArgs a) {
-  __shared__ int wc[NTH / WAVE][MAX_SEG];
+  constexpr int NW = NTH / WAVE;
+  __shared__ int wc[NW][MAX_SEG];
+  __shared__ uint64_t mk[NW][MAX_SEG];
+  __shared__ int uq[64];
   const int tid = threadIdx.x;
   const int lane = tid & (WAVE - 1);
   const int wave = tid / WAVE;
   const int g = blockIdx.x * TB + tid;
   const bool valid = g < a.T;
+  for (int r = tid; r < a.R; r += NTH) uq[r] = 0;
 
   int le_j[MAX_TOPK], r_j[MAX_TOPK];
   int ids[MAX_TOPK];
@@ -601,48 +1135,60 @@ __global__ void __launch_bounds__(NTH) tab_perm_kernel(TableArgs a) {
       for (int j = 0; j < MAX_TOPK; ++j)
         if (le_j[j] == le) r_j[j] = rank;
     }
-    if (lane == 0) wc[wave][le] = __popcll(m);
+    if (lane == 0) {
+      wc[wave][le] = __popcll(m);
+      mk[wave][le] = m;
+    }
   }
   __syncthreads();
-  if (!valid) return;
-  int first = -1, first_le = MAX_SEG;
-  for (int j = 0; j < a.k; ++j) {
-    int le = le_j[j];
-    int s = -1;
-    if (le >= 0) {
-      int pre = 0;
-      for (int w = 0; w < wave; ++w) pre += wc[w][le];
-      s = a.off[le] + a.blk_off[(size_t)blockIdx.x * a.El + le] + pre + r_j[j];
-      a.inv[s] = g * a.k + j;
-      if (le < first_le) { first_le = le; first = s; }
+  // boundaries: rank r*Tr (0 < r < R), then the inner chunk boundaries
+  // ceil(q*T/K) (0 < q < K) of K = 2, 4, 8; chunk(g) = floor(g*K/T) >= q
+  // exactly when g >= ceil(q*T/K)
+  {
+    const int t0 = blockIdx.x * TB, t1 = min(a.T, t0 + TB);
+    const int nrb = a.R - 1, nbnd = nrb + 1 + 3 + 7;
+    for (int v = tid; v < nbnd * a.El; v += NTH) {
+      const int bi = v / a.El, le = v % a.El;
+      long long b;
+      int ki = 0, q = 0;
+      if (bi < nrb) {
+        b = (long long)(bi + 1) * a.Tr;
+      } else {
+        const int c = bi - nrb;  // 0: K = 2, q = 1; 1..3: K = 4, q = 1..3; 4..10: K = 8, q = 1..7
+        ki = c < 1 ? 1 : (c < 4 ? 2 : 3);
+        const int K = kopt_value(ki);
+        q = c - (ki == 1 ? 0 : ki == 2 ? 1 : 4) + 1;
+        b = ((long long)q * a.T + K - 1) / K;
+      }
+      if (b < t0 || b >= t1) continue;
+      const int p = (int)(b - t0), pw = p / WAVE, pl = p % WAVE;
+      int cnt = a.off[le] + a.blk_off[(size_t)blockIdx.x * a.El + le];
+      for (int w = 0; w < pw; ++w) cnt += wc[w][le];
+      cnt += __popcll(mk[pw][le] & (pl == 0 ? 0ull : (~0ull >> (64 - pl))));
+      if (bi < nrb) a.rbnd[le * (a.R + 1) + bi + 1] = cnt;
+      else a.sub_off[(ki * a.El + le) * SUBW + q] = cnt;
     }
-    a.slot[(size_t)g * a.k + j] = s;
   }
-  a.first_slot[g] = first;
-}
-
-// Lower bounds in an expert's segment of slots (tokens ascending): the first
-// slot of expert le whose token is >= b.  The workgroup first stages the
-// token of every STRIDE-th slot in LDS (samp); a search narrows to one
-// window of STRIDE slots there and finishes with a binary search of
-// log2(STRIDE) global reads.
-constexpr int FIN_SAMP = 4096;
-__device__ inline int slot_token(const TableArgs& a, int p) { return a.inv[p] / a.k; }
-__device__ inline int seg_lower_bound(const TableArgs& a, const int* samp, int stride, int le, long long b) {
-  int lo = a.off[le], hi = a.off[le + 1];
-  int jlo = (lo + stride - 1) / stride, jhi = (hi + stride - 1) / stride;  // samples at slots in [lo, hi)
-  int j0 = jlo, j1 = jhi;
-  while (j0 < j1) {  // first sample whose token is >= b
-    const int mid = (j0 + j1) >> 1;
-    if ((long long)samp[mid] < b) j0 = mid + 1; else j1 = mid;
+  int first = -1, first_le = MAX_SEG;
+  if (valid) {
+    for (int j = 0; j < a.k; ++j) {
+      int le = le_j[j];
+      int s = -1;
+      if (le >= 0) {
+        int pre = 0;
+        for (int w = 0; w < wave; ++w) pre += wc[w][le];
+        s = a.off[le] + a.blk_off[(size_t)blockIdx.x * a.El + le] + pre + r_j[j];
+        a.inv[s] = g * a.k + j;
+        if (le < first_le) { first_le = le; first = s; }
+      }
+      a.slot[(size_t)g * a.k + j] = s;
+    }
+    a.first_slot[g] = first;
+    if (first >= 0) atomicAdd(&uq[g / a.Tr], 1);
   }
-  if (j0 > jlo) lo = (j0 - 1) * stride + 1;  // the sample before has a token < b
-  if (j0 < jhi) hi = j0 * stride;            // this sample has a token >= b
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if ((long long)slot_token(a, mid) < b) lo = mid + 1; else hi = mid;
-  }
-  return lo;
+  __syncthreads();
+  for (int r = tid; r < a.R; r += NTH)
+    if (uq[r]) atomicAdd(&a.uniq[r], uq[r]);
 }
 
 // Rows of segment seg (local experts, then shared experts) in chunk q of
@@ -658,50 +1204,23 @@ __device__ inline int seg_chunk_rows(const TableArgs& a, const int* so, int ki, 
   return max(0, t1 - t0);
 }
 
-// One workgroup.  Lower bounds at the rank boundaries (per-(expert, rank)
-// counts) and at the chunk boundaries of every chunk option (sub_off) form
-// one item space, one search per item and thread; the row map and the tile
-// counts of the cost model are then taken from the workgroup's copy of
-// sub_off.
+// One workgroup: per-(expert, rank) counts from the rank-boundary slots,
+// the row map and the tile counts of the cost model from the chunk offsets,
+// and the stats words.
 __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
-  __shared__ int uq[64];
   __shared__ int ntk[KOPT];
-  __shared__ int samp[FIN_SAMP];
-  __shared__ int rb[MAX_EL * 65];              // [El][R + 1] lower bounds at rank boundaries
+  __shared__ int xl_s;
   __shared__ int so_l[KOPT * MAX_EL * SUBW];   // this workgroup's copy of sub_off
   const int tid = threadIdx.x;
-  const int X = a.off[a.El];
-  int stride = 64;
-  while ((X + stride - 1) / stride > FIN_SAMP) stride *= 2;
-  for (int r = tid; r < a.R; r += NTH) uq[r] = 0;
   if (tid < KOPT) ntk[tid] = 0;
-  for (int j = tid; j * stride < X; j += NTH) samp[j] = slot_token(a, j * stride);
-  __syncthreads();
-  // unique tokens per rank (tokens with at least one local pair)
-  for (int g = tid; g < a.T; g += NTH)
-    if (a.first_slot[g] >= 0) atomicAdd(&uq[g / a.Tr], 1);
-  const int n_rank = a.El * (a.R + 1), n_sub = KOPT * a.El * SUBW;
-  for (int v = tid; v < n_rank + n_sub; v += NTH) {
-    if (v < n_rank) {
-      // rank r owns tokens [r*Tr, (r+1)*Tr)
-      const int le = v / (a.R + 1), r = v % (a.R + 1);
-      rb[v] = seg_lower_bound(a, samp, stride, le, (long long)r * a.Tr);
-    } else {
-      // chunk offsets: chunk(g) = floor(g*K/T) >= q  <=>  g >= ceil(q*T/K)
-      const int w = v - n_rank;
-      const int ki = w / (a.El * SUBW), rem = w % (a.El * SUBW);
-      const int le = rem / SUBW, q = rem % SUBW;
-      const int K = kopt_value(ki);
-      int val = 0;
-      if (q <= K) val = seg_lower_bound(a, samp, stride, le, ((long long)q * a.T + K - 1) / K);
-      a.sub_off[w] = val;
-      so_l[w] = val;
-    }
-  }
+  if (tid == 0) xl_s = 0;
+  for (int v = tid; v < KOPT * a.El * SUBW; v += NTH) so_l[v] = a.sub_off[v];
   __syncthreads();
   for (int v = tid; v < a.El * a.R; v += NTH) {
     const int le = v / a.R, r = v % a.R;
-    a.cnt_rank[v] = rb[le * (a.R + 1) + r + 1] - rb[le * (a.R + 1) + r];
+    const int c = a.rbnd[le * (a.R + 1) + r + 1] - a.rbnd[le * (a.R + 1) + r];
+    a.cnt_rank[v] = c;
+    if (r == 0) atomicAdd(&xl_s, c);
   }
   // The row map (common.h): for each chunk option, the (segment, chunk)
   // pairs in segment-major order, each taking its rows rounded up to a
@@ -741,16 +1260,14 @@ __global__ void __launch_bounds__(NTH) tab_finalize_kernel(TableArgs a) {
     if (part) atomicAdd(&ntk[ki], part);
   }
   __syncthreads();
-  for (int r = tid; r < a.R; r += NTH) a.uniq[r] = uq[r];
   if (tid == 0) {
-    int xl = 0;
-    for (int le = 0; le < a.El; ++le) xl += rb[le * (a.R + 1) + 1] - rb[le * (a.R + 1)];
+    const int X = a.off[a.El];
     int uin = 0;
-    for (int r = 1; r < a.R; ++r) uin += uq[r];
+    for (int r = 1; r < a.R; ++r) uin += a.uniq[r];
     a.stats[ST_X] = X;
-    a.stats[ST_XLOCAL] = xl;
-    a.stats[ST_XIN] = X - xl;
-    a.stats[ST_ULOCAL] = uq[0];
+    a.stats[ST_XLOCAL] = xl_s;
+    a.stats[ST_XIN] = X - xl_s;
+    a.stats[ST_ULOCAL] = a.uniq[0];
     a.stats[ST_UIN] = uin;
     for (int ki = 0; ki < KOPT; ++ki) a.stats[ST_NTK + ki] = ntk[ki];
   }
