@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--reps", type=int, default=5, help="stack runs per mode and round")
     ap.add_argument("--flush-mib", type=int, default=512, help="scratch written before each flushed launch")
     ap.add_argument("--no-trace", action="store_true")
+    ap.add_argument("--stack", action="store_true",
+                    help="run the layers of a timed step in one stacked launch (default: one launch per layer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2, help="oracle rows per rank and layer, single-thread leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -133,6 +135,12 @@ class Stack:
         d = self.L[i]
         d["layer"].forward(self.x, d["idx"], d["w"], d["y"], mode, stream=stream)
 
+    def forward_stacked(self, B, mode, stream):
+        """Every layer in one persistent launch (moe_forward_stack)."""
+        B.moe_forward_stack([d["layer"].h for d in self.L], self.x, [d["idx"] for d in self.L],
+                            [d["w"] for d in self.L], [d["layer"].packed for d in self.L],
+                            [d["y"] for d in self.L], B.MODES[mode], stream=stream)
+
     def check(self, B, stream):
         for d in self.L:
             st = B.moe_sync_status(d["layer"].h, stream)
@@ -163,6 +171,18 @@ def time_stack(stack, mode, reps, stream):
             ev[r][i][1].record(stream)
     torch.cuda.synchronize()
     return [[ev[r][i][0].elapsed_time(ev[r][i][1]) * 1e3 for r in range(reps)] for i in range(n)]
+
+
+def time_stacked(B, stack, reps, stream):
+    """Back-to-back stacked launches: the duration (us) of each."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record(stream)
+        stack.forward_stacked(B, "dynamic", stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 for a, b in ev]
 
 
 def time_flushed(stack, reps, stream, flush):
@@ -216,7 +236,11 @@ def traced_phases(B, stack, i, stream, stats, flops):
     comb_span = float((us(comb["t2"]).max() - us(comb["t1"]).min())) if len(comb) else float("nan")
     per_cu_peak = PEAK_BF16_TFLOPS / 256.0
     tl = TL.metrics(tr)
+    gemm_end = float(us(tiles["t2"]).max()) if len(tiles) else float("nan")
     return {
+        "first_tile_start_us": float(us(tiles["t1"]).min()) if len(tiles) else None,
+        "last_tile_end_us": gemm_end,
+        "tail_after_gemm_us": span - gemm_end,
         "traced_layer_us": span,
         "dispatch_us": disp_end,
         "dispatch_hbm_gbs": disp_bytes / (disp_end * 1e-6) / 1e9,
@@ -231,6 +255,30 @@ def traced_phases(B, stack, i, stream, stats, flops):
         "overlap_of_movement": tl["overlap_of_mov"],
         "prologue_us": tl["prologue_us"],
     }
+
+
+def serial_stages(B, stack, i, stream, reps=3):
+    """The serial mode's four kernels timed one at a time on every worker
+    (moe_run_stages: a stage reads what the earlier ones wrote, so this is
+    timing only; the forward before it leaves every stage's inputs in place)."""
+    import numpy as np
+    import torch
+    d = stack.L[i]
+    n = torch.cuda.get_device_properties(0).multi_processor_count
+    out = {}
+    for name, mask in (("dispatch", 1), ("gemm0", 2), ("gemm1", 4), ("combine", 8)):
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            B.moe_run_stages(d["layer"].h, stack.x, d["idx"], d["w"], d["layer"].packed, d["y"], mask, n, 1, stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        out[name] = float(np.median(ts))
+    stack.forward(i, "dynamic", stream)  # leaves y and the tables as the timed forwards did
+    torch.cuda.synchronize()
+    return out
 
 
 def layer_stats(stack, i):
@@ -327,29 +375,39 @@ def y_check(stack, samples, ref):
 
 
 def measure_stack(B, stack, args, stream, flush, trace: bool):
-    """Timed steps, then the baselines, flushed launches and traces."""
+    """Timed steps, then the baselines, flushed launches and traces.  A step
+    routes every layer and runs the MoE layers, one launch per layer (or, with
+    --stack, all of them in one stacked launch)."""
     import numpy as np
     import torch
     n = len(stack.L)
+    stacked = n > 1 and args.stack
+
+    def layers_forward():
+        if stacked:
+            stack.forward_stacked(B, "dynamic", stream)
+        else:
+            for i in range(n):
+                stack.forward(i, "dynamic", stream)
+
     for _ in range(args.warmup):
         for i in range(n):
             stack.route(i, stream)
-            stack.forward(i, "dynamic", stream)
+        layers_forward()
     torch.cuda.synchronize()
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-          for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         for i in range(n):
             stack.route(i, stream)
-            ev[s][i][0].record(stream)
-            stack.forward(i, "dynamic", stream)
-            ev[s][i][1].record(stream)
+        ev[s][0].record(stream)
+        layers_forward()
+        ev[s][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     stack.check(B, stream)
-    fwd_us = [[ev[s][i][0].elapsed_time(ev[s][i][1]) * 1e3 for s in range(args.steps)] for i in range(n)]
+    moe_us = [a.elapsed_time(b) * 1e3 for a, b in ev]  # the MoE layers of a step (one launch or n)
     log(f"{stack.shape.name}: timed steps done ({wall * 1e3 / args.steps:.2f} ms per step)")
     plans = [B.moe_get_plan(d["layer"].h, stream) for d in stack.L]
     stats = [layer_stats(stack, i) for i in range(n)]
@@ -364,48 +422,56 @@ def measure_stack(B, stack, args, stream, flush, trace: bool):
         b.record(stream)
         torch.cuda.synchronize()
         route_us.append(a.elapsed_time(b) * 1e3 / args.steps)
-    # baselines next to the dynamic mode, timed the same way (back-to-back
-    # stacks on the same routing) in interleaved rounds
+    # one launch per layer in each mode, and the stacked launch, timed the
+    # same way (back to back on the same routing) in interleaved rounds
     modes = ["dynamic"] + [m for m in args.modes.split(",") if m]
     runs = {m: [[] for _ in range(n)] for m in modes}
+    stacked_runs = []
     for _ in range(args.rounds):
         for m in modes:
             t = time_stack(stack, m, args.reps, stream)
             for i in range(n):
                 runs[m][i] += t[i]
+        if n > 1:
+            stacked_runs += time_stacked(B, stack, args.reps, stream)
     stack.check(B, stream)
     log(f"{stack.shape.name}: baselines done ({args.rounds} interleaved rounds)")
     fl = time_flushed(stack, args.reps, stream, flush) if flush is not None else None
     layers = []
     for i in range(n):
         p = plans[i]
+        dyn = runs["dynamic"][i]
         rec = {"layer": stack.ids[i], "plan": {"c": p.c, "K": p.K, "n_steal": p.n_steal, "final_all": p.final_all,
                                                 "t_pred_us": p.t_pred_s * 1e6},
                "local_pairs": int(stats[i][0]), "gflop": flops[i] / 1e9,
                "route_exact_chains": int(stats[i][8]),
-               "layer_us": float(np.median(fwd_us[i])),
-               "layer_us_p10_p90": [float(np.percentile(fwd_us[i], 10)), float(np.percentile(fwd_us[i], 90))],
+               "layer_us": float(np.median(dyn)),
+               "layer_us_p10_p90": [float(np.percentile(dyn, 10)), float(np.percentile(dyn, 90))],
                "layer_us_flushed": float(np.median(fl[i])) if fl else None,
                "route_us": route_us[i],
-               "tflops": flops[i] / (float(np.mean(fwd_us[i])) * 1e-6) / 1e12}
-        dyn = float(np.median(runs["dynamic"][i]))
-        rec["baselines"] = {"dynamic_same_timing_us": dyn}
+               "tflops": flops[i] / (float(np.median(dyn)) * 1e-6) / 1e12}
+        rec["baselines"] = {}
         for m in modes[1:]:
             med = float(np.median(runs[m][i]))
-            rec["baselines"][m] = {"layer_us": med, "dynamic_speedup": med / dyn}
+            rec["baselines"][m] = {"layer_us": med, "dynamic_speedup": med / rec["layer_us"]}
         if trace:
             rec["phases"] = traced_phases(B, stack, i, stream, stats[i], flops[i])
+            rec["serial_stages_us"] = serial_stages(B, stack, i, stream)
         layers.append(rec)
     tot = {m: float(sum(np.median(runs[m][i]) for i in range(n))) for m in modes}
     summary = {
         "steps": args.steps, "ms_per_step": wall * 1e3 / args.steps,
-        "stack_layer_us_total": float(sum(np.median(f) for f in fwd_us)),
-        "stack_route_us_total": float(sum(route_us)),
+        "moe_us_per_step": float(np.median(moe_us)),
+        "moe_launches_per_step": 1 if stacked else n,
         "stack_flops": float(sum(flops)),
-        "mean_launch_us": float(np.mean([np.mean(f) for f in fwd_us])),
-        "baseline_totals_us": tot,
+        "stack_route_us_total": float(sum(route_us)),
+        "one_launch_per_layer_us_total": tot,
         "dynamic_speedup_vs": {m: tot[m] / tot["dynamic"] for m in modes[1:]},
     }
+    if stacked_runs:
+        st_med = float(np.median(stacked_runs))
+        summary["stacked_launch_us"] = st_med
+        summary["stacked_speedup_vs"] = {("one_launch_per_layer_" + m): tot[m] / st_med for m in modes}
     return summary, layers
 
 
@@ -433,8 +499,12 @@ def main():
     summary, layers = measure_stack(B, stack, args, stream, flush, trace=not args.no_trace)
 
     n = len(ids)
-    flops_per_launch = summary["stack_flops"] / n
-    achieved = flops_per_launch / (summary["mean_launch_us"] * 1e-6) / 1e12
+    # the dominant kernel: the stacked megakernel (one launch holds every
+    # layer), else the megakernel of the one layer
+    launches = summary["moe_launches_per_step"]
+    flops_per_launch = summary["stack_flops"] / launches
+    achieved = flops_per_launch / (summary["moe_us_per_step"] / launches * 1e-6) / 1e12
+    kernel = "moe_megakernel_stack" if launches == 1 and n > 1 else "moe_megakernel"
     out = {
         "metric": METRIC,
         "value": shape.T / (summary["ms_per_step"] * 1e-3),
@@ -452,15 +522,16 @@ def main():
         "config": {"workload": f"{shape.name}: {n}-layer stack of EP=4 rank shares, E={shape.n_experts} "
                                f"k={shape.top_k} H={shape.hidden} F={shape.ffn}, {shape.n_local_experts} local "
                                f"experts, {shape.n_src_ranks} ranks x {shape.tokens_per_rank} tokens; a step is "
-                               f"routing + MoE layer for every layer",
+                               f"the routing of every layer, then the MoE layers "
+                               f"({'in one stacked launch' if launches == 1 and n > 1 else 'one launch per layer'})",
                    "tokens": shape.T, "layers": ids},
-        "stack": {**summary, "stack_tokens_per_s_layers_only": shape.T / (summary["stack_layer_us_total"] * 1e-6)},
+        "stack": {**summary, "moe_tokens_per_s": shape.T / (summary["moe_us_per_step"] * 1e-6)},
         "layers": layers,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(shape.name),
-                     "kernel": "moe_megakernel", "flop_per_launch": flops_per_launch,
-                     "flop_per_unit": "6*H*F per routed (token, local expert) row and per shared-expert row; "
-                                      "per launch = the stack's flop / its launches"},
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(f"{shape.name}:{kernel}"),
+                     "kernel": kernel, "flop_per_launch": flops_per_launch,
+                     "flop_per_unit": "6*H*F per routed (token, local expert) row and per shared-expert row, "
+                                      "summed over the layers one launch holds"},
         "context": "paper: 2.89x geomean MoE-layer speedup on 4xH100 SXM, EP=4, BF16 - different hardware and "
                    "baselines, not a target",
     }

@@ -314,6 +314,30 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
                        const float* topk_w, const void* packed, uint16_t* y,
                        int32_t mode, const moe_plan* forced, void* stream);
 
+#define MOE_STACK_MAX 12
+
+/* Several MoE layers in one persistent megakernel launch (a stack of
+ * independent layers that share the tokens x but not their outputs, as the
+ * layers of one GPU's expert-parallel share are when each takes its own
+ * routing of the same batch).  layers[l]: the handle of layer l (each with its
+ * own workspace, tables built from topk_idx[l], and n_workers equal to layer
+ * 0's); packed[l], topk_idx[l], topk_w[l], y[l]: as in moe_forward for that
+ * layer (host arrays of device pointers).  Each layer's plan comes from its
+ * own prologue (section 3.3), or is `forced` (host, the same for every layer).
+ * A workgroup moves on to layer l + 1 as soon as it finds no more work to
+ * claim in layer l (section 4's dynamic claiming, across layers), so layer
+ * l + 1's dispatch and first GEMM tiles overlap layer l's last tiles and its
+ * combine; in every layer but the last, the final combine is left to that
+ * layer's movement workers while the compute workers go on to the next
+ * layer.  Results are those of moe_forward on each layer, bit for bit.
+ * mode: MOE_MODE_DYNAMIC or MOE_MODE_STATIC.  1 <= n_layers <= MOE_STACK_MAX,
+ * no handle twice.  The timeline trace is not recorded in a stacked launch.
+ * Errors: as moe_forward, per layer (device errors latch in each layer's
+ * error word). */
+moe_status moe_forward_stack(moe_handle* const* layers, int32_t n_layers, const uint16_t* x,
+                             const int32_t* const* topk_idx, const float* const* topk_w, const void* const* packed,
+                             uint16_t* const* y, int32_t mode, const moe_plan* forced, void* stream);
+
 /* Calibration of the cost model's hardware curves (BW(c), TFLOPS(N-c),
  * eff_chunk(K); Fig 4a/b, Fig 7a): runs the selected stages of the layer as
  * separate kernels on n_workers workgroups.  stages: bit 0 dispatch, bit 1

@@ -102,6 +102,8 @@ _SIGS = {
     "moe_route_topk_static": ([C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P], C.c_int),
     "moe_forward": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.POINTER(moe_plan), _P], C.c_int),
     "moe_run_stages": ([_H, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P], C.c_int),
+    "moe_forward_stack": ([C.POINTER(_H), C.c_int32, _P, C.POINTER(_P), C.POINTER(_P), C.POINTER(_P), C.POINTER(_P),
+                           C.c_int32, C.POINTER(moe_plan), _P], C.c_int),
     "moe_get_plan": ([_H, C.POINTER(moe_plan), _P], C.c_int),
     "moe_sync_status": ([_H, _P], C.c_int),
     "moe_plan_host": ([_H, C.c_double, C.c_double, C.c_double, C.POINTER(C.c_int64), C.POINTER(moe_plan)], C.c_int),
@@ -257,6 +259,18 @@ def moe_forward(h: int, x, topk_idx, topk_w, packed, y, mode: int = MOE_MODE_DYN
     _check("moe_forward", _lib.moe_forward(h, _ptr(x), _ptr(topk_idx), _ptr(topk_w), _ptr(packed), _ptr(y),
                                            int(mode), C.byref(forced) if forced is not None else None,
                                            _stream(stream)))
+
+
+def moe_forward_stack(handles, x, topk_idx, topk_w, packed, y, mode: int = MOE_MODE_DYNAMIC,
+                      forced: Optional[moe_plan] = None, stream=None) -> None:
+    """handles, topk_idx, topk_w, packed, y: one entry per layer."""
+    n = len(handles)
+    hs = (_H * n)(*handles)
+    arr = lambda ts: (_P * n)(*[_ptr(t) for t in ts])
+    _check("moe_forward_stack", _lib.moe_forward_stack(hs, n, _ptr(x), arr(topk_idx), arr(topk_w), arr(packed),
+                                                       arr(y), int(mode),
+                                                       C.byref(forced) if forced is not None else None,
+                                                       _stream(stream)))
 
 
 def moe_run_stages(h: int, x, topk_idx, topk_w, packed, y, stages: int, n_workers: int, K: int = 1,

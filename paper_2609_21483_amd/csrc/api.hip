@@ -158,6 +158,7 @@ struct moe_handle {
   long long* trace = nullptr;
   int trace_cap = 0, trace_rec0 = 0;
   bool resident_ok = false;  // the megakernel's N workgroups fit the GPU at once
+  bool stack_resident_ok = false;  // the same for the stacked megakernel
 };
 
 namespace {
@@ -358,6 +359,21 @@ TableArgs table_args(moe_handle* h, const int32_t* topk_idx) {
 
 
 namespace {
+// A persistent kernel's N workgroups wait on each other, so all of them must
+// be resident at once (checked once per handle and kernel).
+moe_status check_resident(moe_handle* h, const void* kernel, bool& ok) {
+  if (ok) return MOE_OK;
+  int dev = 0, cus = 0, per_cu = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, FNTH, 0));
+  if ((long long)cus * per_cu < h->N)
+    return fail(MOE_ERR_UNSUPPORTED, "n_workers = %d exceeds the %lld workgroups the GPU holds at once", h->N,
+                (long long)cus * per_cu);
+  ok = true;
+  return MOE_OK;
+}
+
 FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, const float* topk_w, const void* packed,
                  uint16_t* y, int32_t mode, const moe_plan* forced) {
   const moe_config& c = h->cfg;
@@ -419,6 +435,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.trace_cap = h->trace_cap;
   a.trace_rec0 = h->trace_rec0;
   a.serial_K = 1;
+  a.static_disp = 1;
   return a;
 }
 }  // namespace
@@ -702,21 +719,61 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
     // ordinary launch: on an otherwise idle GPU one workgroup lands on each
     // CU; a cooperative launch would hold it until all earlier work on the
     // device has drained (~20 us a layer).
-    if (!h->resident_ok) {
-      int dev = 0, cus = 0, per_cu = 0;
-      HIP_TRY(hipGetDevice(&dev));
-      HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-      HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&moe_megakernel),
-                                                           FNTH, 0));
-      if ((long long)cus * per_cu < h->N)
-        return fail(MOE_ERR_UNSUPPORTED, "n_workers = %d exceeds the %lld workgroups the GPU holds at once", h->N,
-                    (long long)cus * per_cu);
-      h->resident_ok = true;
-    }
+    st = check_resident(h, reinterpret_cast<const void*>(&moe_megakernel), h->resident_ok);
+    if (st != MOE_OK) return st;
     moe_megakernel<<<h->N, FNTH, 0, s>>>(a);
     HIP_TRY(hipGetLastError());
   }
   h->launch_seq++;
+  return MOE_OK;
+}
+
+moe_status moe_forward_stack(moe_handle* const* layers, int32_t n_layers, const uint16_t* x,
+                             const int32_t* const* topk_idx, const float* const* topk_w, const void* const* packed,
+                             uint16_t* const* y, int32_t mode, const moe_plan* forced, void* stream) {
+  if (!layers || !x || !topk_idx || !topk_w || !packed || !y) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
+  if (n_layers < 1 || n_layers > MOE_STACK_MAX)
+    return fail(MOE_ERR_INVALID_ARG, "n_layers must be in [1, %d]", MOE_STACK_MAX);
+  if (mode != MOE_MODE_DYNAMIC && mode != MOE_MODE_STATIC)
+    return fail(MOE_ERR_INVALID_ARG, "a stacked launch runs the megakernel modes only");
+  if (forced) {
+    if (forced->K != 1 && forced->K != 2 && forced->K != 4 && forced->K != 8)
+      return fail(MOE_ERR_INVALID_ARG, "forced K must be 1, 2, 4 or 8");
+    if (forced->n_steal < 0 || (forced->final_all != 0 && forced->final_all != 1))
+      return fail(MOE_ERR_INVALID_ARG, "forced n_steal must be >= 0 and final_all 0 or 1");
+  }
+  const int N = layers[0] ? layers[0]->N : 0;
+  for (int l = 0; l < n_layers; ++l) {
+    moe_handle* h = layers[l];
+    moe_status st = need_ws(h);
+    if (st != MOE_OK) return st;
+    if (h->N != N) return fail(MOE_ERR_INVALID_ARG, "layer %d has %d workers, layer 0 has %d", l, h->N, N);
+    if (!topk_idx[l] || !topk_w[l] || !packed[l] || !y[l])
+      return fail(MOE_ERR_INVALID_ARG, "NULL argument of layer %d", l);
+    for (int m = 0; m < l; ++m)
+      if (layers[m] == h) return fail(MOE_ERR_INVALID_ARG, "layer %d repeats the handle of layer %d", l, m);
+    if (h->tables_from != topk_idx[l])
+      return fail(MOE_ERR_STATE, "layer %d: routing tables were not built from its topk_idx", l);
+    if (forced && (forced->c < 1 || forced->c >= N)) return fail(MOE_ERR_INVALID_ARG, "forced c must be in [1, N-1]");
+  }
+  moe_status st = check_resident(layers[0], reinterpret_cast<const void*>(&moe_megakernel_stack),
+                                 layers[0]->stack_resident_ok);
+  if (st != MOE_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  StackArgs sa{};
+  sa.n = n_layers;
+  for (int l = 0; l < n_layers; ++l) {
+    FwdArgs& a = sa.layer[l];
+    a = fwd_args(layers[l], x, topk_idx[l], topk_w[l], packed[l], y[l], mode, forced);
+    // workers reach the later layers at different times: no dispatch unit
+    // is owned by arrival ticket there; no timeline trace in a stacked launch
+    a.static_disp = l == 0 ? 1 : 0;
+    a.stack_next = l + 1 < n_layers ? 1 : 0;
+    a.trace = nullptr;
+  }
+  moe_megakernel_stack<<<N, FNTH, 0, s>>>(sa);
+  HIP_TRY(hipGetLastError());
+  for (int l = 0; l < n_layers; ++l) layers[l]->launch_seq++;
   return MOE_OK;
 }
 

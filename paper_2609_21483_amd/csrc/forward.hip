@@ -1005,10 +1005,8 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
 // timeout, so workers that cannot start (the CUs held by other work) turn
 // into MOE_ERR_TIMEOUT, never a hang.
 // ===========================================================================
-__global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
-  __shared__ Sched S;
-  __shared__ Scratch W;
-  __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
+// One layer, run by this workgroup.
+__device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& W, char* ring) {
   const int tid = threadIdx.x;
   const uint64_t t_entry = a.trace ? now_ticks() : 0;
 
@@ -1037,7 +1035,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   if (tid < NWF) W.tcnt[tid] = 0;
   if (tid == 0) {
     W.ticket = W.bc[0];
-    S.disp0 = min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF);
+    S.disp0 = a.static_disp ? min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF) : 0;
   }
   __syncthreads();
   const int ticket = __builtin_amdgcn_readfirstlane(W.bc[0]);
@@ -1063,8 +1061,11 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   } else {
     ok = compute_tiles(a, S, W, ring, ticket, 1 << 30);
     // the final combine on every worker (section 4): once the compute queue
-    // is empty a compute worker joins the combine
-    if (ok && S.final_all) combine_claimed(a, S, W, ticket);
+    // is empty a compute worker joins the combine; in a stacked launch with a
+    // layer after this one it goes on to that layer's GEMMs instead, and this
+    // layer's movement workers combine meanwhile (on a few CUs a copy moves
+    // more bytes per CU than on all of them)
+    if (ok && S.final_all && !a.stack_next) combine_claimed(a, S, W, ticket);
   }
   if (a.trace) {
     __syncthreads();
@@ -1079,6 +1080,36 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
       hdr[3] = a.trace_rec0;
       hdr[0] = TRACE_MAGIC;
     }
+  }
+}
+
+__global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
+  __shared__ Sched S;
+  __shared__ Scratch W;
+  __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
+  mega_layer(a, S, W, ring);
+}
+
+// Several independent layers (they share x, not their outputs) in one
+// persistent launch: a workgroup moves on to layer l + 1 as soon as it finds
+// no more work to claim in layer l, so layer l + 1's dispatch and first GEMM
+// tiles run while layer l's last tiles and its combine finish.  Every item of
+// layer l is claimed by a workgroup still in layer l, and no wait depends on
+// a later layer, so every wait ends.
+// The layers' argument blocks are read in place from the kernel argument
+// segment (constant memory, scalar loads): indexing the by-value parameter
+// with the layer number would copy it to scratch.
+__global__ void __launch_bounds__(FNTH, 1) moe_megakernel_stack(StackArgs st) {
+  __shared__ Sched S;
+  __shared__ Scratch W;
+  __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
+  (void)st;
+  const __attribute__((address_space(4))) StackArgs* ka =
+      (const __attribute__((address_space(4))) StackArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int n = ka->n;
+  for (int l = 0; l < n; ++l) {
+    __syncthreads();  // the previous layer's LDS state is dead
+    mega_layer(*(const FwdArgs*)&ka->layer[l], S, W, ring);
   }
 }
 

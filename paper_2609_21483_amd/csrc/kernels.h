@@ -124,7 +124,19 @@ struct FwdArgs {
   long long timeout_ticks;  // per wait, 100 MHz ticks
   int inject_stall;         // test hook: every wait targets an unreachable value
   int serial_K;             // chunk tiling used by the separate-kernel GEMMs
+  int static_disp;          // megakernel: the first round of dispatch units is owned by arrival ticket
+  int stack_next;           // stacked launch: another layer follows, so compute workers go on to it
+                            // instead of joining this layer's final combine (its movement workers do it)
 };
+
+// Layers of one stacked megakernel launch, their argument blocks by value
+// (kernel arguments: read by scalar loads, like a single launch's).
+constexpr int STACK_MAX = MOE_STACK_MAX;
+struct StackArgs {
+  int n;
+  FwdArgs layer[STACK_MAX];
+};
+static_assert(sizeof(StackArgs) <= 4096, "the stacked launch's arguments fit the kernel argument segment");
 
 // ---- cost model (sections 3.1-3.3) ------------------------------------------
 // Evaluates T_total(c, K) of Eq 15 over the calibrated (c, K) grid, takes the
@@ -245,6 +257,7 @@ __global__ void zero_i32_kernel(int* p, int n);
 __global__ void pack_transpose_kernel(PackArgs a);
 __global__ void pack_pad_kernel(PadArgs a);
 __global__ void moe_megakernel(FwdArgs a);
+__global__ void moe_megakernel_stack(StackArgs st);
 __global__ void serial_dispatch_kernel(FwdArgs a);
 __global__ void serial_gemm0_kernel(FwdArgs a);
 __global__ void serial_gemm1_kernel(FwdArgs a);

@@ -8,7 +8,7 @@ compiler inserts one when a loop-invariant vector register was reloaded from
 scratch in front of the loop, which happens when other code keeps values live
 across the mainloop.  A scratch access inside the loop is a spill in the
 hottest code of the library.  Both are checked in every kernel that holds the
-mainloop (the megakernel and the serial GEMM kernels).
+mainloop (the megakernel, its stacked form and the serial GEMM kernels).
 """
 import os
 import re
@@ -55,7 +55,7 @@ def _mainloop_blocks(asm: str):
 
 def test_mainloop_keeps_its_dma_in_flight(tmp_path):
     blocks = list(_mainloop_blocks(_device_asm(tmp_path)))
-    for name in ("moe_megakernel", "serial_gemm0_kernel", "serial_gemm1_kernel"):
+    for name in ("moe_megakernelENS_7FwdArgs", "moe_megakernel_stack", "serial_gemm0_kernel", "serial_gemm1_kernel"):
         # one mainloop instance per count of active 32-row blocks (0..4), each
         # with that many MFMAs per 16-deep slice
         counts = {sum(i.startswith("v_mfma") for i in ins) for fn, _, ins in blocks if name in fn}
