@@ -335,6 +335,11 @@ __device__ __forceinline__ void dispatch_copy(const FwdArgs& a, Scratch& W, int 
         val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.x + (size_t)(g0 + act[t]) * H) + c);
       }
     }
+    // every load of the pass has landed: the stores below (a run-time number
+    // per vector) then issue back to back.  Without this drain the compiler
+    // cannot count the stores in flight between a load and its use, and
+    // waits for all of them (vmcnt counts stores too) before every vector.
+    gemm::wait_vm<0>();
 #pragma unroll
     for (int i = 0; i < VB; ++i) {
       const int v = v0 + i * WAVE;
@@ -462,7 +467,7 @@ __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& 
   }
 }
 
-__device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target);
+__device__ __forceinline__ bool wave_wait_all(const FwdArgs& a, const int* p, int target);
 
 // One wavefront combines nt <= ct tokens.  Each token has KS = k + S source
 // rows: its k routed slots (weight w, absent when the expert is not local)
@@ -470,6 +475,12 @@ __device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, in
 // 0).  They are summed in that order in fp32.  A source row is O (bf16).  KS
 // is a template constant so that every lane keeps about 16 row vectors in
 // flight.
+// Entries past a token's present rows (or past the unit) load from x with
+// weight 0 (x is finite and never written during a launch), so they add +0
+// and the loads of a pass are straight-line code that issues them all before
+// the first wait (a load under a per-lane branch is preceded by a full
+// drain).  They must not read O: a line of O loaded before its row tile is
+// published would sit stale in this CU's L1 for the unit that needs it.
 template <int KS>
 __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, const float* wt, int g0, int nt) {
   constexpr int P = KS >= 2 ? 16 / KS : 8;  // positions per lane per pass (~16 row vectors in flight)
@@ -488,25 +499,24 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
       for (int e = 0; e < 8; ++e) acc[i][e] = 0.0f;
     }
     u32x4_t o[P][KS];
+    float w[P][KS];
 #pragma unroll
     for (int i = 0; i < P; ++i)
 #pragma unroll
       for (int j = 0; j < KS; ++j) {
         const int s = tt[i] >= 0 ? sl[tt[i] * KS + j] : -1;
-        if (s >= 0) o[i][j] = *reinterpret_cast<const u32x4_t*>(a.O + (size_t)s * a.H + cc[i] * 8);
+        w[i][j] = s >= 0 ? wt[tt[i] * KS + j] : 0.0f;
+        o[i][j] = *reinterpret_cast<const u32x4_t*>((s >= 0 ? a.O + (size_t)s * a.H : a.x) + cc[i] * 8);
       }
 #pragma unroll
     for (int i = 0; i < P; ++i)
 #pragma unroll
-      for (int j = 0; j < KS; ++j) {
-        if (tt[i] < 0 || sl[tt[i] * KS + j] < 0) continue;
-        const float w = wt[tt[i] * KS + j];
+      for (int j = 0; j < KS; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[i][2 * q] += w * bf16_lo(o[i][j][q]);
-          acc[i][2 * q + 1] += w * bf16_hi(o[i][j][q]);
+          acc[i][2 * q] += w[i][j] * bf16_lo(o[i][j][q]);
+          acc[i][2 * q + 1] += w[i][j] * bf16_hi(o[i][j][q]);
         }
-      }
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       if (tt[i] < 0) continue;
@@ -521,7 +531,8 @@ __device__ __forceinline__ void combine_body(const FwdArgs& a, const int* sl, co
 
 // A wavefront combines tokens [g0, g0 + nt).  In the megakernel (S given) it
 // first waits until every GEMM1 column tile of each row tile holding one of
-// those tokens' source rows is done: one lane polls per distinct row tile.
+// those tokens' source rows is done: every lane with a source row polls its
+// row tile's counter, all in one vector load per round.
 // Returns false when the launch was aborted.  With tracing on, t_ready gets
 // the time the waits ended.
 __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S, Scratch& W, int g0, int nt,
@@ -573,14 +584,8 @@ __device__ __forceinline__ bool combine_tokens(const FwdArgs& a, const Sched* S,
     wt[t * kp + r] = w;
   }
   if (S) {
-    const int need = a.nt1;  // every column tile of the row tile (split ones reduced)
-    uint64_t pending = __builtin_amdgcn_ballot_w64(id >= 0);
-    while (pending) {
-      const int leader = __builtin_ctzll(pending);
-      const int tile = __builtin_amdgcn_readlane(id, leader);
-      pending &= ~__builtin_amdgcn_ballot_w64(id == tile);
-      if (!wave_wait_geq(a, &a.ctl[CTL_READY + (2 * a.mt_max + tile) * CTL_PAD], need)) return false;
-    }
+    // every column tile of the row tile (split ones reduced)
+    if (!wave_wait_all(a, id >= 0 ? &a.ctl[CTL_READY + (2 * a.mt_max + id) * CTL_PAD] : nullptr, a.nt1)) return false;
     if (a.trace) t_ready = now_ticks();
   }
   __builtin_amdgcn_wave_barrier();
@@ -973,12 +978,33 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
   return true;
 }
 
-// wavefront-level wait: lane 0 polls, the others follow
-__device__ __forceinline__ bool wave_wait_geq(const FwdArgs& a, const int* p, int target) {
+// wavefront-level wait on up to 64 counters at once: each lane with p set
+// waits for *p >= target, one vector load per round for all of them
+__device__ __forceinline__ bool wave_wait_all(const FwdArgs& a, const int* p, int target) {
   if (a.inject_stall) target += 1 << 30;
-  int ok = 1;
-  if (lane_id() == 0) ok = poll_geq(a, p, target) ? 1 : 0;
-  return __builtin_amdgcn_readfirstlane(ok) != 0;
+  bool done = p == nullptr || ld_relaxed(p) >= target;
+  if (__builtin_amdgcn_ballot_w64(!done) == 0) return true;
+  const uint64_t deadline = now_ticks() + (uint64_t)a.timeout_ticks;
+  int backoff = 1;
+  for (int it = 1;; ++it) {
+    for (int i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(4);
+    if (!done) done = ld_relaxed(p) >= target;
+    if (__builtin_amdgcn_ballot_w64(!done) == 0) return true;
+    backoff = min(backoff * 2, 8);
+    if ((it & 7) == 0) {
+      int stop = 0;
+      if (lane_id() == 0) {
+        if (ld_relaxed(&a.ctl[CTL_ABORT])) {
+          stop = 1;
+        } else if (now_ticks() > deadline) {
+          st_relaxed(&a.ctl[CTL_ABORT], 1);
+          atomicOr(a.err, ERR_TIMEOUT);
+          stop = 1;
+        }
+      }
+      if (__builtin_amdgcn_readfirstlane(stop)) return false;
+    }
+  }
 }
 
 // Combine units (ct tokens, in token and hence chunk order) are claimed per
