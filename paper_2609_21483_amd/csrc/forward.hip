@@ -742,15 +742,18 @@ __device__ __forceinline__ void reduce_split_n(const FwdArgs& a, size_t orow, in
   constexpr int RB = NS >= 8 ? 4 : 32 / NS;  // 32 vectors in flight per thread
   for (int v0 = threadIdx.x; v0 < total; v0 += RB * FNTH) {
     f32x4_t u[RB][NS];
+    // straight-line loads (a position past the tile re-reads the last one)
+    // and one drain before the stores, so that every load is in flight at
+    // once (see combine_body)
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
-      const int v = v0 + i * FNTH;
-      if (v >= total) continue;
+      const int v = min(v0 + i * FNTH, total - 1);
       const int r = v / q4, c = (v - r * q4) * 4;
       const float* src = a.part + (orow + r) * (size_t)a.H + n0 + c;
 #pragma unroll
       for (int p = 0; p < NS; ++p) u[i][p] = *reinterpret_cast<const f32x4_t*>(src + p * pstride);
     }
+    gemm::wait_vm<0>();
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int v = v0 + i * FNTH;
