@@ -159,6 +159,22 @@ def markdown(results) -> str:
         a = r["accuracy"]
         out.append(f"| {r['workload']} | {tuple(a['pick'])} | {a['t_pick_us']:.1f} | {tuple(a['best'])} | "
                    f"{a['t_best_us']:.1f} | {a['gap']:.1%} |")
+    for r in results:
+        # Fig 7b: the layer time over the (c, K) grid, each point run as the
+        # cost model plans it there (its n_steal), next to the model's T_total
+        g = {(c, K): (t, tp) for c, K, _, _, t, tp in r["grid"]}
+        cs = sorted({c for c, _ in g})
+        ks = sorted({K for _, K in g})
+        best = min(g, key=lambda ck: g[ck][0])
+        out += ["", f"(c, K) grid, {r['workload']}: measured µs (predicted T_total µs); fastest point in bold", "",
+                "| c | " + " | ".join(f"K = {K}" for K in ks) + " |", "|---" * (len(ks) + 1) + "|"]
+        for c in cs:
+            cells = []
+            for K in ks:
+                t, tp = g[(c, K)]
+                cell = f"{t:.1f} ({tp:.0f})"
+                cells.append(f"**{cell}**" if (c, K) == best else cell)
+            out.append(f"| {c} | " + " | ".join(cells) + " |")
     out += ["", "| Workload | plan | SM Active | overlap (of layer) | overlap (of movement) | prologue µs |",
             "|---|---|---|---|---|---|"]
     for r in results:
