@@ -198,6 +198,15 @@ moe_status moe_get_calib(const moe_handle* h, moe_calib* out);
  * Default: 2000 ms, no injection. */
 moe_status moe_set_timeout_ms(moe_handle* h, double ms, int32_t inject_stall);
 
+/* Test hook for section 4's claim that dynamic claiming tolerates CUs that
+ * run at different speeds: with max_sleeps > 0, every workgroup of the
+ * megakernel waits a pseudo-random 0..max_sleeps times 64 cycles before
+ * taking its arrival ticket and before each GEMM tile, and every wavefront
+ * before each dispatch and combine unit it claims.  The counts are drawn
+ * from (seed, workgroup, wavefront, event).  Results must not change.
+ * max_sleeps in [0, 4096]; 0 (the default) turns it off. */
+moe_status moe_set_jitter(moe_handle* h, uint32_t seed, int32_t max_sleeps);
+
 /* Timeline trace of the megakernel (a measurement aid for the schedule of
  * sections 3-4: worker roles, tile waits, movement phases).  buf is caller-
  * owned device memory of `bytes` bytes, or NULL to turn tracing off.  Each

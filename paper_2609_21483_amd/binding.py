@@ -91,6 +91,7 @@ _SIGS = {
     "moe_set_calib": ([_H, C.POINTER(moe_calib)], C.c_int),
     "moe_get_calib": ([_H, C.POINTER(moe_calib)], C.c_int),
     "moe_set_timeout_ms": ([_H, C.c_double, C.c_int32], C.c_int),
+    "moe_set_jitter": ([_H, C.c_uint32, C.c_int32], C.c_int),
     "moe_set_trace": ([_H, C.c_void_p, C.c_int64], C.c_int),
     "moe_workspace_size": ([_H, C.POINTER(C.c_size_t)], C.c_int),
     "moe_workspace_layout": ([_H, C.POINTER(moe_ws_layout)], C.c_int),
@@ -205,6 +206,10 @@ def read_trace(buf) -> "np.ndarray":
     out["id"] = w0 >> 32
     out["t0"], out["t1"], out["t2"] = rec[:, 1], rec[:, 2], rec[:, 3]
     return out
+
+
+def moe_set_jitter(h: int, seed: int, max_sleeps: int) -> None:
+    _check("moe_set_jitter", _lib.moe_set_jitter(h, C.c_uint32(seed & 0xFFFFFFFF), int(max_sleeps)))
 
 
 def moe_set_timeout_ms(h: int, ms: float, inject_stall: int = 0) -> None:

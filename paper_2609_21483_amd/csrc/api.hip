@@ -155,6 +155,8 @@ struct moe_handle {
   unsigned long long launch_seq = 0;
   long long timeout_ticks = 200000000LL;  // 2 s at 100 MHz
   int inject_stall = 0;
+  uint32_t jitter_seed = 0;
+  int jitter_max = 0;
   long long* trace = nullptr;
   int trace_cap = 0, trace_rec0 = 0;
   bool resident_ok = false;  // the megakernel's N workgroups fit the GPU at once
@@ -431,6 +433,8 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   if (forced) a.fplan = *forced;
   a.timeout_ticks = h->timeout_ticks;
   a.inject_stall = h->inject_stall;
+  a.jitter_seed = h->jitter_seed;
+  a.jitter_max = h->jitter_max;
   a.trace = h->trace;
   a.trace_cap = h->trace_cap;
   a.trace_rec0 = h->trace_rec0;
@@ -547,6 +551,14 @@ moe_status moe_set_calib(moe_handle* h, const moe_calib* calib) {
 moe_status moe_get_calib(const moe_handle* h, moe_calib* out) {
   if (!h || !out) return fail(MOE_ERR_INVALID_ARG, "NULL argument");
   *out = h->calib;
+  return MOE_OK;
+}
+
+moe_status moe_set_jitter(moe_handle* h, uint32_t seed, int32_t max_sleeps) {
+  if (!h) return fail(MOE_ERR_INVALID_ARG, "handle is NULL");
+  if (max_sleeps < 0 || max_sleeps > 4096) return fail(MOE_ERR_INVALID_ARG, "max_sleeps must be in [0, 4096]");
+  h->jitter_seed = seed;
+  h->jitter_max = max_sleeps;
   return MOE_OK;
 }
 

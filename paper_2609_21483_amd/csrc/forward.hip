@@ -220,6 +220,22 @@ __device__ __forceinline__ int xcd_id() {
   return v;
 }
 
+// Test hook (moe_set_jitter): a pseudo-random delay of 0..jitter_max sleeps
+// of 64 cycles, drawn from (seed, workgroup, wavefront, event), so that
+// workgroups reach their claims in perturbed orders.
+__device__ __forceinline__ void jitter(const FwdArgs& a, uint32_t event) {
+  if (!a.jitter_max) return;
+  uint32_t h = a.jitter_seed ^ (blockIdx.x * 0x9E3779B1u) ^ (event * 0x85EBCA77u) ^
+               ((uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * 0xC2B2AE3Du);
+  h ^= h >> 16;
+  h *= 0x7FEB352Du;
+  h ^= h >> 15;
+  h *= 0x846CA68Bu;
+  h ^= h >> 16;
+  const int n = __builtin_amdgcn_readfirstlane((int)(h % (uint32_t)(a.jitter_max + 1)));
+  for (int i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(1);
+}
+
 // One lane of a wavefront appends one record to the wavefront's own segment
 // of the trace buffer (segment blockIdx.x * NWF + wave, trace_cap records):
 // a per-wavefront LDS counter, no global atomics, so tracing does not
@@ -463,6 +479,7 @@ __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& 
   for (;;) {
     const int u = claim_disp(a, S, shard);
     if (u < 0) break;
+    jitter(a, 0x20000u + (uint32_t)u);
     dispatch_one<true>(a, &S, W, u, unit_row(a, &S, u));
   }
 }
@@ -948,6 +965,7 @@ __device__ __forceinline__ bool compute_tiles(const FwdArgs& a, const Sched& S, 
   int t = __builtin_amdgcn_readfirstlane(W.bc[1]);
   __syncthreads();
   for (int done = 1; t >= 0; ++done) {
+    jitter(a, 0x40000u + (uint32_t)t);
     const uint64_t t0 = a.trace ? now_ticks() : 0;
     const TileRef r = decode_tile(a, S, t);
     const int id = S.mb[r.q * S.nseg + r.seg] + r.mt;
@@ -1019,6 +1037,7 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
   for (;;) {
     const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
     if (u < 0) return true;
+    jitter(a, 0x10000u + (uint32_t)u);
     const uint64_t t0 = a.trace ? now_ticks() : 0;
     uint64_t t1 = t0;
     const int g0 = u * a.ct;
@@ -1043,6 +1062,7 @@ __device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& 
     for (int i = tid; i < a.ctl_words; i += FNTH) a.ctl_next[i] = 0;
 
   // arrival ticket (role) first, so that its round trip overlaps the staging
+  jitter(a, 0);
   int tk = 0;
   if (tid == 0) {
     tk = fetch_add_relaxed(&a.ctl[CTL_TICKET], 1);

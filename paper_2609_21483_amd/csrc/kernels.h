@@ -123,6 +123,8 @@ struct FwdArgs {
   moe_plan fplan;
   long long timeout_ticks;  // per wait, 100 MHz ticks
   int inject_stall;         // test hook: every wait targets an unreachable value
+  uint32_t jitter_seed;     // test hook: seeded random delays (moe_set_jitter)
+  int jitter_max;           //   at most this many 64-cycle sleeps per event; 0 = off
   int serial_K;             // chunk tiling used by the separate-kernel GEMMs
   int static_disp;          // megakernel: the first round of dispatch units is owned by arrival ticket
   int stack_next;           // stacked launch: another layer follows, so compute workers go on to it
