@@ -59,11 +59,18 @@ def test_ablation_summary_table():
          "plans": {"no_T": (32, 1, 0, 0), "best_static": (24, 1, 0, 0)},
          "reduction": {"S": -0.2, "T": 0.25, "S+T": 0.1},
          "accuracy": {"pick": [32, 1], "t_pick_us": 90.0, "best": [24, 1], "t_best_us": 88.0, "gap": 90 / 88 - 1},
-         "timeline": {"full": m, "no_T": None}}
+         "timeline": {"full": m, "no_T": None},
+         # (c, K, n_steal, final_all, measured us, predicted us)
+         "grid": [[24, 1, 3, 1, 88.0, 95.0], [24, 2, 2, 1, 93.5, 97.0], [32, 1, 4, 1, 90.0, 94.0],
+                  [32, 2, 3, 1, 91.25, 96.0]]}
     md = A.markdown([r])
     assert "| w | 100.0 | 120.0 (c 32) | 90.0 | 130.0 | 110.0 (24) | -20.0% | +25.0% | +10.0% |" in md
     assert "| w | (32, 1) | 90.0 | (24, 1) | 88.0 | 2.3% |" in md
     assert "| w | full | 90.0% | 5.0% | 40.0% | 15.0 |" in md
+    # the Fig 7b grid: rows c, columns K, measured (predicted), the fastest point in bold
+    assert "| c | K = 1 | K = 2 |" in md
+    assert "| 24 | **88.0 (95)** | 93.5 (97) |" in md
+    assert "| 32 | 90.0 (94) | 91.2 (96) |" in md
 
 
 def test_read_trace_decodes_wavefront_segments():
