@@ -110,8 +110,13 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
   u += 0x7fffu + ((u >> 16) & 1u);
   return u >> 16;
 }
+// two fp32 -> packed bf16 (lo in bits 0-15), round to nearest even, in one
+// v_cvt_pk_bf16_f32; the same bits as f32_to_bf16 for every non-NaN value
+typedef __bf16 bf16x2_hw_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_hw_t));
 }
 
 // ---- memory-model helpers (agent scope: every CU of every XCD) ---------------

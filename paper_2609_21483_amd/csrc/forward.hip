@@ -735,10 +735,10 @@ __device__ __forceinline__ int run_gemm(const FwdArgs& a, const Sched& S, const 
   int nxt = -1;
   if (threadIdx.x == 0) nxt = claim_next();
   if (r.ph == 0) {
-    gemm::store_silu_mul_tiled<CP>(acc, a.Hb + (orow >> 5) * (size_t)a.F * gemm::GROUP + (size_t)(n0 / 2) * gemm::GROUP,
-                                   (int)(orow & 31), a.F * gemm::GROUP, r.rows, a.F - n0 / 2);
+    gemm::store_silu_mul_tiled_lds<CP>(acc, a.Hb + (orow >> 5) * (size_t)a.F * gemm::GROUP + (size_t)(n0 / 2) * gemm::GROUP,
+                                       (int)(orow & 31), a.F * gemm::GROUP, r.rows, a.F - n0 / 2, ring);
   } else if (a.nsplit == 1) {
-    gemm::store_bf16<CP>(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0);
+    gemm::store_bf16_lds<CP>(acc, a.O + orow * a.H + n0, a.H, r.rows, a.H - n0, ring);
   } else {
     gemm::store_f32<CP>(acc, a.part + ((size_t)r.ks * a.prow + orow) * a.H + n0, a.H, r.rows, a.H - n0);
   }

@@ -331,74 +331,129 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* p) {
                                            0x00020000);
 }
 
-// GEMM0 epilogue: gate/up 32-column pairs -> bf16(silu(gate) * up); the tile
-// writes TILE_N/2 output columns
-template <int CP>
-__device__ __forceinline__ void store_silu_mul(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
-  ldo = opaque(ldo);
-  const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
-  const OutMap m = out_map(TN / 2);
-  const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int dr = out_dr(mb, r);
-      if (m.row_l + dr < out_rows && m.col_l < out_cols) {
-        const float g = acc[mb][0][r], u = acc[mb][1][r];
-        const float hv = (g / (1.0f + __expf(-g))) * u;
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(hv), rs, (base + (uint32_t)(dr * ldo)) * 2u, 0, CP);
-      }
-    }
+// Epilogues, staged through LDS.  A lane holds one column of each 32 x 32
+// accumulator block (out_map), so stores straight from the accumulators are
+// 2-byte stores, 128 per lane for the 256 x 256 GEMM1 tile.  Instead each
+// lane converts pairs of rows with one packed conversion, swaps the packed
+// word with its neighbour (adjacent lanes hold adjacent columns) so that it
+// holds two adjacent columns of one row, and writes 32-bit words into the
+// free ring, row-major with a padded row stride (rows r and r + 4 of one
+// write fall in different bank halves).  Then every thread stores whole
+// 16-byte pieces of rows.  The barriers wait for LDS traffic only: the
+// stores drain while the next tile starts.
+constexpr int EPI_PAD = 16;  // bytes of padding per staged row
+
+// Barrier for LDS traffic only: this wave's LDS operations have completed,
+// then every wave meets.  (__syncthreads also waits for this wave's global
+// stores, vmcnt(0): the whole write latency of the tile's output.)
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt((3 << 14) | (7 << 4) | 15);  // lgkmcnt(0); vmcnt, expcnt not waited for
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
 }
 
-// GEMM0 epilogue into a group-tiled h: `out` points at the k-step block of
-// the tile's first h column in the group holding its first row, which is row
-// r0 of that group; groups are gs elements apart.  The 32 h columns of a
-// wave are one 64-byte row piece of a block.
+__device__ __forceinline__ uint32_t swap_lane_pair(uint32_t v) {
+  // quad_perm [1, 0, 3, 2]: lane l takes lane l ^ 1's value
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+}
+
+// Stages accumulator pairs (rows r, r + 1 of a column) of the row blocks
+// mb in [mb0, mb1) into `lds` as bf16 words of two adjacent columns, rows
+// relative to row `row_off`.  vals(mb, j, r) gives the value of the lane's
+// column j (0 .. ncol-1 per wave) at register r of block mb.
+template <int NCOL, typename ValFn>
+__device__ __forceinline__ void stage_pairs(char* lds, int stride, int mb0, int mb1, int row_off, int cols_per_wave,
+                                            ValFn&& vals) {
+  const int lane = lane_here(), wave = opaque((int)(threadIdx.x >> 6));
+  const int wm = wave % WM, wn = wave / WM;
+  const bool odd = lane & 1;
+  const int col = wn * cols_per_wave + ((lane & 31) & ~1);
+  const int rl = wm * 32 + 4 * (lane >> 5) + (odd ? 1 : 0) - row_off;
+  // unrolled over every block (the accumulators are registers); mb0 and mb1
+  // are constants where the callers' loops are unrolled
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    if (mb < mb0 || mb >= mb1) continue;
+#pragma unroll
+    for (int j = 0; j < NCOL; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        const uint32_t p = pack_bf16x2(vals(mb, j, r), vals(mb, j, r + 1));
+        const uint32_t q = swap_lane_pair(p);
+        const uint32_t w = odd ? ((q >> 16) | (p & 0xFFFF0000u)) : ((p & 0xFFFFu) | (q << 16));
+        const int row = rl + out_dr(mb, r);
+        *reinterpret_cast<uint32_t*>(lds + row * stride + (col + j * 32) * 2) = w;
+      }
+  }
+}
+
+// GEMM0 epilogue through LDS into a group-tiled h (as store_silu_mul_tiled).
+// ring: RING_BYTES of LDS, free (the mainloop ended with a barrier); ends
+// with a barrier on the LDS traffic (the stores may still be in flight).
 template <int CP>
-__device__ __forceinline__ void store_silu_mul_tiled(const Acc& acc, uint16_t* out, int r0, int gs, int out_rows,
-                                                     int out_cols) {
+__device__ __forceinline__ void store_silu_mul_tiled_lds(const Acc& acc, uint16_t* out, int r0, int gs, int out_rows,
+                                                         int out_cols, char* ring) {
+  constexpr int COLS = TN / 2 * WN;  // 128 h columns
+  constexpr int STRIDE = COLS * 2 + EPI_PAD;
+  static_assert(TILE_M * STRIDE <= RING_BYTES, "staged h tile fits the ring");
   r0 = opaque(r0);
   gs = opaque(gs);
+  out_rows = opaque(out_rows);
+  out_cols = opaque(out_cols);
+  stage_pairs<1>(ring, STRIDE, 0, MB, 0, TN / 2, [&](int mb, int, int r) {
+    const float g = acc[mb][0][r], u = acc[mb][1][r];
+    return (g / (1.0f + __expf(-g))) * u;
+  });
+  lds_barrier();
   const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
-  const OutMap m = out_map(TN / 2);
-  const uint32_t cpart = (uint32_t)((m.col_l >> 5) * (GROUP * KSTEP) + (m.col_l & (KSTEP - 1)));
+  constexpr int PPR = COLS / 8;  // 16-byte pieces per row
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int dr = out_dr(mb, r);
-      if (m.row_l + dr < out_rows && m.col_l < out_cols) {
-        const float g = acc[mb][0][r], u = acc[mb][1][r];
-        const float hv = (g / (1.0f + __expf(-g))) * u;
-        const int p = r0 + m.row_l + dr;
-        const uint32_t off = (uint32_t)((p >> 5) * gs + (p & (GROUP - 1)) * KSTEP) + cpart;
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(hv), rs, off * 2u, 0, CP);
-      }
+  for (int i = 0; i < TILE_M * PPR / (NWAVE * 64); ++i) {
+    const int piece = (int)threadIdx.x + i * NWAVE * 64;
+    const int row = piece / PPR, c = (piece % PPR) * 8;
+    if (row < out_rows && c < out_cols) {
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ring + row * STRIDE + c * 2);
+      const int p = r0 + row;
+      const uint32_t off = (uint32_t)((p >> 5) * gs + (c >> 5) * (GROUP * KSTEP) + (p & (GROUP - 1)) * KSTEP + (c & 31));
+      __builtin_amdgcn_raw_buffer_store_b128(v, rs, off * 2u, 0, CP);
     }
+  }
+  lds_barrier();
 }
 
-// GEMM1 epilogue: bf16(acc) into the tile
+// GEMM1 epilogue through LDS into a row-major O (as store_bf16), in two
+// halves of 128 rows (a staged 256-row tile would exceed the ring).  Ends
+// with a barrier on the LDS traffic (the stores may still be in flight).
 template <int CP>
-__device__ __forceinline__ void store_bf16(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols) {
+__device__ __forceinline__ void store_bf16_lds(const Acc& acc, uint16_t* out, int ldo, int out_rows, int out_cols,
+                                               char* ring) {
+  constexpr int COLS = TILE_N;
+  constexpr int STRIDE = COLS * 2 + EPI_PAD;
+  constexpr int HALF = TILE_M / 2;
+  static_assert(HALF * STRIDE <= RING_BYTES, "staged half tile fits the ring");
+  static_assert(MB % 2 == 0, "a half holds whole row blocks of every wave");
   ldo = opaque(ldo);
+  out_rows = opaque(out_rows);
+  out_cols = opaque(out_cols);
   const __amdgpu_buffer_rsrc_t rs = out_rsrc(out);
-  const OutMap m = out_map(TN);
-  const uint32_t base = (uint32_t)(m.row_l * ldo + m.col_l);
+  constexpr int PPR = COLS / 8;
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+  for (int h = 0; h < 2; ++h) {
+    stage_pairs<NB>(ring, STRIDE, h * MB / 2, (h + 1) * MB / 2, h * HALF, TN,
+                    [&](int mb, int j, int r) { return acc[mb][j][r]; });
+    lds_barrier();
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int dr = out_dr(mb, r);
-      if (m.row_l + dr < out_rows) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          if (m.col_l + nb * 32 < out_cols)
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f32_to_bf16(acc[mb][nb][r]), rs,
-                                                  (base + (uint32_t)(dr * ldo) + nb * 32) * 2u, 0, CP);
+    for (int i = 0; i < HALF * PPR / (NWAVE * 64); ++i) {
+      const int piece = (int)threadIdx.x + i * NWAVE * 64;
+      const int row = piece / PPR, c = (piece % PPR) * 8;
+      if (h * HALF + row < out_rows && c < out_cols) {
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ring + row * STRIDE + c * 2);
+        const uint32_t off = (uint32_t)((h * HALF + row) * ldo + c);
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, off * 2u, 0, CP);
       }
     }
+    lds_barrier();
+  }
 }
 
 // GEMM1 split-K epilogue: this split's fp32 partial into a row-major buffer
