@@ -119,7 +119,8 @@ moe_status launch_gate(GateArgs& g, hipStream_t s) {
     // chains than about 64 ranges, one chain per lane over many small
     // workgroups spreads them over more CUs)
     const long long ranges = ((long long)g.T * g.E + GATE_CHAIN_STAGED_W - 1) / GATE_CHAIN_STAGED_W;
-    gate_chain_staged_kernel<<<(int)std::min<long long>(ranges, 256), GATE_CHAIN_STAGED_W, 0, s>>>(g);
+    // two workgroups per CU (the kernel's registers and LDS allow it)
+    gate_chain_staged_kernel<<<(int)std::min<long long>(ranges, 512), GATE_CHAIN_STAGED_W, 0, s>>>(g);
   } else {
     gate_chain_kernel<<<std::min(16384, std::max(1, (g.T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
   }

@@ -882,8 +882,10 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
 // (coherent across XCDs, no cache invalidation: an acquire here would
 // invalidate this XCD's L2 on every poll, under the GEMM tiles of the other
 // workgroups).  No acquire is needed for the data that follows: producers
-// write back their L2 before publishing (release), and no CU reads a
-// dispatched row, an Hbuf/O row or a partial before it is published, so no
+// store it with agent-coherent (sc1) stores and drain them before their
+// relaxed increment, and no CU loads a line of a dispatched row, an Hbuf/O
+// row or a partial before its counter says it is complete (the row map keeps
+// every row tile's lines its own; the combine's absent entries read x), so no
 // stale copy of those lines can sit in the consumer's L1 or L2 (caches are
 // invalidated at kernel start).
 // One lane polls *p until it reaches target, backing off exponentially up to

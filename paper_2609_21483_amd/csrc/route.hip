@@ -857,19 +857,14 @@ __global__ void __launch_bounds__(WAVE) gate_chain_kernel(GateArgs a) {
 // global->LDS loads, rows past E repeating the last one) in a ring of CH_P
 // stages; a lane reads its gate values from there and its x values straight
 // from global memory into one of CH_P register sets: the chains of one token
-// are adjacent in the list, so a wavefront's load touches few lines.  The
-// 64 products of a block are added in order, each rounded before the add, as
+// are adjacent in the list, so a wavefront's load touches few lines.  Two
+// stages keep the registers under 128, so that two workgroups share a CU and
+// their wavefronts hide each other's latency.  The 64 products of a block are
+// added in order, one fused multiply-add each: the product of two bf16 values
+// is exact in fp32, so this is the product rounded, then the sum rounded, as
 // in exact_logit.  Granules of a staged row are XOR-swizzled by (row & 7).
-constexpr int CH_W = 512, CH_E = 128, CH_K = 64, CH_P = 4;
+constexpr int CH_W = 512, CH_E = 128, CH_K = 64, CH_P = 2;
 constexpr int CH_DMA = CH_E / 8 / (CH_W / WAVE);  // DMA instructions per wavefront and block
-constexpr int CH_VM = 8 + CH_DMA;                  // vector memory instructions per wavefront and block
-
-template <int OUT>
-__device__ __forceinline__ void ch_wait(int ahead) {
-  if (ahead >= 2) gemm::wait_vm<2 * OUT>();
-  else if (ahead == 1) gemm::wait_vm<OUT>();
-  else gemm::wait_vm<0>();
-}
 
 // One range of CH_W chains from c0 (< n).
 __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c0, int n) {
@@ -899,15 +894,15 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c
   };
   float acc = 0.0f;
   const int wrow = e * (2 * CH_K), wsw = e & 7;
-  // block b: wait for its loads (blocks b + 1 and b + 2 may still be in
-  // flight), then, past the barrier that every wavefront reaches only after
-  // adding block b - 1, refill that block's stage and register set with
-  // block b + 3, and add block b
+  // block b: wait for its loads, then, past the barrier that every
+  // wavefront reaches only after adding block b - 1 (and after its own loads
+  // of block b have landed), issue block b + 1 into that stage and register
+  // set, and add block b
   auto step = [&](int b, const u32x4_t (&xs)[8], u32x4_t (&refill)[8]) {
-    ch_wait<CH_VM>(min(CH_P - 2, nb - 1 - b));
+    gemm::wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     gemm::compiler_fence();
-    if (b + CH_P - 1 < nb) issue(b + CH_P - 1, refill);
+    if (b + 1 < nb) issue(b + 1, refill);
     const char* st = ring + (b % CH_P) * (CH_E * 2 * CH_K) + wrow;
     u32x4_t wv[8];
 #pragma unroll
@@ -921,16 +916,10 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c
       }
   };
   if (0 < nb) issue(0, xv[0]);
-  if (1 < nb) issue(1, xv[1]);
-  if (2 < nb) issue(2, xv[2]);
   for (int b = 0; b < nb; b += CH_P) {
-    step(b, xv[0], xv[3]);
+    step(b, xv[0], xv[1]);
     if (b + 1 >= nb) break;
     step(b + 1, xv[1], xv[0]);
-    if (b + 2 >= nb) break;
-    step(b + 2, xv[2], xv[1]);
-    if (b + 3 >= nb) break;
-    step(b + 3, xv[3], xv[2]);
   }
   if (live) a.ch_l[i] = a.bias ? acc + a.bias[e] : acc;
   // the next range refills every stage
@@ -940,8 +929,8 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c
 
 // Persistent over the ranges of CH_W chains (the chain count is known only
 // on the device).
-__global__ void __launch_bounds__(CH_W) gate_chain_staged_kernel(GateArgs a) {
-  static_assert(CH_P == 4 && CH_E % (8 * (CH_W / WAVE)) == 0, "chain staging geometry");
+__global__ void __launch_bounds__(CH_W, 4) gate_chain_staged_kernel(GateArgs a) {  // 4 waves per SIMD: two workgroups per CU
+  static_assert(CH_P == 2 && CH_E % (8 * (CH_W / WAVE)) == 0, "chain staging geometry");
   __shared__ __attribute__((aligned(1024))) char ring[CH_P * CH_E * 2 * CH_K];
   const int n = a.stats[ST_CANDS];
   for (int c0 = blockIdx.x * CH_W; c0 < n; c0 += gridDim.x * CH_W) chain_range(a, ring, c0, n);
