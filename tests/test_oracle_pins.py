@@ -263,7 +263,7 @@ def _dense_masked(x, idx, w, w1, w3, w2, ws, Tr, e0):
 
 @pytest.mark.parametrize("shared", [False, True])
 def test_layer_sparse_equals_dense_masked(orc, shared):
-    """North-star brute force: dense evaluation of every local expert, masked by
+    """Brute force: dense evaluation of every local expert, masked by
     top-k, equals the oracle's sparse path."""
     sh = W.TINY.with_(hidden=64, ffn=64, n_local_experts=5, n_shared_experts=2 if shared else 0)
     rng = np.random.default_rng(8)
