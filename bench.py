@@ -60,8 +60,8 @@ def parse():
     ap.add_argument("--reps", type=int, default=5, help="stack runs per mode and round")
     ap.add_argument("--flush-mib", type=int, default=512, help="scratch written before each flushed launch")
     ap.add_argument("--no-trace", action="store_true")
-    ap.add_argument("--stack", action="store_true",
-                    help="run the layers of a timed step in one stacked launch (default: one launch per layer)")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="run the layers of a timed step as one launch per layer (default: one stacked launch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2, help="oracle rows per rank and layer, single-thread leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -376,12 +376,12 @@ def y_check(stack, samples, ref):
 
 def measure_stack(B, stack, args, stream, flush, trace: bool):
     """Timed steps, then the baselines, flushed launches and traces.  A step
-    routes every layer and runs the MoE layers, one launch per layer (or, with
-    --stack, all of them in one stacked launch)."""
+    routes every layer and runs the MoE layers in one stacked launch (or, with
+    --no-stack, one launch per layer)."""
     import numpy as np
     import torch
     n = len(stack.L)
-    stacked = n > 1 and args.stack
+    stacked = n > 1 and not args.no_stack
 
     def layers_forward():
         if stacked:
