@@ -369,6 +369,10 @@ __device__ __forceinline__ void stage_pairs(char* lds, int stride, int mb0, int 
   const bool odd = lane & 1;
   const int col = wn * cols_per_wave + ((lane & 31) & ~1);
   const int rl = wm * 32 + 4 * (lane >> 5) + (odd ? 1 : 0) - row_off;
+  // byte selector of v_perm_b32 over (q, p), bytes 0-3 from p and 4-7 from q:
+  // an even lane keeps its low half and takes its neighbour's (row r),
+  // an odd lane takes its neighbour's high half and keeps its own (row r + 1)
+  const uint32_t sel = odd ? 0x03020706u : 0x05040100u;
   // unrolled over every block (the accumulators are registers); mb0 and mb1
   // are constants where the callers' loops are unrolled
 #pragma unroll
@@ -380,7 +384,7 @@ __device__ __forceinline__ void stage_pairs(char* lds, int stride, int mb0, int 
       for (int r = 0; r < 16; r += 2) {
         const uint32_t p = pack_bf16x2(vals(mb, j, r), vals(mb, j, r + 1));
         const uint32_t q = swap_lane_pair(p);
-        const uint32_t w = odd ? ((q >> 16) | (p & 0xFFFF0000u)) : ((p & 0xFFFFu) | (q << 16));
+        const uint32_t w = __builtin_amdgcn_perm(q, p, sel);
         const int row = rl + out_dr(mb, r);
         *reinterpret_cast<uint32_t*>(lds + row * stride + (col + j * 32) * 2) = w;
       }
