@@ -114,13 +114,16 @@ moe_status launch_gate(GateArgs& g, hipStream_t s) {
       else gate_tile_kernel<64, 32><<<grid, NTH, 0, s>>>(g);
     }
   }
-  if (g.E <= 128 && (long long)g.T * g.k >= 32768) {
+  if (g.E <= 128 && g.k >= 4 && (long long)g.T * g.k >= 32768) {
     // persistent over ranges of chains, at most T * E of them (with fewer
     // chains than about 64 ranges, one chain per lane over many small
-    // workgroups spreads them over more CUs)
+    // workgroups spreads them over more CUs); a range holds at most
+    // 512 / k + 2 tokens, whose x rows a stage holds
     const long long ranges = ((long long)g.T * g.E + GATE_CHAIN_STAGED_W - 1) / GATE_CHAIN_STAGED_W;
     // two workgroups per CU (the kernel's registers and LDS allow it)
-    gate_chain_staged_kernel<<<(int)std::min<long long>(ranges, 512), GATE_CHAIN_STAGED_W, 0, s>>>(g);
+    const int grid = (int)std::min<long long>(ranges, 512);
+    if (g.k >= 8) gate_chain_staged_kernel<72, 3><<<grid, GATE_CHAIN_STAGED_W, 0, s>>>(g);
+    else gate_chain_staged_kernel<136, 2><<<grid, GATE_CHAIN_STAGED_W, 0, s>>>(g);
   } else {
     gate_chain_kernel<<<std::min(16384, std::max(1, (g.T * g.k * 3 / 2 + WAVE - 1) / WAVE)), WAVE, 0, s>>>(g);
   }

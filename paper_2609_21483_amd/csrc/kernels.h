@@ -244,7 +244,8 @@ template <int GT_M, int EPL>
 __global__ void gate_tile_kernel(GateArgs a);  // E > 32; GT_M tokens per workgroup (64 or 128),
                                                // EPL >= E / 16 experts per lane in the candidate pass
 __global__ void gate_chain_kernel(GateArgs a);
-__global__ void gate_chain_staged_kernel(GateArgs a);  // E <= 128
+template <int CX, int NP>
+__global__ void gate_chain_staged_kernel(GateArgs a);  // E <= 128, CX tokens per range, NP stages
 constexpr int GATE_CHAIN_STAGED_W = 512;               // chains per workgroup of gate_chain_staged_kernel
 template <int GT_M>
 __global__ void gate_tile2_kernel(GateArgs a);  // 32 < E <= 128; GT_M tokens per workgroup (64 or 128)

@@ -852,89 +852,163 @@ __global__ void __launch_bounds__(WAVE) gate_chain_kernel(GateArgs a) {
 }
 
 // The chains of the list for E <= CH_E: one lane per chain, CH_W chains per
-// workgroup.  For each 64-value block of h the workgroup stages that block of
-// all gate rows in LDS (CH_E rows of 128 bytes, whole lines by direct
-// global->LDS loads, rows past E repeating the last one) in a ring of CH_P
-// stages; a lane reads its gate values from there and its x values straight
-// from global memory into one of CH_P register sets: the chains of one token
-// are adjacent in the list, so a wavefront's load touches few lines.  Two
-// stages keep the registers under 128, so that two workgroups share a CU and
-// their wavefronts hide each other's latency.  The 64 products of a block are
-// added in order, one fused multiply-add each: the product of two bf16 values
-// is exact in fp32, so this is the product rounded, then the sum rounded, as
-// in exact_logit.  Granules of a staged row are XOR-swizzled by (row & 7).
-constexpr int CH_W = 512, CH_E = 128, CH_K = 64, CH_P = 2;
-constexpr int CH_DMA = CH_E / 8 / (CH_W / WAVE);  // DMA instructions per wavefront and block
+// workgroup.  The chains of one token are adjacent in the list and every
+// token has at least k of them (its top k are among them), so a range of
+// CH_W chains holds at most CH_W / k + 2 tokens, CX of them in a stage.  For
+// each 64-value block of h the workgroup stages in LDS that block of all gate
+// rows (CH_E rows of 128 bytes, rows past E repeating the last one) and of the
+// x rows of its tokens (CX rows, slots past the range's tokens repeating its
+// first), whole lines by direct global->LDS loads, in a ring of NP stages: no
+// operand goes through registers ahead of its use, so with NP = 3 two blocks
+// are in flight while one is added, and two workgroups share a CU.  A lane
+// reads its token's x and its expert's gate values from the stage and adds
+// the 64 products in order, one fused multiply-add each: the product of two
+// bf16 values is exact in fp32, so this is the product rounded, then the sum
+// rounded, as in exact_logit.  Granules of a staged row are XOR-swizzled
+// (chain_swz).
+constexpr int CH_W = 512, CH_E = 128, CH_K = 64;
+constexpr int CH_NW = CH_W / WAVE;       // wavefronts per workgroup
+constexpr int CH_WB = CH_E * 2 * CH_K;   // gate bytes of a stage
+constexpr int CH_DMA = CH_E / 8 / CH_NW; // gate DMA instructions per wavefront and block
 
-// One range of CH_W chains from c0 (< n).
-__device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int c0, int n) {
+// Granule swizzle of a staged 128-byte row: two rows share a 256-byte bank
+// window, so the granule is XOR-ed with bits 1-3 of the row, and rows that
+// differ in their low four bits put a given granule in different banks.
+__device__ __forceinline__ int chain_swz(int row) { return (row >> 1) & 7; }
+
+template <int CX, int NP>
+struct ChainGeo {
+  static constexpr int STAGE = CH_WB + CX * 2 * CH_K;        // bytes of a stage
+  static constexpr int XI = (CX / 8 + CH_NW - 1) / CH_NW;    // x DMA instructions per wavefront and block (at most)
+  static_assert(CX % 8 == 0 && STAGE % 1024 == 0 && (NP == 2 || NP == 3), "chain staging geometry");
+};
+
+// One range of CH_W chains from c0 (< n); the range's chains belong to at
+// most CX tokens (the host picks CX from k).
+template <int CX, int NP>
+__device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int* tok, int* wsum, int c0, int n) {
+  using Geo = ChainGeo<CX, NP>;
   const int lane = gemm::lane_here(), wave = gemm::opaque((int)(threadIdx.x / WAVE));
   const int i = c0 + (int)threadIdx.x;
   const bool live = i < n;
-  const int g = a.ch_g[live ? i : c0], e = a.ch_e[live ? i : c0];
+  const int ic = live ? i : n - 1;
+  const int g = a.ch_g[ic], e = a.ch_e[ic];
+  // the range's tokens, in list order: a live lane starts a slot where its
+  // token differs from the previous entry's (the range's first entry always)
+  const bool head = live && (i == c0 || a.ch_g[i - 1] != g);
+  const uint64_t hm = __builtin_amdgcn_ballot_w64(head);
+  const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(hm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)hm, 0));
+  if (lane == 0) wsum[wave] = __builtin_popcountll(hm);
+  __syncthreads();
+  int base = 0, nslot = 0;
+  for (int w = 0; w < CH_NW; ++w) {
+    const int c = wsum[w];
+    if (w < wave) base += c;
+    nslot += c;
+  }
+  if (nslot > CX) {
+    // more tokens than a stage holds (not expected: every token has at least
+    // k chains): each lane evaluates its chain straight from global memory
+    if (live) {
+      const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(a.x + (size_t)g * a.H);
+      const u32x4_t* wv = reinterpret_cast<const u32x4_t*>(a.wgt + (size_t)e * a.H);
+      float l = 0.0f;
+      for (int v = 0; v < (a.H >> 3); ++v) {
+        const u32x4_t xq = xv[v], wq = wv[v];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          l = __builtin_fmaf(bf16_lo(xq[q]), bf16_lo(wq[q]), l);
+          l = __builtin_fmaf(bf16_hi(xq[q]), bf16_hi(wq[q]), l);
+        }
+      }
+      a.ch_l[i] = a.bias ? l + a.bias[e] : l;
+    }
+    __syncthreads();
+    return;
+  }
+  const int slot = base + before - (head ? 0 : 1);
+  if (head) tok[slot] = g;
+  __syncthreads();
   const int H = gemm::opaque(a.H), nb = H / CH_K;
   const uint32_t ring0 = (uint32_t)gemm::opaque((int)gemm::lds_u32(ring));
-  uint32_t wo[CH_DMA];
+  uint32_t wo[CH_DMA], xo[Geo::XI];
 #pragma unroll
   for (int j = 0; j < CH_DMA; ++j) {
     const int row = (wave * CH_DMA + j) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ (row & 7);
+    const int c = (lane & 7) ^ chain_swz(row);
     wo[j] = (uint32_t)(min(row, a.E - 1) * H * 2 + c * 16);
   }
+#pragma unroll
+  for (int j = 0; j < Geo::XI; ++j) {
+    const int row = (j * CH_NW + wave) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ chain_swz(row);
+    xo[j] = (uint32_t)(tok[row < nslot ? row : 0] * H * 2 + c * 16);
+  }
+  // x DMA instructions of this wavefront: Geo::XI, or one fewer where the
+  // last round of 8-row instructions does not reach it
+  const int nxi = gemm::opaque((CX / 8 - wave + CH_NW - 1) / CH_NW);
   const char* wb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.wgt));
-  const u32x4_t* xr = reinterpret_cast<const u32x4_t*>(a.x + (size_t)g * H);
-  // block b: LDS stage b % CH_P, x register set b % CH_P
-  u32x4_t xv[CH_P][8];
-  auto issue = [&](int b, u32x4_t (&dst)[8]) {
-    const uint32_t st = ring0 + (uint32_t)((b % CH_P) * (CH_E * 2 * CH_K));
+  const char* xb = gemm::uniform_ptr(reinterpret_cast<const char*>(a.x));
+  auto issue = [&](int b) {
+    const uint32_t st = ring0 + (uint32_t)((b % NP) * Geo::STAGE);
 #pragma unroll
     for (int j = 0; j < CH_DMA; ++j) gemm::dma16(wb + (size_t)b * (2 * CH_K), wo[j], st + (wave * CH_DMA + j) * 1024);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) dst[q] = xr[b * 8 + q];
+    for (int j = 0; j < Geo::XI; ++j)
+      if (j < nxi) gemm::dma16(xb + (size_t)b * (2 * CH_K), xo[j], st + CH_WB + (j * CH_NW + wave) * 1024);
   };
   float acc = 0.0f;
-  const int wrow = e * (2 * CH_K), wsw = e & 7;
-  // block b: wait for its loads, then, past the barrier that every
-  // wavefront reaches only after adding block b - 1 (and after its own loads
-  // of block b have landed), issue block b + 1 into that stage and register
-  // set, and add block b
-  auto step = [&](int b, const u32x4_t (&xs)[8], u32x4_t (&refill)[8]) {
-    gemm::wait_vm<0>();
+  const int wrow = e * (2 * CH_K), wsw = chain_swz(e);
+  const int xrow = CH_WB + slot * (2 * CH_K), xsw = chain_swz(slot);
+  // block b: its stage holds this wavefront's loads once at most the blocks
+  // issued after it are outstanding; past the barrier every wavefront's have
+  // landed and every wavefront has added block b - 1, so the stage of block
+  // b + NP - 1 (that of b - 1) is refilled, then block b is added
+  auto step = [&](int b) {
+    if (NP == 3 && b + 1 < nb) {
+      if (nxi == Geo::XI) gemm::wait_vm<CH_DMA + Geo::XI>(); else gemm::wait_vm<CH_DMA + Geo::XI - 1>();
+    } else {
+      gemm::wait_vm<0>();
+    }
     __builtin_amdgcn_s_barrier();
     gemm::compiler_fence();
-    if (b + 1 < nb) issue(b + 1, refill);
-    const char* st = ring + (b % CH_P) * (CH_E * 2 * CH_K) + wrow;
-    u32x4_t wv[8];
+    if (b + NP - 1 < nb) issue(b + NP - 1);
+    const char* st = ring + (b % NP) * Geo::STAGE;
+    u32x4_t xv[8], wv[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) wv[q] = *reinterpret_cast<const u32x4_t*>(st + ((q ^ wsw) << 4));
+    for (int q = 0; q < 8; ++q) {
+      xv[q] = *reinterpret_cast<const u32x4_t*>(st + xrow + ((q ^ xsw) << 4));
+      wv[q] = *reinterpret_cast<const u32x4_t*>(st + wrow + ((q ^ wsw) << 4));
+    }
 #pragma unroll
     for (int q = 0; q < 8; ++q)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        acc = __builtin_fmaf(bf16_lo(xs[q][r]), bf16_lo(wv[q][r]), acc);
-        acc = __builtin_fmaf(bf16_hi(xs[q][r]), bf16_hi(wv[q][r]), acc);
+        acc = __builtin_fmaf(bf16_lo(xv[q][r]), bf16_lo(wv[q][r]), acc);
+        acc = __builtin_fmaf(bf16_hi(xv[q][r]), bf16_hi(wv[q][r]), acc);
       }
   };
-  if (0 < nb) issue(0, xv[0]);
-  for (int b = 0; b < nb; b += CH_P) {
-    step(b, xv[0], xv[1]);
-    if (b + 1 >= nb) break;
-    step(b + 1, xv[1], xv[0]);
-  }
+  for (int b = 0; b < NP - 1 && b < nb; ++b) issue(b);
+  for (int b = 0; b < nb; ++b) step(b);
   if (live) a.ch_l[i] = a.bias ? acc + a.bias[e] : acc;
-  // the next range refills every stage
-  __builtin_amdgcn_s_barrier();
-  gemm::compiler_fence();
+  // the next range refills every stage and rewrites the slot table
+  __syncthreads();
 }
 
 // Persistent over the ranges of CH_W chains (the chain count is known only
-// on the device).
-__global__ void __launch_bounds__(CH_W, 4) gate_chain_staged_kernel(GateArgs a) {  // 4 waves per SIMD: two workgroups per CU
-  static_assert(CH_P == 2 && CH_E % (8 * (CH_W / WAVE)) == 0, "chain staging geometry");
-  __shared__ __attribute__((aligned(1024))) char ring[CH_P * CH_E * 2 * CH_K];
+// on the device).  Two workgroups per CU: 4 wavefronts per SIMD.
+template <int CX, int NP>
+__global__ void __launch_bounds__(CH_W, 4) gate_chain_staged_kernel(GateArgs a) {
+  static_assert(CH_E % (8 * CH_NW) == 0, "gate rows per DMA round");
+  __shared__ __attribute__((aligned(1024))) char ring[NP * ChainGeo<CX, NP>::STAGE];
+  __shared__ int tok[CX];
+  __shared__ int wsum[CH_NW];
   const int n = a.stats[ST_CANDS];
-  for (int c0 = blockIdx.x * CH_W; c0 < n; c0 += gridDim.x * CH_W) chain_range(a, ring, c0, n);
+  for (int c0 = blockIdx.x * CH_W; c0 < n; c0 += gridDim.x * CH_W) chain_range<CX, NP>(a, ring, tok, wsum, c0, n);
 }
+
+template __global__ void gate_chain_staged_kernel<72, 3>(GateArgs);
+template __global__ void gate_chain_staged_kernel<136, 2>(GateArgs);
 
 // top-k of the candidates' defined logits (descending, equal logits ->
 // smaller id), one lane per token keeping a sorted list of the k best, then
