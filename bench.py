@@ -63,7 +63,10 @@ def parse():
     ap.add_argument("--no-stack", action="store_true",
                     help="run the layers of a timed step as one launch per layer (default: one stacked launch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=2, help="oracle rows per rank and layer, single-thread leg")
+    ap.add_argument("--cpu-rows", type=int, default=8, help="oracle rows per rank and layer, single-thread leg")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="wall time the host-cores leg of the CPU baseline is sized for")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the dense-GEMM ceiling measurement")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain torch copy of this many MiB (the scale for PMC byte counters)")
     return ap.parse_args()
@@ -289,6 +292,47 @@ def layer_flops(shape, stats):
     return (int(stats[0]) + shape.n_shared_experts * shape.tokens_per_rank) * 6.0 * shape.hidden * shape.ffn
 
 
+def dense_ceiling(shape, rows: int, reps: int = 5):
+    """The library bf16 GEMM (hipBLASLt through torch.matmul) on dense GEMMs
+    of the layer's two expert products with all `rows` routed rows stacked:
+    [rows, H] x [H, 2F] (gate and up) and [rows, F] x [F, H] (down), operands
+    drawn like the layer's (x ~ N(0,1), weights ~ N(0, 0.02^2)).  The part is
+    power-limited, and MFMA power depends on the operand bits, so this rate,
+    not the nominal peak, is what a bf16 GEMM of these shapes reaches on this
+    GPU.  Returns TFLOP/s of each product and of the two together."""
+    import numpy as np
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1234)
+    H, F = shape.hidden, shape.ffn
+    m = max(256, rows // 256 * 256)
+
+    def rate(M, K, N):
+        a = torch.randn(M, K, device="cuda", dtype=torch.float32, generator=g).to(torch.bfloat16)
+        b = (torch.randn(K, N, device="cuda", dtype=torch.float32, generator=g) * 0.02).to(torch.bfloat16)
+        for _ in range(2):
+            torch.matmul(a, b)
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            torch.matmul(a, b)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        del a, b
+        return float(np.median(ts))
+
+    t0 = rate(m, H, 2 * F)
+    t1 = rate(m, F, H)
+    torch.cuda.empty_cache()
+    f0, f1 = 4.0 * m * H * F, 2.0 * m * F * H
+    return {"what": "torch.matmul (hipBLASLt) bf16 on the dense GEMMs of one layer's routed rows stacked: "
+                    "[rows,H]x[H,2F] and [rows,F]x[F,H], random operands of the layer's distributions",
+            "rows": m, "gemm0_tflops": f0 / t0 / 1e12, "gemm1_tflops": f1 / t1 / 1e12,
+            "tflops": (f0 + f1) / (t0 + t1) / 1e12}
+
+
 def host_info():
     model = ""
     try:
@@ -303,15 +347,17 @@ def host_info():
     return {"cpu_model": model, "nproc": os.cpu_count(), "affinity_cpus": aff}
 
 
-def cpu_baseline(stack, W, per_rank, cores):
+def cpu_baseline(stack, W, per_rank, cores, seconds):
     """The oracle as it stands on a bounded sample, timed on the host: for
     `per_rank` seeded tokens of each source rank and every layer of the stack,
     routing (gate logits, softmax, top-k of those rows: rows are independent)
-    and the layer's output rows.  First on one thread, then `cores` threads
-    on `cores` times as many rows (the C oracle releases the interpreter lock,
-    so the threads run in parallel).  tokens/s = sampled tokens through all
-    layers / wall time.  Returns the baseline and the oracle's rows of the
-    single-thread leg (for the check against the GPU)."""
+    and the layer's output rows.  First on one thread, then on `cores`
+    threads, each taking its own rows (the C oracle releases the interpreter
+    lock, so the threads run in parallel), with as many rows as the
+    single-thread rate says fill about `seconds` of wall time.  tokens/s =
+    sampled tokens through all layers / wall time.  Returns the baseline and
+    the oracle's rows of the single-thread leg (for the check against the
+    GPU)."""
     import numpy as np
     from concurrent.futures import ThreadPoolExecutor
     from oracle import oracle as O
@@ -338,8 +384,12 @@ def cpu_baseline(stack, W, per_rank, cores):
     ref = [run_rows(i, rows) for i, rows in enumerate(samples)]
     t1 = time.perf_counter() - t0
     n1 = len(samples[0])
-    # host cores: each thread takes its own rows of every layer
-    big = [W.sample_tokens(shape, min(Tr, per_rank * cores), seed=1900 + l) for l in stack.ids]
+    # host cores: each thread takes its own rows of every layer, sized from
+    # the single-thread rate to about `seconds` of wall time
+    rate1 = len(samples[0]) / t1
+    mt_rank = int(rate1 * cores * seconds / shape.n_src_ranks)
+    mt_rank = max(per_rank, min(Tr, (mt_rank // cores) * cores))
+    big = [W.sample_tokens(shape, mt_rank, seed=1900 + l) for l in stack.ids]
     shards = [[(i, b[c::cores]) for i, b in enumerate(big)] for c in range(cores)]
     t0 = time.perf_counter()
     with ThreadPoolExecutor(cores) as ex:
@@ -535,10 +585,16 @@ def main():
         "context": "paper: 2.89x geomean MoE-layer speedup on 4xH100 SXM, EP=4, BF16 - different hardware and "
                    "baselines, not a target",
     }
+    if not args.no_ceiling:
+        rows = int(round(summary["stack_flops"] / n / (6.0 * shape.hidden * shape.ffn)))
+        ceil = dense_ceiling(shape, rows)
+        ceil["megakernel_frac_of_ceiling"] = achieved / ceil["tflops"]
+        out["roofline"]["ceiling"] = ceil
+        log(f"dense GEMM ceiling: {ceil['tflops']:.0f} TFLOP/s; megakernel at {achieved:.0f}")
     if want_cpu:
         log("oracle CPU baseline")
         cores = max(1, min(16, host_info()["affinity_cpus"]))
-        base, samples, ref = cpu_baseline(stack, W, args.cpu_rows, cores)
+        base, samples, ref = cpu_baseline(stack, W, args.cpu_rows, cores, args.cpu_seconds)
         out["cpu_baseline"] = base
         out["y_check"] = y_check(stack, samples, ref)
         log(f"y check: {out['y_check']}")

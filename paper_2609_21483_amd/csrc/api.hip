@@ -153,6 +153,7 @@ struct moe_handle {
   size_t off_calib = 0, off_blk_cnt = 0, off_blk_off = 0, off_blk_bad = 0, off_rbnd = 0, off_ctl[2] = {0, 0};
   size_t off_part = 0;
   size_t off_gate = 0;  // the gate's scratch (gate_layout)
+  size_t off_sched = 0;  // schedule images, one per K option (sched_build_kernel)
   char* ws = nullptr;
   size_t ws_bytes = 0;
   const int32_t* tables_from = nullptr;
@@ -306,6 +307,7 @@ void compute_layout(moe_handle* h) {
   L.err = take(sizeof(int32_t) * 4);
   h->off_calib = take(sizeof(DevCalib));
   h->off_gate = take(gate_layout(T, c.hidden, c.n_experts).total);
+  h->off_sched = take(sizeof(int32_t) * (size_t)KOPT * SCHED_WORDS);
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
@@ -415,11 +417,12 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.topk_idx = topk_idx;
   a.topk_w = topk_w;
   a.w13 = static_cast<const uint16_t*>(packed);
-  a.w2t = a.w13 + (size_t)h->nseg * slab_rows(2 * c.ffn) * c.hidden;
+  a.w2t = a.w13 ? a.w13 + (size_t)h->nseg * slab_rows(2 * c.ffn) * c.hidden : nullptr;
   a.y = y;
   a.slot = at<int32_t>(h, h->lay.slot);
   a.sub_off = at<int32_t>(h, h->lay.sub_off);
   a.row_off = at<int32_t>(h, h->lay.row_off);
+  a.sched = at<int32_t>(h, h->off_sched);
   a.stats = at<int32_t>(h, h->lay.stats);
   a.A = at<uint16_t>(h, h->lay.A);
   a.Hb = at<uint16_t>(h, h->lay.Hbuf);
@@ -661,6 +664,8 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
   tab_scan_kernel<<<1, TAB_SCAN_THREADS, 0, s>>>(a);
   tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_finalize_kernel<<<1, NTH, 0, s>>>(a);
+  // the launches' schedules for every chunk option, from these tables
+  sched_build_kernel<<<KOPT, FNTH, 0, s>>>(fwd_args(h, nullptr, topk_idx, nullptr, nullptr, nullptr, MOE_MODE_DYNAMIC, nullptr));
   HIP_TRY(hipGetLastError());
   h->tables_from = topk_idx;
   return MOE_OK;

@@ -33,22 +33,7 @@ constexpr int NWF = FNTH / WAVE;  // waves per forward workgroup
 // tiles, then GEMM1 tiles), then segment; inside a group the row tile runs
 // fastest (GEMM1: the split runs fastest, then the row tile).
 // ===========================================================================
-struct Sched {
-  int K, nseg, G;        // chunks, segments, groups = K*2*nseg
-  int n_comp, n_disp, n_comb;
-  int disp0;             // dispatch units [0, disp0) are owned statically (megakernel)
-  int c, n_steal, final_all;
-  int bnd[MAX_K + 1];    // chunk token boundaries ceil(q*T/K)
-  // per (chunk q, segment) at index q*nseg + seg
-  int rows[MAX_K * MAX_SEG];
-  int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts), a 32-row group boundary
-  int sbase[MAX_K * MAX_SEG];  // first slot (local expert) or token (shared expert) of the segment
-  int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A row or token)
-  int mb[MAX_K * MAX_SEG];     // first row-tile id (counter index)
-  int lvl[MAX_K][NLVL + 1];    // row tiles of chunk q at readiness level <= L
-  int gstart[MAX_K * 2 * MAX_SEG + 1];
-  int ncls[2 * MAX_K][NXCD];   // tiles of stage (chunk, phase) in slab class x
-};
+
 
 struct Scratch {
   int bc[8];
@@ -199,6 +184,19 @@ __device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, co
   block_exscan(S.mb, K * nseg, W.part);
   block_exscan(S.gstart, S.G + 1, W.part);
   if (tid == 0) S.n_comp = S.gstart[S.G];
+  __syncthreads();
+}
+
+// A launch's schedule for chunk count K: the stored image (built by
+// sched_build_kernel when the routing tables were) copied into S after the
+// plan fields, which it leaves alone.  All threads call; ends with a barrier.
+__device__ __forceinline__ void load_sched(const FwdArgs& a, Sched& S, int K) {
+  const int32_t* src = a.sched + (size_t)kopt_index(K) * SCHED_WORDS;
+  int* dst = reinterpret_cast<int*>(&S);
+  constexpr int N4 = (SCHED_WORDS - SCHED_IMG0) / 4;
+  static_assert(SCHED_IMG0 % 4 == 0 && SCHED_WORDS % 4 == 0, "16-byte copies");
+  for (int i = threadIdx.x; i < N4; i += FNTH)
+    reinterpret_cast<u32x4_t*>(dst + SCHED_IMG0)[i] = reinterpret_cast<const u32x4_t*>(src + SCHED_IMG0)[i];
   __syncthreads();
 }
 
@@ -823,38 +821,113 @@ __device__ __forceinline__ bool arrive_and_reduce(const FwdArgs& a, const Sched&
 // ===========================================================================
 // sub: the chunk sub-offset tables staged in LDS (see moe_megakernel); the
 // calibration table is staged here, in the same round trip.
+// Wavefront argmin of (t, i) (lanes with i < 0 hold no point): the smallest
+// t, the lowest i among equal ones, with n carried along; lane 0 ends with
+// the result.  DPP exchanges within each row of 16 lanes (xor 1, xor 2, then
+// the half-row and row mirrors, each pairing the lanes of two disjoint halves),
+// then the four rows' results through readlane.  The order of the minimum
+// with its index tie-break is total, so the pairing order does not matter.
+__device__ __forceinline__ void argmin_take(double& t, int& i, int& n, double t2, int i2, int n2) {
+  if (i2 >= 0 && (i < 0 || t2 < t || (t2 == t && i2 < i))) {
+    t = t2;
+    i = i2;
+    n = n2;
+  }
+}
+template <int CTRL>
+__device__ __forceinline__ void argmin_dpp_step(double& t, int& i, int& n) {
+  const uint64_t b = (uint64_t)__builtin_bit_cast(uint64_t, t);
+  const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)b, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
+  const int i2 = __builtin_amdgcn_mov_dpp(i, CTRL, 0xF, 0xF, false);
+  const int n2 = __builtin_amdgcn_mov_dpp(n, CTRL, 0xF, 0xF, false);
+  const double t2 = __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+  argmin_take(t, i, n, t2, i2, n2);
+}
+__device__ __forceinline__ void wave_argmin(double& t, int& i, int& n) {
+  argmin_dpp_step<0xB1>(t, i, n);   // quad_perm [1, 0, 3, 2]
+  argmin_dpp_step<0x4E>(t, i, n);   // quad_perm [2, 3, 0, 1]
+  argmin_dpp_step<0x141>(t, i, n);  // row_half_mirror
+  argmin_dpp_step<0x140>(t, i, n);  // row_mirror
+  const uint64_t b = (uint64_t)__builtin_bit_cast(uint64_t, t);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, 16 * r);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), 16 * r);
+    const int i2 = __builtin_amdgcn_readlane(i, 16 * r);
+    const int n2 = __builtin_amdgcn_readlane(n, 16 * r);
+    argmin_take(t, i, n, __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo), i2, n2);
+  }
+}
+
 __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   const int tid = threadIdx.x;
   {
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(a.calib);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(&W.cal);
-    for (int i = tid; i < (int)(sizeof(DevCalib) / 4); i += FNTH) dst[i] = src[i];
-    if (tid >= FNTH - ST_WORDS) W.st[tid - (FNTH - ST_WORDS)] = a.stats[tid - (FNTH - ST_WORDS)];
+    // one memory round trip for the calibration table, the routing stats
+    // and the schedule image for K = 1 (the usual pick; another K is loaded
+    // once the plan has chosen it): every load is issued before the first
+    // store to LDS
+    constexpr int NCW = (int)(sizeof(DevCalib) / 4);
+    constexpr int NC = (NCW + FNTH - 1) / FNTH;
+    constexpr int NIV = (SCHED_WORDS - SCHED_IMG0) / 4;
+    constexpr int NI = (NIV + FNTH - 1) / FNTH;
+    const uint32_t* csrc = reinterpret_cast<const uint32_t*>(a.calib);
+    const u32x4_t* isrc = reinterpret_cast<const u32x4_t*>(a.sched + SCHED_IMG0);
+    uint32_t cv[NC];
+    u32x4_t iv[NI];
+    int sv = 0;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) cv[j] = tid + j * FNTH < NCW ? csrc[tid + j * FNTH] : 0u;
+    if (tid >= FNTH - ST_WORDS) sv = a.stats[tid - (FNTH - ST_WORDS)];
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+      if (tid + j * FNTH < NIV) iv[j] = isrc[tid + j * FNTH];
+    uint32_t* cdst = reinterpret_cast<uint32_t*>(&W.cal);
+#pragma unroll
+    for (int j = 0; j < NC; ++j)
+      if (tid + j * FNTH < NCW) cdst[tid + j * FNTH] = cv[j];
+    if (tid >= FNTH - ST_WORDS) W.st[tid - (FNTH - ST_WORDS)] = sv;
+    u32x4_t* idst = reinterpret_cast<u32x4_t*>(reinterpret_cast<int*>(&S) + SCHED_IMG0);
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+      if (tid + j * FNTH < NIV) idst[tid + j * FNTH] = iv[j];
   }
   __syncthreads();
   const bool model = !a.forced && a.mode != MOE_MODE_STATIC;
-  double wc = 0.0, wd = 0.0, wb = 0.0, best = 0.0;
-  int bi = 0;
+  moe_plan p;
   if (model && tid < WAVE) {
-    // Eq 15 at every grid point, one point per lane of the first wavefront;
-    // Eq 16 by a wavefront reduction in the host model's order (c ascending,
-    // then K): the smallest T_total, the lowest grid index among equal ones,
-    // which is the first strict minimum of the host's scan
+    // Eq 15 at every grid point, one point per lane of the first wavefront,
+    // with its steal count (Eq 11-14) alongside; Eq 16 by a wavefront
+    // argmin in the host model's order (c ascending, then K): the smallest
+    // T_total, the lowest grid index among equal ones, which is the first
+    // strict minimum of the host's scan
+    double wc, wd, wb;
     cm_volumes(W.st, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
     const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
-    bi = -1;
+    double best = 0.0;
+    int bi = -1;
     for (int i = tid; i < npt; i += WAVE) {
       const double t = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
       if (bi < 0 || t < best) { best = t; bi = i; }
     }
-    for (int d = 1; d < WAVE; d <<= 1) {
-      const double ob = __shfl_xor(best, d, WAVE);
-      const int oi = __shfl_xor(bi, d, WAVE);
-      if (oi >= 0 && (bi < 0 || ob < best || (ob == best && oi < bi))) { best = ob; bi = oi; }
+    int ns = 0;
+    if (bi >= 0) {
+      long long nt_by_k[MOE_CALIB_MAX_K];
+      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.st[ST_NTK + kopt_index(W.cal.kk[j])];
+      moe_plan q;
+      cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &q);
+      ns = q.n_steal;
+    }
+    wave_argmin(best, bi, ns);
+    if (tid == 0) {
+      p.c = W.cal.c[bi / nk];
+      p.K = W.cal.kk[bi - (bi / nk) * nk];
+      p.n_steal = ns;
+      p.final_all = 1;
+      p.t_pred_s = best;
     }
   }
   if (tid == 0) {
-    moe_plan p;
     if (a.forced) {
       p = a.fplan;
     } else if (a.mode == MOE_MODE_STATIC) {
@@ -863,14 +936,9 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
       p.n_steal = 0;
       p.final_all = 0;
       p.t_pred_s = 0.0;
-    } else {
-      const int nk = W.cal.n_k;
-      long long nt_by_k[MOE_CALIB_MAX_K];
-      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.st[ST_NTK + kopt_index(W.cal.kk[j])];
-      cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &p);
     }
     S.c = p.c;
-    S.K = p.K;
+    W.bc[5] = p.K;
     S.n_steal = p.n_steal;
     S.final_all = p.final_all;
     if (blockIdx.x == 0) *a.plan_out = p;
@@ -1071,21 +1139,14 @@ __device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& 
     W.dexh = 0;
   }
 
-  // the chunk sub-offset and row-map tables, staged in the GEMM ring (idle
-  // until the first tile) so that the schedule reads them from LDS
-  static_assert(KOPT * (2 * MAX_EL + MAX_S) * SUBW * (int)sizeof(int) <= gemm::RING_BYTES,
-                "sub-offset and row-map tables fit the ring");
-  int* sub = reinterpret_cast<int*>(ring);
-  int* rof = sub + KOPT * a.El * SUBW;
-  for (int i = tid; i < KOPT * a.El * SUBW; i += FNTH) sub[i] = a.sub_off[i];
-  for (int i = tid; i < KOPT * (a.El + a.S) * SUBW; i += FNTH) rof[i] = a.row_off[i];
-  if (tid == 0) W.bc[0] = tk;
   prologue_plan(a, S, W);
-  build_sched(a, sub, rof, S, W, S.K);
+  if (W.bc[5] != 1) load_sched(a, S, W.bc[5]);  // K = 1's image came with the calibration
 
   if (tid < NWF) W.tcnt[tid] = 0;
   if (tid == 0) {
-    W.ticket = W.bc[0];
+    // the ticket's round trip overlapped the plan
+    W.bc[0] = tk;
+    W.ticket = tk;
     S.disp0 = a.static_disp ? min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF) : 0;
   }
   __syncthreads();
@@ -1167,6 +1228,18 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel_stack(StackArgs st) {
 // ===========================================================================
 // Serial baseline: four kernels, each on every CU, no overlap.
 // ===========================================================================
+// The schedule images of the routing tables just built: workgroup ki builds
+// the schedule for K = 2^ki in LDS and stores it.
+__global__ void __launch_bounds__(FNTH, 1) sched_build_kernel(FwdArgs a) {
+  __shared__ Sched S;
+  __shared__ Scratch W;
+  const int ki = blockIdx.x;
+  build_sched(a, a.sub_off, a.row_off, S, W, 1 << ki);
+  const int* src = reinterpret_cast<const int*>(&S);
+  int32_t* dst = const_cast<int32_t*>(a.sched) + (size_t)ki * SCHED_WORDS;  // the images' one writer
+  for (int i = SCHED_IMG0 + threadIdx.x; i < SCHED_WORDS; i += FNTH) dst[i] = src[i];
+}
+
 __global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {
   __shared__ Scratch W;
   const int tid = threadIdx.x;
@@ -1180,7 +1253,7 @@ __device__ __forceinline__ void serial_gemm(const FwdArgs& a) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
-  build_sched(a, a.sub_off, a.row_off, S, W, a.serial_K);
+  load_sched(a, S, a.serial_K);
   const int home = xcd_id() & (NXCD - 1);
   int stage = 0;
   uint32_t exhausted = 0;

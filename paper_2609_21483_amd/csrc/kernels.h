@@ -79,6 +79,34 @@ struct DevCalib {
   int32_t steal_ceil;    // Eq 14's share rounded up (1) or down (0)
 };
 
+// Schedule of one launch for chunk count K (section 4, the chunk-pipeline DAG
+// order): segment seg < E_l is local expert seg, seg >= E_l shared expert
+// seg - E_l.  Queue order: chunk, then phase (GEMM0 tiles, then GEMM1 tiles),
+// then segment; inside a group the row tile runs fastest (GEMM1: the split
+// runs fastest, then the row tile).  Everything from K on depends only on the
+// routing tables and the handle, so the routing's last kernel
+// (sched_build_kernel) stores it once per K option as an image that a
+// launch's prologue copies into LDS once its plan has picked K; the plan
+// fields come first and are not part of the image.
+struct Sched {
+  int c, n_steal, final_all;  // the plan
+  int disp0;                  // dispatch units [0, disp0) are owned statically (megakernel)
+  int K, nseg, G;             // chunks, segments, groups = K*2*nseg
+  int n_comp, n_disp, n_comb;
+  int bnd[MAX_K + 1];         // chunk token boundaries ceil(q*T/K)
+  // per (chunk q, segment) at index q*nseg + seg
+  int rows[MAX_K * MAX_SEG];
+  int row0[MAX_K * MAX_SEG];   // first row in Hbuf / O (and in A for local experts), a 32-row group boundary
+  int sbase[MAX_K * MAX_SEG];  // first slot (local expert) or token (shared expert) of the segment
+  int arow0[MAX_K * MAX_SEG];  // first row of the GEMM0 A operand (A row or token)
+  int mb[MAX_K * MAX_SEG];     // first row-tile id (counter index)
+  int lvl[MAX_K][NLVL + 1];    // row tiles of chunk q at readiness level <= L
+  int gstart[MAX_K * 2 * MAX_SEG + 1];
+  int ncls[2 * MAX_K][NXCD];   // tiles of stage (chunk, phase) in slab class x
+};
+constexpr int SCHED_WORDS = (int)(sizeof(Sched) / 4);  // int32 words of a stored image slot
+constexpr int SCHED_IMG0 = 4;                          // first word of the image (K)
+
 struct FwdArgs {
   // shape
   int T, Tr, R, H, F, k, El, S, e0, N;
@@ -102,6 +130,7 @@ struct FwdArgs {
   const int32_t* slot;
   const int32_t* sub_off;
   const int32_t* row_off;  // [KOPT][E_l + S][SUBW] first row of each (segment, chunk) in A / Hbuf / O
+  const int32_t* sched;    // [KOPT][SCHED_WORDS] schedule images (written by sched_build_kernel), K = 1, 2, 4, 8
   const int32_t* stats;
   // intermediate buffers
   uint16_t* A;
@@ -261,6 +290,7 @@ __global__ void pack_transpose_kernel(PackArgs a);
 __global__ void pack_pad_kernel(PadArgs a);
 __global__ void moe_megakernel(FwdArgs a);
 __global__ void moe_megakernel_stack(StackArgs st);
+__global__ void sched_build_kernel(FwdArgs a);  // one workgroup per K option
 __global__ void serial_dispatch_kernel(FwdArgs a);
 __global__ void serial_gemm0_kernel(FwdArgs a);
 __global__ void serial_gemm1_kernel(FwdArgs a);
