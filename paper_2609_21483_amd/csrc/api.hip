@@ -154,6 +154,7 @@ struct moe_handle {
   size_t off_part = 0;
   size_t off_gate = 0;  // the gate's scratch (gate_layout)
   size_t off_sched = 0;  // schedule images, one per K option (sched_build_kernel)
+  uint32_t calib_gen = 1;  // bumped by every moe_set_calib (a stored plan of an older table is stale)
   char* ws = nullptr;
   size_t ws_bytes = 0;
   const int32_t* tables_from = nullptr;
@@ -307,7 +308,7 @@ void compute_layout(moe_handle* h) {
   L.err = take(sizeof(int32_t) * 4);
   h->off_calib = take(sizeof(DevCalib));
   h->off_gate = take(gate_layout(T, c.hidden, c.n_experts).total);
-  h->off_sched = take(sizeof(int32_t) * (size_t)KOPT * SCHED_WORDS);
+  h->off_sched = take(sizeof(int32_t) * (size_t)KOPT * SCHED_WORDS + sizeof(StoredPlan));
   h->off_blk_cnt = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_off = take(sizeof(int32_t) * (size_t)h->nblk * El);
   h->off_blk_bad = take(sizeof(int32_t) * (size_t)h->nblk);
@@ -423,6 +424,7 @@ FwdArgs fwd_args(moe_handle* h, const uint16_t* x, const int32_t* topk_idx, cons
   a.sub_off = at<int32_t>(h, h->lay.sub_off);
   a.row_off = at<int32_t>(h, h->lay.row_off);
   a.sched = at<int32_t>(h, h->off_sched);
+  a.calib_gen = h->calib_gen;
   a.stats = at<int32_t>(h, h->lay.stats);
   a.A = at<uint16_t>(h, h->lay.A);
   a.Hb = at<uint16_t>(h, h->lay.Hbuf);
@@ -551,6 +553,7 @@ moe_status moe_set_calib(moe_handle* h, const moe_calib* calib) {
   if (st != MOE_OK) return st;
   h->calib = *calib;
   to_dev(h->calib, &h->dcal);
+  h->calib_gen++;
   if (h->ws) HIP_TRY(hipMemcpy(h->ws + h->off_calib, &h->dcal, sizeof(DevCalib), hipMemcpyHostToDevice));
   return MOE_OK;
 }

@@ -860,8 +860,48 @@ __device__ __forceinline__ void wave_argmin(double& t, int& i, int& n) {
   }
 }
 
+__device__ __forceinline__ const StoredPlan* stored_plan(const FwdArgs& a) {
+  return reinterpret_cast<const StoredPlan*>(a.sched + (size_t)KOPT * SCHED_WORDS);
+}
+
+// The cost model's plan on the first wavefront (all 64 lanes call; lane 0
+// ends with it in p): Eq 15 at every grid point, one point per lane, with its
+// steal count (Eq 11-14) alongside; Eq 16 by a wavefront argmin in the host
+// model's order (c ascending, then K): the smallest T_total, the lowest grid
+// index among equal ones, which is the first strict minimum of the host's
+// scan.  W.cal and W.st hold the calibration table and the routing stats.
+__device__ __forceinline__ void model_plan(const FwdArgs& a, const Scratch& W, moe_plan& p) {
+  const int tid = threadIdx.x;
+  double wc, wd, wb;
+  cm_volumes(W.st, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
+  const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
+  double best = 0.0;
+  int bi = -1;
+  for (int i = tid; i < npt; i += WAVE) {
+    const double t = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
+    if (bi < 0 || t < best) { best = t; bi = i; }
+  }
+  int ns = 0;
+  if (bi >= 0) {
+    long long nt_by_k[MOE_CALIB_MAX_K];
+    for (int j = 0; j < nk; ++j) nt_by_k[j] = W.st[ST_NTK + kopt_index(W.cal.kk[j])];
+    moe_plan q;
+    cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &q);
+    ns = q.n_steal;
+  }
+  wave_argmin(best, bi, ns);
+  if (tid == 0) {
+    p.c = W.cal.c[bi / nk];
+    p.K = W.cal.kk[bi - (bi / nk) * nk];
+    p.n_steal = ns;
+    p.final_all = 1;
+    p.t_pred_s = best;
+  }
+}
+
 __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratch& W) {
   const int tid = threadIdx.x;
+  StoredPlan sp{};  // thread 0: the stored plan, read in the same round trip
   {
     // one memory round trip for the calibration table, the routing stats
     // and the schedule image for K = 1 (the usual pick; another K is loaded
@@ -879,6 +919,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
 #pragma unroll
     for (int j = 0; j < NC; ++j) cv[j] = tid + j * FNTH < NCW ? csrc[tid + j * FNTH] : 0u;
     if (tid >= FNTH - ST_WORDS) sv = a.stats[tid - (FNTH - ST_WORDS)];
+    if (tid == 0) sp = *stored_plan(a);
 #pragma unroll
     for (int j = 0; j < NI; ++j)
       if (tid + j * FNTH < NIV) iv[j] = isrc[tid + j * FNTH];
@@ -887,6 +928,7 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
     for (int j = 0; j < NC; ++j)
       if (tid + j * FNTH < NCW) cdst[tid + j * FNTH] = cv[j];
     if (tid >= FNTH - ST_WORDS) W.st[tid - (FNTH - ST_WORDS)] = sv;
+    if (tid == 0) W.bc[6] = sp.gen == a.calib_gen ? 1 : 0;
     u32x4_t* idst = reinterpret_cast<u32x4_t*>(reinterpret_cast<int*>(&S) + SCHED_IMG0);
 #pragma unroll
     for (int j = 0; j < NI; ++j)
@@ -895,40 +937,13 @@ __device__ __forceinline__ void prologue_plan(const FwdArgs& a, Sched& S, Scratc
   __syncthreads();
   const bool model = !a.forced && a.mode != MOE_MODE_STATIC;
   moe_plan p;
-  if (model && tid < WAVE) {
-    // Eq 15 at every grid point, one point per lane of the first wavefront,
-    // with its steal count (Eq 11-14) alongside; Eq 16 by a wavefront
-    // argmin in the host model's order (c ascending, then K): the smallest
-    // T_total, the lowest grid index among equal ones, which is the first
-    // strict minimum of the host's scan
-    double wc, wd, wb;
-    cm_volumes(W.st, a.H, a.F, a.S * a.Tr, W.cal.literal, &wc, &wd, &wb);
-    const int nk = W.cal.n_k, npt = W.cal.n_c * nk;
-    double best = 0.0;
-    int bi = -1;
-    for (int i = tid; i < npt; i += WAVE) {
-      const double t = cm_t_total(W.cal, i / nk, i - (i / nk) * nk, wc, wd, wb);
-      if (bi < 0 || t < best) { best = t; bi = i; }
-    }
-    int ns = 0;
-    if (bi >= 0) {
-      long long nt_by_k[MOE_CALIB_MAX_K];
-      for (int j = 0; j < nk; ++j) nt_by_k[j] = W.st[ST_NTK + kopt_index(W.cal.kk[j])];
-      moe_plan q;
-      cm_finish(W.cal, a.N, wc, wd, wb, nt_by_k, bi / nk, bi - (bi / nk) * nk, best, &q);
-      ns = q.n_steal;
-    }
-    wave_argmin(best, bi, ns);
-    if (tid == 0) {
-      p.c = W.cal.c[bi / nk];
-      p.K = W.cal.kk[bi - (bi / nk) * nk];
-      p.n_steal = ns;
-      p.final_all = 1;
-      p.t_pred_s = best;
-    }
-  }
+  // the plan the routing's last kernel evaluated on these tables, when the
+  // calibration has not changed since (W.bc[6]); else evaluated here
+  if (model && !W.bc[6] && tid < WAVE) model_plan(a, W, p);
   if (tid == 0) {
-    if (a.forced) {
+    if (model && W.bc[6]) {
+      p = sp.p;
+    } else if (a.forced) {
       p = a.fplan;
     } else if (a.mode == MOE_MODE_STATIC) {
       p.c = W.cal.static_c;
@@ -1103,6 +1118,10 @@ __device__ __forceinline__ bool wave_wait_all(const FwdArgs& a, const int* p, in
 // waits only for the row tiles its tokens' rows come from, so the combine of
 // finished tokens starts while the last GEMM tiles run.
 __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S, Scratch& W, int ticket) {
+  // at most one wavefront per unit joins, the lowest arrival tickets first
+  // (movement workers before compute workers): with fewer units than
+  // wavefronts the others' claims could only fail, on the same few counters
+  if (ticket * NWF + wave_id() >= S.n_comb) return true;
   int shard = first_shard(W);
   for (;;) {
     const int u = claim_unit(a, CTL_QC, S.n_comb, shard);
@@ -1238,6 +1257,22 @@ __global__ void __launch_bounds__(FNTH, 1) sched_build_kernel(FwdArgs a) {
   const int* src = reinterpret_cast<const int*>(&S);
   int32_t* dst = const_cast<int32_t*>(a.sched) + (size_t)ki * SCHED_WORDS;  // the images' one writer
   for (int i = SCHED_IMG0 + threadIdx.x; i < SCHED_WORDS; i += FNTH) dst[i] = src[i];
+  if (ki != 0) return;
+  // the cost model's plan of these tables under the current calibration
+  // (every workgroup of a launch would evaluate the same; a prologue whose
+  // calibration generation differs evaluates it again)
+  const uint32_t* csrc = reinterpret_cast<const uint32_t*>(a.calib);
+  uint32_t* cdst = reinterpret_cast<uint32_t*>(&W.cal);
+  for (int i = threadIdx.x; i < (int)(sizeof(DevCalib) / 4); i += FNTH) cdst[i] = csrc[i];
+  for (int i = threadIdx.x; i < ST_WORDS; i += FNTH) W.st[i] = a.stats[i];
+  __syncthreads();
+  moe_plan p;
+  if (threadIdx.x < WAVE) model_plan(a, W, p);
+  if (threadIdx.x == 0) {
+    StoredPlan* sp = const_cast<StoredPlan*>(stored_plan(a));
+    sp->p = p;
+    sp->gen = a.calib_gen;
+  }
 }
 
 __global__ void __launch_bounds__(FNTH, 1) serial_dispatch_kernel(FwdArgs a) {

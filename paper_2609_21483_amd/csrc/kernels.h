@@ -105,6 +105,14 @@ struct Sched {
   int ncls[2 * MAX_K][NXCD];   // tiles of stage (chunk, phase) in slab class x
 };
 constexpr int SCHED_WORDS = (int)(sizeof(Sched) / 4);  // int32 words of a stored image slot
+
+// The cost model's plan for the tables the schedule images were built from,
+// evaluated by sched_build_kernel with the calibration of generation `gen`
+// (it follows the images in the workspace).
+struct StoredPlan {
+  moe_plan p;
+  uint32_t gen, pad;
+};
 constexpr int SCHED_IMG0 = 4;                          // first word of the image (K)
 
 struct FwdArgs {
@@ -119,6 +127,7 @@ struct FwdArgs {
   int mt_max;     // capacity of the per-row-tile counters
   int ctl_words;  // int32 words per control set
   int qx, qxs;    // word offsets of the [2 MAX_K][NXCD] tile queue heads (megakernel, serial GEMMs)
+  uint32_t calib_gen;  // generation of the calibration table (a StoredPlan of another one is stale)
   // inputs / output
   const uint16_t* x;
   const int32_t* topk_idx;

@@ -83,3 +83,33 @@ def test_table_builder_tile_counts(B, name):
         assert [int(v) for v in st[10:14]] == [oracle_tiles(B, layer.h, shape, tab, K) for K in (1, 2, 4, 8)]
     finally:
         layer.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "shared_routed"])
+def test_stored_plan_matches_prologue(B, name):
+    """The plan the routing's last kernel stores with the tables and the plan
+    the prologue evaluates itself (after moe_set_calib, which makes the
+    stored one stale) are identical, and both match the oracle's."""
+    shape = W.WORKLOADS[name]
+    c = make_case(shape)
+    idx, w = c.oracle_route()
+    layer = B.MoeLayer(shape, c.w1, c.w3, c.w2, c.ws1, c.ws3, c.ws2)
+    try:
+        x = c.x.cuda()
+        idx_d = torch.from_numpy(idx).cuda()
+        w_d = torch.from_numpy(w.astype(np.float32)).cuda()
+        y = torch.empty((shape.T, shape.hidden), dtype=torch.bfloat16, device="cuda")
+        plans = []
+        for step in ("stored", "recomputed", "stored again"):
+            if step == "recomputed":
+                B.moe_set_calib(layer.h, B.moe_get_calib(layer.h))
+            else:
+                B.moe_build_tables(layer.h, idx_d)
+            layer.forward(x, idx_d, w_d, y, "dynamic")
+            assert B.moe_sync_status(layer.h) == B.MOE_OK
+            p = B.moe_get_plan(layer.h)
+            plans.append((p.as_tuple(), p.t_pred_s))
+            check_plan(B, layer.h, shape, idx)
+        assert plans[0] == plans[1] == plans[2]
+    finally:
+        layer.close()
