@@ -1166,7 +1166,7 @@ __device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& 
     // the ticket's round trip overlapped the plan
     W.bc[0] = tk;
     W.ticket = tk;
-    S.disp0 = a.static_disp ? min(S.n_disp, (a.move_steal ? (int)gridDim.x : S.c) * NWF) : 0;
+    S.disp0 = a.static_disp ? (a.move_steal ? ceil_div(S.bnd[1], a.dt) : min(S.n_disp, S.c * NWF)) : 0;
   }
   __syncthreads();
   const int ticket = __builtin_amdgcn_readfirstlane(W.bc[0]);
@@ -1174,10 +1174,16 @@ __device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& 
   const uint64_t t_sched = a.trace ? now_ticks() : 0;
   __syncthreads();
 
-  // this wavefront's statically owned dispatch unit, if any
+  // this wavefront's statically owned dispatch units, if any: with movement
+  // stealing every unit of the first chunk, round-robin over all wavefronts
+  // (that chunk's dispatch at the full chip's copy rate before the first
+  // tile, whose rows would otherwise wait for units claimed one by one; the
+  // later chunks' units go through the queue, beside the first chunk's
+  // GEMMs); else one unit per wavefront of the movement workers
   {
-    const int u0 = ticket * NWF + wave_id();
-    if (u0 < S.disp0) dispatch_one<true>(a, &S, W, u0, unit_row(a, &S, u0));
+    const int stride = (a.move_steal ? (int)gridDim.x : S.c) * NWF;
+    for (int u0 = ticket * NWF + wave_id(); u0 < S.disp0; u0 += stride)
+      dispatch_one<true>(a, &S, W, u0, unit_row(a, &S, u0));
   }
 
   bool ok = true;
