@@ -27,11 +27,9 @@ namespace moe {
 constexpr int NWF = FNTH / WAVE;  // waves per forward workgroup
 
 // ===========================================================================
-// Schedule of one launch for chunk count K (built by every workgroup in LDS).
-// Segment seg < E_l is local expert seg; seg >= E_l is shared expert seg-E_l.
-// Queue order (section 4, chunk-pipeline DAG order): chunk, then phase (GEMM0
-// tiles, then GEMM1 tiles), then segment; inside a group the row tile runs
-// fastest (GEMM1: the split runs fastest, then the row tile).
+// Schedule of one launch for chunk count K (struct Sched, kernels.h): built
+// once per K option by sched_build_kernel when the routing tables are, and
+// copied into each workgroup's LDS by its prologue.
 // ===========================================================================
 
 
@@ -119,8 +117,8 @@ __device__ __forceinline__ int stage_qph(int s, int K) {
   return (s & 1) ? (j << 1) : (((j - 1) << 1) | 1);
 }
 
-// sub, rof: the chunk sub-offset and row-map tables (a.sub_off and
-// a.row_off, or copies of them in LDS)
+// The schedule for K in S (all threads call; sched_build_kernel's workgroups).
+// sub, rof: the chunk sub-offset and row-map tables (a.sub_off, a.row_off)
 __device__ __forceinline__ void build_sched(const FwdArgs& a, const int* sub, const int* rof, Sched& S, Scratch& W,
                                             int K) {
   const int tid = threadIdx.x;
