@@ -958,13 +958,26 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int* 
       if (j < nxi) gemm::dma16(xb + (size_t)b * (2 * CH_K), xo[j], st + CH_WB + (j * CH_NW + wave) * 1024);
   };
   float acc = 0.0f;
-  const int wrow = e * (2 * CH_K), wsw = chain_swz(e);
-  const int xrow = CH_WB + slot * (2 * CH_K), xsw = chain_swz(slot);
-  // block b: its stage holds this wavefront's loads once at most the blocks
-  // issued after it are outstanding; past the barrier every wavefront's have
-  // landed and every wavefront has added block b - 1, so the stage of block
-  // b + NP - 1 (that of b - 1) is refilled, then block b is added
-  auto step = [&](int b) {
+  // this lane's 16 granule offsets within a stage (its x row and its gate
+  // row, swizzled), computed once: with the stage index a constant (the
+  // block loop below runs NP blocks per iteration) every read is one of
+  // these plus an immediate
+  int xg[8], wg[8];
+  {
+    const int wrow = e * (2 * CH_K), wsw = chain_swz(e);
+    const int xrow = CH_WB + slot * (2 * CH_K), xsw = chain_swz(slot);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      xg[q] = xrow + ((q ^ xsw) << 4);
+      wg[q] = wrow + ((q ^ wsw) << 4);
+    }
+  }
+  // block b, in stage sb = b mod NP: the stage holds this wavefront's loads
+  // once at most the blocks issued after it are outstanding; past the
+  // barrier every wavefront's have landed and every wavefront has added
+  // block b - 1, so the stage of block b + NP - 1 (that of b - 1) is
+  // refilled, then block b is added
+  auto step = [&](int b, int sb) {
     if (NP == 3 && b + 1 < nb) {
       if (nxi == Geo::XI) gemm::wait_vm<CH_DMA + Geo::XI>(); else gemm::wait_vm<CH_DMA + Geo::XI - 1>();
     } else {
@@ -973,12 +986,12 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int* 
     __builtin_amdgcn_s_barrier();
     gemm::compiler_fence();
     if (b + NP - 1 < nb) issue(b + NP - 1);
-    const char* st = ring + (b % NP) * Geo::STAGE;
+    const char* st = ring + sb * Geo::STAGE;
     u32x4_t xv[8], wv[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      xv[q] = *reinterpret_cast<const u32x4_t*>(st + xrow + ((q ^ xsw) << 4));
-      wv[q] = *reinterpret_cast<const u32x4_t*>(st + wrow + ((q ^ wsw) << 4));
+      xv[q] = *reinterpret_cast<const u32x4_t*>(st + xg[q]);
+      wv[q] = *reinterpret_cast<const u32x4_t*>(st + wg[q]);
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q)
@@ -987,9 +1000,18 @@ __device__ __forceinline__ void chain_range(const GateArgs& a, char* ring, int* 
         acc = __builtin_fmaf(bf16_lo(xv[q][r]), bf16_lo(wv[q][r]), acc);
         acc = __builtin_fmaf(bf16_hi(xv[q][r]), bf16_hi(wv[q][r]), acc);
       }
+    // the block's adds complete here, before the next block's barrier (the
+    // compiler would otherwise interleave them with the next block's reads
+    // and hold both blocks' operands at once)
+    asm volatile("" : "+v"(acc));
   };
   for (int b = 0; b < NP - 1 && b < nb; ++b) issue(b);
-  for (int b = 0; b < nb; ++b) step(b);
+  int b = 0;
+  for (; b + NP <= nb; b += NP) {
+#pragma unroll
+    for (int sb = 0; sb < NP; ++sb) step(b + sb, sb);
+  }
+  for (int sb = 0; b < nb; ++b, ++sb) step(b, sb);
   if (live) a.ch_l[i] = a.bias ? acc + a.bias[e] : acc;
   // the next range refills every stage and rewrites the slot table
   __syncthreads();
