@@ -480,6 +480,34 @@ __device__ __forceinline__ void dispatch_claimed(const FwdArgs& a, const Sched& 
   }
 }
 
+__device__ __forceinline__ const StoredPlan* stored_plan(const FwdArgs& a) {
+  return reinterpret_cast<const StoredPlan*>(a.sched + (size_t)KOPT * SCHED_WORDS);
+}
+
+// The chunk count a layer's prologue will pick without evaluating the cost
+// model: the forced plan's, or the plan stored with its routing tables while
+// the calibration is unchanged; 0 when it will evaluate the model (or runs
+// no movement stealing).
+__device__ __forceinline__ int planned_K(const FwdArgs& a) {
+  if (!a.move_steal || a.mode == MOE_MODE_STATIC || a.static_disp) return 0;
+  if (a.forced) return a.fplan.K;
+  const StoredPlan* sp = stored_plan(a);
+  return sp->gen == a.calib_gen ? sp->p.K : 0;
+}
+
+// A later layer of a stacked launch (an): its dispatch units, claimed from
+// its queue by this layer's movement workers while this layer's GEMMs run
+// (they depend on nothing of this layer), with that layer's schedule image
+// read in place; its own workers claim what is left when they arrive.
+__device__ __forceinline__ void dispatch_ahead(const FwdArgs& an, Scratch& W) {
+  const int K = planned_K(an);
+  if (K <= 0) return;
+  const Sched* Sg = reinterpret_cast<const Sched*>(an.sched + (size_t)kopt_index(K) * SCHED_WORDS);
+  const int n_disp = ceil_div(an.T, an.dt);
+  int shard = first_shard(W);
+  for (int u; (u = claim_unit(an, CTL_QD, n_disp, shard)) >= 0;) dispatch_one<true>(an, Sg, W, u, unit_row(an, Sg, u));
+}
+
 __device__ __forceinline__ bool wave_wait_all(const FwdArgs& a, const int* p, int target);
 
 // One wavefront combines nt <= ct tokens.  Each token has KS = k + S source
@@ -858,10 +886,6 @@ __device__ __forceinline__ void wave_argmin(double& t, int& i, int& n) {
   }
 }
 
-__device__ __forceinline__ const StoredPlan* stored_plan(const FwdArgs& a) {
-  return reinterpret_cast<const StoredPlan*>(a.sched + (size_t)KOPT * SCHED_WORDS);
-}
-
 // The cost model's plan on the first wavefront (all 64 lanes call; lane 0
 // ends with it in p): Eq 15 at every grid point, one point per lane, with its
 // steal count (Eq 11-14) alongside; Eq 16 by a wavefront argmin in the host
@@ -1140,8 +1164,9 @@ __device__ __forceinline__ bool combine_claimed(const FwdArgs& a, const Sched& S
 // timeout, so workers that cannot start (the CUs held by other work) turn
 // into MOE_ERR_TIMEOUT, never a hang.
 // ===========================================================================
-// One layer, run by this workgroup.
-__device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& W, char* ring) {
+// One layer, run by this workgroup.  next: the following layer of a
+// stacked launch, whose dispatch the movement workers start.
+__device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& W, char* ring, const FwdArgs* next) {
   const int tid = threadIdx.x;
   const uint64_t t_entry = a.trace ? now_ticks() : 0;
 
@@ -1190,6 +1215,8 @@ __device__ __forceinline__ void mega_layer(const FwdArgs& a, Sched& S, Scratch& 
     dispatch_claimed(a, S, W);
     __syncthreads();
     if (a.trace && tid == 0) trace_rec(a, W, 3, ticket, 0, t_sched, now_ticks(), 0);
+    // the next layer's dispatch beside this layer's GEMMs
+    if (next) dispatch_ahead(*next, W);
     // bubble stealing: n_steal GEMM tiles right after dispatch (section 3.2.2)
     ok = compute_tiles(a, S, W, ring, ticket, S.n_steal);
     if (ok) combine_claimed(a, S, W, ticket);
@@ -1222,7 +1249,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel(FwdArgs a) {
   __shared__ Sched S;
   __shared__ Scratch W;
   __shared__ __attribute__((aligned(1024))) char ring[gemm::RING_BYTES];
-  mega_layer(a, S, W, ring);
+  mega_layer(a, S, W, ring, nullptr);
 }
 
 // Several independent layers (they share x, not their outputs) in one
@@ -1244,7 +1271,7 @@ __global__ void __launch_bounds__(FNTH, 1) moe_megakernel_stack(StackArgs st) {
   const int n = ka->n;
   for (int l = 0; l < n; ++l) {
     __syncthreads();  // the previous layer's LDS state is dead
-    mega_layer(*(const FwdArgs*)&ka->layer[l], S, W, ring);
+    mega_layer(*(const FwdArgs*)&ka->layer[l], S, W, ring, l + 1 < n ? (const FwdArgs*)&ka->layer[l + 1] : nullptr);
   }
 }
 
