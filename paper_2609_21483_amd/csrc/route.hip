@@ -718,42 +718,70 @@ __global__ void __launch_bounds__(2 * NTH) gate_tile2_kernel(GateArgs a) {
       }
   }
   __syncthreads();
-  // candidates, one lane per token: the k largest lower ends (a sorted
-  // list; equal values are all kept, so top[k-1] is the k-th largest)
-  const int t = threadIdx.x;
-  const int g = g0 + t;
-  const bool mine = t < GT_M && g < a.T;
-  float tau = -INFINITY;
-  float xn = 0.0f;
-  int cnt = 0;
+  // candidates, LPT adjacent lanes per token (lane q takes experts
+  // [q * EQ, q * EQ + EQ)): each keeps the k largest lower ends of its
+  // experts in a sorted list (equal values all kept) and the upper ends in
+  // registers; the lists are merged across the token's lanes, so top[k-1] is
+  // the k-th largest lower end over every expert; then the experts whose
+  // upper end reaches it, in expert order
+  constexpr int LPT = 2 * NTH / GT_M, EQ = GT_N / LPT;
+  static_assert(LPT * GT_M == 2 * NTH && (LPT & (LPT - 1)) == 0 && LPT <= WAVE, "lanes per token");
+  const int tq = threadIdx.x / LPT, q = threadIdx.x % LPT;
+  const int g = g0 + tq;
+  const bool mine = g < a.T;
+  float top[MAX_TOPK];
+#pragma unroll
+  for (int j = 0; j < MAX_TOPK; ++j) top[j] = -INFINITY;
+  auto insert = [&](float v) {
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) {
+      const float hi = fmaxf(v, top[j]);
+      v = fminf(v, top[j]);
+      top[j] = hi;
+    }
+  };
+  float up[EQ];
   if (mine) {
-    xn = sqrtf(ssq[0][t] + ssq[1][t]);
-    float top[MAX_TOPK];
+    const float xn = sqrtf(ssq[0][tq] + ssq[1][tq]);
 #pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j) top[j] = -INFINITY;
-    for (int e = 0; e < a.E; ++e) {
-      const float l = tile[t * G2_PAD + e];
-      float d = a.bound * xn * wn_s[e];
-      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
-      float v = l - d;
-#pragma unroll
-      for (int j = 0; j < MAX_TOPK; ++j) {
-        const float hi = fmaxf(v, top[j]);
-        v = fminf(v, top[j]);
-        top[j] = hi;
+    for (int i = 0; i < EQ; ++i) {
+      const int e = q * EQ + i;
+      up[i] = -INFINITY;
+      if (e < a.E) {
+        const float l = tile[tq * G2_PAD + e];
+        float d = a.bound * xn * wn_s[e];
+        d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
+        insert(l - d);
+        up[i] = l + d;
       }
     }
-#pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j)
-      if (j == a.k - 1) tau = top[j];
-    for (int e = 0; e < a.E; ++e) {
-      const float l = tile[t * G2_PAD + e];
-      float d = a.bound * xn * wn_s[e];
-      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
-      cnt += l + d >= tau;
-    }
   }
-  if (t < GT_M) t_cnt[t] = cnt;  // 0 for rows past T
+#pragma unroll
+  for (int m = 1; m < LPT; m <<= 1) {
+    float other[MAX_TOPK];
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) other[j] = __shfl_xor(top[j], m, WAVE);
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j) insert(other[j]);
+  }
+  float tau = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < MAX_TOPK; ++j)
+    if (j == a.k - 1) tau = top[j];
+  int cnt = 0;
+  if (mine) {
+#pragma unroll
+    for (int i = 0; i < EQ; ++i) cnt += (q * EQ + i < a.E && up[i] >= tau) ? 1 : 0;
+  }
+  // this lane's place among its token's candidates, and the token's count
+  int incl = cnt;
+#pragma unroll
+  for (int m = 1; m < LPT; m <<= 1) {
+    const int y = __shfl_up(incl, m, WAVE);
+    if (q >= m) incl += y;
+  }
+  const int ntok = __shfl(incl, (lane | (LPT - 1)), WAVE);
+  if (q == 0) t_cnt[tq] = ntok;  // 0 for rows past T
   __syncthreads();
   if (threadIdx.x < WAVE) {  // exclusive scan of the counts, one atomic for the tile
     int carry = 0;
@@ -772,14 +800,16 @@ __global__ void __launch_bounds__(2 * NTH) gate_tile2_kernel(GateArgs a) {
   }
   __syncthreads();
   if (mine) {
-    int pos = base_s + t_off[t];
-    a.tok_base[g] = pos;
-    a.tok_n[g] = cnt;
-    for (int e = 0; e < a.E; ++e) {
-      const float l = tile[t * G2_PAD + e];
-      float d = a.bound * xn * wn_s[e];
-      d = d + 4.0f * 5.9604645e-8f * (fabsf(l) + d) + 1e-30f;
-      if (l + d >= tau) {
+    const int tb = base_s + t_off[tq];
+    if (q == 0) {
+      a.tok_base[g] = tb;
+      a.tok_n[g] = ntok;
+    }
+    int pos = tb + incl - cnt;
+#pragma unroll
+    for (int i = 0; i < EQ; ++i) {
+      const int e = q * EQ + i;
+      if (e < a.E && up[i] >= tau) {
         a.ch_g[pos] = g;
         a.ch_e[pos] = e;
         ++pos;
