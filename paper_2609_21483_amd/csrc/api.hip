@@ -80,8 +80,10 @@ void bind_gate(GateArgs& g, char* base, const GateLayout& L, int32_t* stats) {
 }
 
 // Top-k routing (gate logits, softmax, top-k, renormalisation) on a bound
-// GateArgs: the certified filter's kernels in order on `s`.
-moe_status launch_gate(GateArgs& g, hipStream_t s) {
+// GateArgs: the certified filter's kernels in order on `s`.  tab: the
+// routing tables to start on the chosen ids (their counting step, done by the
+// last kernel), or null.
+moe_status launch_gate(GateArgs& g, hipStream_t s, const TableArgs* tab) {
   // |L - L~| <= (gamma_{H-1}(2^-24) + gamma_H(2^-23)) * sum_h |x_h w_h|: the
   // defined recursive fp32 sum and an fp32 accumulation of the MFMA products
   // allowed twice the unit roundoff; sum |x w| <= ||x|| ||w||; 1% for the norms
@@ -129,11 +131,17 @@ moe_status launch_gate(GateArgs& g, hipStream_t s) {
   }
   {
     const dim3 grid((g.T + NTH - 1) / NTH);
-    if (g.E <= 16) gate_final_kernel<1><<<grid, NTH, 0, s>>>(g);
-    else if (g.E <= 32) gate_final_kernel<2><<<grid, NTH, 0, s>>>(g);
-    else if (g.E <= 64) gate_final_kernel<4><<<grid, NTH, 0, s>>>(g);
-    else if (g.E <= 128) gate_final_kernel<8><<<grid, NTH, 0, s>>>(g);
-    else gate_final_kernel<32><<<grid, NTH, 0, s>>>(g);
+    const TableArgs t = tab ? *tab : TableArgs{};
+    auto final_ = [&](auto epl) {
+      constexpr int EPL = decltype(epl)::value;
+      if (tab) gate_final_kernel<EPL, true><<<grid, NTH, 0, s>>>(g, t);
+      else gate_final_kernel<EPL, false><<<grid, NTH, 0, s>>>(g, t);
+    };
+    if (g.E <= 16) final_(std::integral_constant<int, 1>{});
+    else if (g.E <= 32) final_(std::integral_constant<int, 2>{});
+    else if (g.E <= 64) final_(std::integral_constant<int, 4>{});
+    else if (g.E <= 128) final_(std::integral_constant<int, 8>{});
+    else final_(std::integral_constant<int, 32>{});
   }
   HIP_TRY(hipGetLastError());
   return MOE_OK;
@@ -657,13 +665,11 @@ moe_status moe_pack_weights(moe_handle* h, const uint16_t* w1, const uint16_t* w
   return MOE_OK;
 }
 
-moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream) {
-  moe_status st = need_ws(h);
-  if (st != MOE_OK) return st;
-  if (!topk_idx) return fail(MOE_ERR_INVALID_ARG, "topk_idx is NULL");
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+// The routing tables' kernels on `s`; counted: the counting step already ran
+// (the routing's last kernel did it on the ids it chose).
+static moe_status launch_tables(moe_handle* h, const int32_t* topk_idx, hipStream_t s, bool counted) {
   TableArgs a = table_args(h, topk_idx);
-  tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
+  if (!counted) tab_count_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_scan_kernel<<<1, TAB_SCAN_THREADS, 0, s>>>(a);
   tab_perm_kernel<<<h->nblk, NTH, 0, s>>>(a);
   tab_finalize_kernel<<<1, NTH, 0, s>>>(a);
@@ -672,6 +678,13 @@ moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream
   HIP_TRY(hipGetLastError());
   h->tables_from = topk_idx;
   return MOE_OK;
+}
+
+moe_status moe_build_tables(moe_handle* h, const int32_t* topk_idx, void* stream) {
+  moe_status st = need_ws(h);
+  if (st != MOE_OK) return st;
+  if (!topk_idx) return fail(MOE_ERR_INVALID_ARG, "topk_idx is NULL");
+  return launch_tables(h, topk_idx, reinterpret_cast<hipStream_t>(stream), false);
 }
 
 moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const float* logit_bias, int32_t top_k,
@@ -693,9 +706,10 @@ moe_status moe_route(moe_handle* h, const uint16_t* x, const uint16_t* wg, const
   g.k = top_k;
   // the chain counter goes to the layer's stats (word ST_CANDS, reported)
   bind_gate(g, h->ws + h->off_gate, gate_layout(g.T, g.H, g.E), at<int32_t>(h, h->lay.stats));
-  st = launch_gate(g, s);
+  const TableArgs ta = table_args(h, topk_idx);
+  st = launch_gate(g, s, &ta);
   if (st != MOE_OK) return st;
-  return moe_build_tables(h, topk_idx, stream);
+  return launch_tables(h, topk_idx, s, true);
 }
 
 moe_status moe_set_trace(moe_handle* h, void* buf, int64_t bytes) {
@@ -905,7 +919,7 @@ moe_status moe_route_topk_static(int32_t T, int32_t H, int32_t E, int32_t top_k,
   // the first kernel of the gate; every other region is written before it
   // is read
   bind_gate(g, base, L, reinterpret_cast<int32_t*>(base + L.stats));
-  return launch_gate(g, reinterpret_cast<hipStream_t>(stream));
+  return launch_gate(g, reinterpret_cast<hipStream_t>(stream), nullptr);
 }
 
 }  // extern "C"

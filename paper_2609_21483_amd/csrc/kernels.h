@@ -287,8 +287,9 @@ __global__ void gate_chain_staged_kernel(GateArgs a);  // E <= 128, CX tokens pe
 constexpr int GATE_CHAIN_STAGED_W = 512;               // chains per workgroup of gate_chain_staged_kernel
 template <int GT_M>
 __global__ void gate_tile2_kernel(GateArgs a);  // 32 < E <= 128; GT_M tokens per workgroup (64 or 128)
-template <int EPL>
-__global__ void gate_final_kernel(GateArgs a);  // EPL >= E / 16 experts per lane
+template <int EPL, bool COUNT>
+__global__ void gate_final_kernel(GateArgs a, TableArgs t);  // EPL >= E / 16 experts per lane; COUNT: also
+                                                             // tab_count_kernel's step on the chosen ids
 __global__ void tab_count_kernel(TableArgs a);
 __global__ void tab_scan_kernel(TableArgs a);
 __global__ void tab_perm_kernel(TableArgs a);

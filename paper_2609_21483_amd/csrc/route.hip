@@ -1062,54 +1062,83 @@ __global__ void __launch_bounds__(CH_W, 4) gate_chain_staged_kernel(GateArgs a) 
 template __global__ void gate_chain_staged_kernel<72, 3>(GateArgs);
 template __global__ void gate_chain_staged_kernel<136, 2>(GateArgs);
 
+// Counts the local selections of this block's tokens per local expert into
+// blk_cnt (one table block = NTH tokens) and the tokens with an invalid or
+// repeated id into blk_bad; ids: this thread's token's k ids (valid: g < T).
+__device__ __forceinline__ void count_block(const TableArgs& t, const int* ids, bool valid);
+
 // top-k of the candidates' defined logits (descending, equal logits ->
 // smaller id), one lane per token keeping a sorted list of the k best, then
 // the renormalised softmax weights of the chosen experts: exp(l_j - m) over
 // their sum (the normaliser over all experts cancels in the renormalisation,
-// so it is not formed)
-template <int EPL>
-__global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a) {
+// so it is not formed).  COUNT: the routing tables' first step on the ids
+// just chosen (the table blocks are these workgroups' tokens), as
+// tab_count_kernel would do it on topk_idx.
+template <int EPL, bool COUNT>
+__global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a, TableArgs tab) {
   const int g = blockIdx.x * NTH + threadIdx.x;
-  if (g >= a.T) return;
-  const int tb = a.tok_base[g], tn = a.tok_n[g];
+  const bool valid = g < a.T;
   float tv[MAX_TOPK];
   int ti[MAX_TOPK];
 #pragma unroll
   for (int j = 0; j < MAX_TOPK; ++j) { tv[j] = -INFINITY; ti[j] = 1 << 30; }
-  for (int c = 0; c < tn; ++c) {
-    float v = a.ch_l[tb + c];
-    int e = a.ch_e[tb + c];
+  if (valid) {
+    const int tb = a.tok_base[g], tn = a.tok_n[g];
+    // the candidates in batches of CB, every load of a batch in flight
+    // before the first insertion (list order, as one at a time)
+    constexpr int CB = 16;
+    for (int c0 = 0; c0 < tn; c0 += CB) {
+      float cv[CB];
+      int ce[CB];
 #pragma unroll
-    for (int j = 0; j < MAX_TOPK; ++j) {
-      if (better(v, e, tv[j], ti[j])) {
-        const float ov = tv[j];
-        const int oe = ti[j];
-        tv[j] = v;
-        ti[j] = e;
-        v = ov;
-        e = oe;
+      for (int i = 0; i < CB; ++i)
+        if (c0 + i < tn) {
+          cv[i] = a.ch_l[tb + c0 + i];
+          ce[i] = a.ch_e[tb + c0 + i];
+        }
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        if (c0 + i >= tn) break;
+        float v = cv[i];
+        int e = ce[i];
+#pragma unroll
+        for (int j = 0; j < MAX_TOPK; ++j) {
+          if (better(v, e, tv[j], ti[j])) {
+            const float ov = tv[j];
+            const int oe = ti[j];
+            tv[j] = v;
+            ti[j] = e;
+            v = ov;
+            e = oe;
+          }
+        }
       }
     }
+    const float m = tv[0];
+    float p[MAX_TOPK];
+    float ps = 0.0f;
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j)
+      if (j < a.k) { p[j] = expf(tv[j] - m); ps += p[j]; }
+#pragma unroll
+    for (int j = 0; j < MAX_TOPK; ++j)
+      if (j < a.k) {
+        a.topk_idx[(size_t)g * a.k + j] = ti[j];
+        a.topk_w[(size_t)g * a.k + j] = p[j] / ps;
+      }
   }
-  const float m = tv[0];
-  float p[MAX_TOPK];
-  float ps = 0.0f;
-#pragma unroll
-  for (int j = 0; j < MAX_TOPK; ++j)
-    if (j < a.k) { p[j] = expf(tv[j] - m); ps += p[j]; }
-#pragma unroll
-  for (int j = 0; j < MAX_TOPK; ++j)
-    if (j < a.k) {
-      a.topk_idx[(size_t)g * a.k + j] = ti[j];
-      a.topk_w[(size_t)g * a.k + j] = p[j] / ps;
-    }
+  if constexpr (COUNT) count_block(tab, ti, valid);
 }
 
-template __global__ void gate_final_kernel<1>(GateArgs);
-template __global__ void gate_final_kernel<2>(GateArgs);
-template __global__ void gate_final_kernel<4>(GateArgs);
-template __global__ void gate_final_kernel<8>(GateArgs);
-template __global__ void gate_final_kernel<32>(GateArgs);
+#define MOE_GATE_FINAL(EPL)                                                  \
+  template __global__ void gate_final_kernel<EPL, false>(GateArgs, TableArgs); \
+  template __global__ void gate_final_kernel<EPL, true>(GateArgs, TableArgs);
+MOE_GATE_FINAL(1)
+MOE_GATE_FINAL(2)
+MOE_GATE_FINAL(4)
+MOE_GATE_FINAL(8)
+MOE_GATE_FINAL(32)
+#undef MOE_GATE_FINAL
 
 // ---------------------------------------------------------------------------
 // Routing tables.  A pair (g, j) is local when id = topk_idx[g,j] is in
@@ -1126,18 +1155,15 @@ __device__ inline int local_expert(const TableArgs& a, const int* ids, int j, bo
   return (le >= 0 && le < a.El) ? le : -1;
 }
 
-__global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
+__device__ __forceinline__ void count_block(const TableArgs& a, const int* ids, bool valid) {
   __shared__ int hist[MAX_SEG];
   __shared__ int nbad;
   const int tid = threadIdx.x;
   for (int i = tid; i < a.El; i += NTH) hist[i] = 0;
   if (tid == 0) nbad = 0;
   __syncthreads();
-  const int g = blockIdx.x * TB + tid;
   bool bad = false;
-  if (g < a.T) {
-    int ids[MAX_TOPK];
-    for (int j = 0; j < a.k; ++j) ids[j] = a.topk_idx[(size_t)g * a.k + j];
+  if (valid) {
     for (int j = 0; j < a.k; ++j) {
       int le = local_expert(a, ids, j, &bad);
       if (le >= 0) atomicAdd(&hist[le], 1);
@@ -1150,6 +1176,15 @@ __global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
   __syncthreads();
   for (int i = tid; i < a.El; i += NTH) a.blk_cnt[(size_t)blockIdx.x * a.El + i] = hist[i];
   if (tid == 0) a.blk_bad[blockIdx.x] = nbad;
+}
+
+__global__ void __launch_bounds__(NTH) tab_count_kernel(TableArgs a) {
+  const int g = blockIdx.x * TB + threadIdx.x;
+  const bool valid = g < a.T;
+  int ids[MAX_TOPK];
+  if (valid)
+    for (int j = 0; j < a.k; ++j) ids[j] = a.topk_idx[(size_t)g * a.k + j];
+  count_block(a, ids, valid);
 }
 
 // Expert offsets and each table block's offset within every expert: one
