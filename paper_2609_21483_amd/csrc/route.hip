@@ -1096,7 +1096,6 @@ __global__ void __launch_bounds__(NTH) gate_final_kernel(GateArgs a, TableArgs t
           cv[i] = a.ch_l[tb + c0 + i];
           ce[i] = a.ch_e[tb + c0 + i];
         }
-#pragma unroll
       for (int i = 0; i < CB; ++i) {
         if (c0 + i >= tn) break;
         float v = cv[i];
