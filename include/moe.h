@@ -338,7 +338,11 @@ moe_status moe_forward(moe_handle* h, const uint16_t* x, const int32_t* topk_idx
  * l + 1's dispatch and first GEMM tiles overlap layer l's last tiles and its
  * combine; in every layer but the last, the final combine is left to that
  * layer's movement workers while the compute workers go on to the next
- * layer.  Results are those of moe_forward on each layer, bit for bit.
+ * layer.  In dynamic mode those movement workers first claim layer l + 1's
+ * dispatch units, beside layer l's GEMMs, when layer l + 1's prologue will
+ * take a plan known before it runs (forced, or stored with its tables under
+ * the current calibration).  Results are those of moe_forward on each layer,
+ * bit for bit.
  * mode: MOE_MODE_DYNAMIC or MOE_MODE_STATIC.  1 <= n_layers <= MOE_STACK_MAX,
  * no handle twice.  The timeline trace is not recorded in a stacked launch.
  * Errors: as moe_forward, per layer (device errors latch in each layer's
