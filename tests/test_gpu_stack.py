@@ -68,6 +68,41 @@ def test_stack_matches_single_launches_and_oracle(B, shape, n_layers, mode):
             ml.close()
 
 
+@pytest.mark.parametrize("plan", [(8, 2, 3, 1), (4, 4, 0, 0), "stale"], ids=["K2", "K4", "stale-calibration"])
+def test_stack_dispatch_ahead_plans(B, plan):
+    """A layer's movement workers dispatch the next layer ahead under that
+    layer's chunk count: forced plans with K = 2 and 4 (chunked readiness
+    counts), and a layer whose calibration changed after its tables were built
+    (its prologue evaluates the model again, so nothing is dispatched ahead for
+    it).  Each layer's y equals its own launch's, bit for bit."""
+    shape = W.FINE_ZIPF.with_(tokens_per_rank=512)
+    cases, layers, idx, w = build_stack(B, shape, 3)
+    try:
+        forced = None if plan == "stale" else B.moe_plan(*plan, 0.0)
+        if plan == "stale":
+            B.moe_set_calib(layers[1].h, B.moe_get_calib(layers[1].h))
+        x = cases[0][0].x.cuda()
+        singles = []
+        for l, ml in enumerate(layers):
+            y = torch.full((shape.T, shape.hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+            ml.forward(x, idx[l], w[l], y, "dynamic", forced=forced)
+            assert B.moe_sync_status(ml.h) == B.MOE_OK
+            singles.append(y)
+        if plan == "stale":  # the single launch stored nothing: the stack's layer 1 is still stale
+            B.moe_set_calib(layers[1].h, B.moe_get_calib(layers[1].h))
+        for rep in range(2):
+            ys = [torch.full((shape.T, shape.hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+                  for _ in layers]
+            B.moe_forward_stack([ml.h for ml in layers], x, idx, w, [ml.packed for ml in layers], ys,
+                                B.MOE_MODE_DYNAMIC, forced=forced)
+            for l, ml in enumerate(layers):
+                assert B.moe_sync_status(ml.h) == B.MOE_OK, (rep, l, B.moe_last_error())
+                assert torch.equal(ys[l].view(torch.int16), singles[l].view(torch.int16)), (rep, l)
+    finally:
+        for ml in layers:
+            ml.close()
+
+
 def test_large_stack_all_layers_in_one_launch(B):
     """The 8 layers of the large fine-grained stack in one launch: each layer's
     y equals its own launch's, bit for bit (each launch is checked against the
