@@ -62,6 +62,8 @@ def parse():
     ap.add_argument("--no-trace", action="store_true")
     ap.add_argument("--no-stack", action="store_true",
                     help="run the layers of a timed step as one launch per layer (default: one stacked launch)")
+    ap.add_argument("--route-streams", type=int, default=2,
+                    help="streams (default priority) the layers of a step are routed on; the layers are independent")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8, help="oracle rows per rank and layer, single-thread leg")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -440,17 +442,40 @@ def measure_stack(B, stack, args, stream, flush, trace: bool):
             for i in range(n):
                 stack.forward(i, "dynamic", stream)
 
-    for _ in range(args.warmup):
+    # the layers' routings are independent (each layer routes the same tokens
+    # with its own gate): with several streams, one layer's small table
+    # kernels and the last round of its chain kernel run beside the next
+    # layer's routing; the stream of the MoE launch waits for all of them
+    n_rs = max(1, min(args.route_streams, n))
+    side = [torch.cuda.Stream() for _ in range(n_rs)] if n_rs > 1 else []
+
+    def route_step():
+        if not side:
+            for i in range(n):
+                stack.route(i, stream)
+            return
+        fork = torch.cuda.Event()
+        fork.record(stream)
+        for sd in side:
+            sd.wait_event(fork)
         for i in range(n):
-            stack.route(i, stream)
+            stack.route(i, side[i % n_rs])
+        for sd in side:
+            join = torch.cuda.Event()
+            join.record(sd)
+            stream.wait_event(join)
+
+    for _ in range(args.warmup):
+        route_step()
         layers_forward()
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev_r = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        for i in range(n):
-            stack.route(i, stream)
+        ev_r[s].record(stream)
+        route_step()
         ev[s][0].record(stream)
         layers_forward()
         ev[s][1].record(stream)
@@ -458,6 +483,7 @@ def measure_stack(B, stack, args, stream, flush, trace: bool):
     wall = time.perf_counter() - t0
     stack.check(B, stream)
     moe_us = [a.elapsed_time(b) * 1e3 for a, b in ev]  # the MoE layers of a step (one launch or n)
+    step_route_us = [r.elapsed_time(a) * 1e3 for r, (a, _) in zip(ev_r, ev)]  # the routing of a step
     log(f"{stack.shape.name}: timed steps done ({wall * 1e3 / args.steps:.2f} ms per step)")
     plans = [B.moe_get_plan(d["layer"].h, stream) for d in stack.L]
     stats = [layer_stats(stack, i) for i in range(n)]
@@ -515,6 +541,8 @@ def measure_stack(B, stack, args, stream, flush, trace: bool):
         "moe_launches_per_step": 1 if stacked else n,
         "stack_flops": float(sum(flops)),
         "stack_route_us_total": float(sum(route_us)),
+        "route_streams": n_rs,
+        "route_us_per_step": float(np.median(step_route_us)),
         "one_launch_per_layer_us_total": tot,
         "dynamic_speedup_vs": {m: tot[m] / tot["dynamic"] for m in modes[1:]},
     }
@@ -552,6 +580,7 @@ def main():
     # the dominant kernel: the stacked megakernel (one launch holds every
     # layer), else the megakernel of the one layer
     launches = summary["moe_launches_per_step"]
+    rs_txt = f" (on {summary['route_streams']} streams)" if summary["route_streams"] > 1 else ""
     flops_per_launch = summary["stack_flops"] / launches
     achieved = flops_per_launch / (summary["moe_us_per_step"] / launches * 1e-6) / 1e12
     kernel = "moe_megakernel_stack" if launches == 1 and n > 1 else "moe_megakernel"
@@ -572,7 +601,7 @@ def main():
         "config": {"workload": f"{shape.name}: {n}-layer stack of EP=4 rank shares, E={shape.n_experts} "
                                f"k={shape.top_k} H={shape.hidden} F={shape.ffn}, {shape.n_local_experts} local "
                                f"experts, {shape.n_src_ranks} ranks x {shape.tokens_per_rank} tokens; a step is "
-                               f"the routing of every layer, then the MoE layers "
+                               f"the routing of every layer{rs_txt}, then the MoE layers "
                                f"({'in one stacked launch' if launches == 1 and n > 1 else 'one launch per layer'})",
                    "tokens": shape.T, "layers": ids},
         "stack": {**summary, "moe_tokens_per_s": shape.T / (summary["moe_us_per_step"] * 1e-6)},
