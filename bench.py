@@ -62,7 +62,7 @@ def parse():
     ap.add_argument("--no-trace", action="store_true")
     ap.add_argument("--no-stack", action="store_true",
                     help="run the layers of a timed step as one launch per layer (default: one stacked launch)")
-    ap.add_argument("--route-streams", type=int, default=2,
+    ap.add_argument("--route-streams", type=int, default=3,
                     help="streams (default priority) the layers of a step are routed on; the layers are independent")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8, help="oracle rows per rank and layer, single-thread leg")
