@@ -95,6 +95,38 @@ def test_route_parity(B, name, layer):
         hd.close()
 
 
+def test_route_layers_on_several_streams(B):
+    """Independent layers routed concurrently on three streams (as the bench
+    routes the layers of a step), each with its own handle: ids, weights and
+    routing tables are those of the oracle, as when routed one at a time."""
+    shape = W.FINE_ZIPF
+    layers = range(6)
+    cases = [make_case(shape, l, weights=False) for l in layers]
+    hds = [Handle(B, shape) for _ in layers]
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    try:
+        x = cases[0].x.cuda()
+        args = []
+        for c in cases:
+            idx = torch.full((shape.T, shape.top_k), -7, dtype=torch.int32, device="cuda")
+            w = torch.zeros((shape.T, shape.top_k), dtype=torch.float32, device="cuda")
+            args.append((c.wg.cuda(), None if c.bias is None else c.bias.cuda(), idx, w))
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for l, (hd, (wg, bias, idx, w)) in enumerate(zip(hds, args)):
+                B.moe_route(hd.h, x, wg, bias, shape.top_k, idx, w, stream=streams[l % 3])
+            torch.cuda.synchronize()
+            for l, (c, hd, (_, _, idx, w)) in enumerate(zip(cases, hds, args)):
+                assert B.moe_sync_status(hd.h) == B.MOE_OK, B.moe_last_error()
+                idx_ref, w_ref = c.oracle_route()
+                assert np.array_equal(idx.cpu().numpy(), idx_ref), (rep, l)
+                assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= 1e-6, (rep, l)
+                check_tables(hd, shape, idx_ref)
+    finally:
+        for hd in hds:
+            hd.close()
+
+
 @pytest.mark.parametrize("bias", [False, True])
 def test_route_ties_and_candidate_overflow(B, bias):
     """Exact ties and the exact fallback: zero token rows tie every expert
